@@ -1,0 +1,197 @@
+#!/usr/bin/env python3
+"""Throughput of the Adaptive SGD hot path on one MI355X.
+
+One step = one SGD step of one replica on one batch of the workload: the
+first-layer gather, the radix sort of the batch's feature and label ids, the
+output-layer forward (online softmax over all labels), the per-row combine
+(loss, dH1), the output-layer backward with the in-place W2/b2 update, the b1
+update and the sparse W1 update.  The dataset is staged in HBM before timing;
+batches are zero-copy row slices.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--workload wide-label|wide-feature|mid|tiny]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+METRIC = "training samples/sec at 1 GPU + % of HBM/MFMA roofline per kernel"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}
+H = 128
+
+
+def log(msg: str):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="wide-label")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
+                    help="budget of the oracle CPU baseline (0 disables it)")
+    return ap.parse_args()
+
+
+def kernel_model(w, B, nnz, lnnz, uniq):
+    """Algorithmic bytes and flops of one launch of each kernel group."""
+    F, L = w.n_features, w.n_labels
+    op = 2 if w.gemm_bf16 else 4
+    return {
+        # reads the touched W1 rows once, the batch's (id, value) pairs; writes A1 and H1 (2 layouts)
+        "gather": dict(bytes=uniq * H * 4 + nnz * 8 + B * H * (4 + 2 * op), flops=2.0 * nnz * H),
+        # two radix passes over (key, position) of every feature and label entry
+        "sort": dict(bytes=2 * (nnz + lnnz) * 4 * 5, flops=0.0),
+        # reads W2 and b2 once; Z = H1 W2^T and O = P W2 (the dense part of dH1)
+        "out_fwd": dict(bytes=4.0 * L * (H + 1), flops=4.0 * B * H * L),
+        "out_combine": dict(bytes=B * H * 4 * 2 + lnnz * H * 4, flops=2.0 * lnnz * H),
+        "hidden": dict(bytes=B * H * 4, flops=B * H),
+        # reads and writes W2 and b2 once; dW2 = dZ^T H1 (the Z recompute is not counted)
+        "out_bwd": dict(bytes=8.0 * L * (H + 1), flops=2.0 * B * H * L),
+        # reads and writes the touched W1 rows once
+        "w1_update": dict(bytes=uniq * H * 8 + nnz * 12, flops=2.0 * nnz * H),
+    }
+
+
+def cpu_baseline(w, ds, B, budget_s):
+    """The oracle as it stands, timed on this host on a bounded sample of the workload."""
+    from oracle import model as om
+    p = om.init_params(w.n_features, w.n_labels, H, w.init_seed)
+    ops = "bf16" if w.gemm_bf16 else "fp32"
+    n_steps, samples = 0, 0
+    t0 = time.perf_counter()
+    r0 = 0
+    while True:
+        r1 = min(r0 + B, ds.x.n_rows)
+        p, *_ = om.train_step(p, ds.x.rows(r0, r1), ds.y.rows(r0, r1), w.lr, ops)
+        n_steps += 1
+        samples += r1 - r0
+        r0 = r1 % ds.x.n_rows
+        el = time.perf_counter() - t0
+        log(f"oracle step {n_steps}: {el:.1f} s")
+        if el >= budget_s or n_steps >= 64:
+            break
+    try:  # threads of the BLAS the oracle's products ran on (loaded by now)
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        cores = os.cpu_count() or 1
+    return {"value": samples / el, "unit": "samples/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{n_steps} oracle steps x {B} rows of {w.name} ({samples} samples, {el:.1f} s)"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: every run in this build uses a single MI355X "
+              f"(got --gpus {args.gpus}); the multi-GPU merge is a design, not a measured path.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    import paper_2110_07029_amd as asgd
+    from paper_2110_07029_amd import synth
+
+    asgd.load()
+    w = synth.WORKLOADS[args.workload]
+    B = w.batch
+    K, W = args.steps, args.warmup
+    n_samples = min(w.n_samples, (K + W) * B)
+    log(f"workload {w.name}: F={w.n_features} L={w.n_labels} B={B}; generating {n_samples} samples")
+    ds = synth.generate(w, n_samples=n_samples)
+    n_full = ds.x.n_rows // B
+    bounds = [(i * B, (i + 1) * B) for i in range(n_full)]
+    ipx, ipy = np.asarray(ds.x.indptr), np.asarray(ds.y.indptr)
+    nnz = [int(ipx[b] - ipx[a]) for a, b in bounds]
+    lnnz = [int(ipy[b] - ipy[a]) for a, b in bounds]
+    dx, dy = asgd.DeviceCSR(ds.x), asgd.DeviceCSR(ds.y)
+    xs = [dx.batch(a, b) for a, b in bounds]
+    ys = [dy.batch(a, b) for a, b in bounds]
+    stream = torch.cuda.current_stream()
+    m = asgd.asgd_model_init(w.n_features, w.n_labels, B, max(nnz), max(lnnz), gemm_bf16=w.gemm_bf16,
+                             seed=w.init_seed, stream=stream)
+    try:
+        lr = w.lr
+        for i in range(W):
+            asgd.asgd_train_step(m, xs[i % n_full], ys[i % n_full], lr)
+        torch.cuda.synchronize()
+        log(f"warmup done ({W} steps)")
+        asgd.asgd_model_set_timing(m, True)
+        for k in range(len(asgd.KERNELS)):
+            asgd.asgd_model_get_timing(m, k)
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t_start.record(stream)
+        used = []
+        for i in range(K):
+            j = (W + i) % n_full
+            used.append(j)
+            asgd.asgd_train_step(m, xs[j], ys[j], lr)
+        t_end.record(stream)
+        torch.cuda.synchronize()
+        ms = t_start.elapsed_time(t_end)
+        loss = asgd.asgd_model_last_loss(m)
+        log(f"timed {K} steps: {ms:.2f} ms, last loss {loss:.4f}")
+        kt = {}
+        for k, name in enumerate(asgd.KERNELS):
+            tot, n = asgd.asgd_model_get_timing(m, k)
+            if n:
+                kt[name] = (tot, n)
+    finally:
+        asgd.asgd_model_free(m)
+
+    samples = K * B
+    value = samples / (ms / 1e3)
+    mean_nnz = float(np.mean([nnz[j] for j in used]))
+    mean_lnnz = float(np.mean([lnnz[j] for j in used]))
+    uniq = float(np.mean([len(np.unique(ds.x.indices[ipx[bounds[j][0]]:ipx[bounds[j][1]]]))
+                          for j in used[:32]]))
+    model = kernel_model(w, B, mean_nnz, mean_lnnz, uniq)
+    dtype = "bf16" if w.gemm_bf16 else "fp32"
+    kernels = {}
+    for name, (tot, n) in kt.items():
+        avg = tot / n
+        km = model.get(name, dict(bytes=0.0, flops=0.0))
+        gbs = km["bytes"] / (avg * 1e-3) / 1e9
+        tfs = km["flops"] / (avg * 1e-3) / 1e12
+        kernels[name] = {"avg_us": round(avg * 1e3, 2), "launches": n,
+                         "alg_bytes": km["bytes"], "alg_flops": km["flops"],
+                         "GB/s": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+                         "TFLOP/s": round(tfs, 2), "mfma_frac": round(tfs / MFMA_PEAK_TFLOPS[dtype], 4),
+                         "share_of_step": round(tot / ms, 4)}
+    dom = max(kt, key=lambda k: kt[k][0])
+    d = kernels[dom]
+    roofline = {"kernel": dom, "bound": "hbm", "achieved": d["GB/s"], "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": d["hbm_frac"], "traffic": None}
+    cpu = None
+    if args.cpu_seconds > 0:
+        log(f"oracle CPU baseline, ~{args.cpu_seconds:.0f} s budget")
+        cpu = cpu_baseline(w, ds, B, args.cpu_seconds)
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "samples/s", "n_gpus": 1, "steps": K,
+        "warmup": W, "ms_per_step": round(ms / K, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": dtype, "data": "synthetic",
+        "config": {"workload": w.name, "n_features": w.n_features, "n_labels": w.n_labels,
+                   "hidden": H, "batch": B, "global_batch": B, "mean_nnz_per_batch": round(mean_nnz, 1),
+                   "mean_labels_per_batch": round(mean_lnnz, 1), "master_weights": "fp32",
+                   "parallelism": "single replica"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,254 @@
+/*
+ * asgd.h - C ABI of the MI355X (gfx950) hot path of Adaptive SGD
+ * (Ma, Rusu, Wu, Sim: "Adaptive Elastic Training for Sparse Deep Learning on
+ * Heterogeneous Multi-GPU Servers", arXiv 2110.07029).
+ *
+ * The library trains replicas of the paper's sparse extreme-multi-label MLP
+ * (Sec. 5.1 "Datasets and Model": sparse input layer, one ReLU hidden layer,
+ * softmax + cross-entropy output layer) with mini-batch SGD (Sec. 2.1), and
+ * merges replicas with the normalized, momentum-corrected model merge of
+ * Alg. 2 (Sec. 3.3).  Batch-size scaling (Alg. 1, Sec. 3.2) and the merge
+ * weights run on the host.
+ *
+ * Model:  A1 = X W1 + b1 ; H1 = ReLU(A1) ; Z = H1 W2^T + b2
+ *         loss = mean_i [ logsumexp_j Z_ij - (1/|Y_i|) sum_{y in Y_i} Z_iy ]
+ *         (target distribution 1/|Y_i| on each true label; mean over the batch)
+ * Shapes: W1 [F x H] row-major, b1 [H], W2 [L x H] row-major (label-major),
+ *         b2 [L]; H = 128.  Parameters are float32.
+ *
+ * Conventions shared by every entry point
+ *  - Every call returns an asgd_status and never throws or aborts.  On a
+ *    non-OK status asgd_last_error() gives a message (thread-local).
+ *  - Argument and shape errors (EINVAL / ERANGE) are detected on the host
+ *    before anything is enqueued; the model is then unchanged.
+ *  - EHIP: a HIP runtime call failed; the model's device state is undefined
+ *    and the model should be freed.
+ *  - Device pointers (CSR arrays, outputs) are owned by the caller and are
+ *    only borrowed for the call; they must stay valid until the model's
+ *    stream has executed the enqueued work.
+ *  - Work is enqueued on the model's HIP stream (hipStream_t passed as
+ *    void*; NULL = the default stream).  Calls return before the GPU work
+ *    finishes unless stated otherwise.
+ *  - A model must not be used from two host threads at once.
+ *  - Every kernel bounds-checks feature and label ids and never reads the
+ *    caller's index/value arrays outside [indptr[0], indptr[0] + nnz).
+ *    Ids out of range are skipped on the device and raise the model's
+ *    device error flag; with ASGD_VALIDATE the call then returns EINVAL.
+ */
+#ifndef ASGD_H
+#define ASGD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct asgd_model asgd_model; /* opaque, created and freed only by the library */
+
+typedef enum asgd_status {
+  ASGD_OK = 0,
+  ASGD_EINVAL = -1, /* invalid argument or malformed CSR content */
+  ASGD_ERANGE = -2, /* size beyond what the model was provisioned for */
+  ASGD_ENOMEM = -3, /* device or host allocation failed */
+  ASGD_EHIP = -4,   /* HIP runtime error */
+  ASGD_ESTATE = -5  /* call not valid in the object's current state */
+} asgd_status;
+
+/* asgd_config.flags */
+#define ASGD_VALIDATE 0x1u /* check CSR content on the device and synchronize each step */
+
+typedef struct asgd_config {
+  int32_t n_features;    /* F >= 1 */
+  int32_t n_labels;      /* L >= 1 */
+  int32_t hidden;        /* H; must be 128 */
+  int32_t max_batch;     /* largest B any call will use (memory pool sized for it, Sec. 4) */
+  int32_t max_nnz;       /* largest sum of nnz over the rows of one batch */
+  int32_t max_label_nnz; /* largest sum of |Y_i| over the rows of one batch */
+  int32_t gemm_bf16;     /* 1: output-layer products on bf16 operands with fp32 accumulation
+                            (fp32 master weights); 0: fp32 operands */
+  uint32_t flags;        /* ASGD_VALIDATE or 0 */
+} asgd_config;
+
+/* A CSR row block living in device memory.  Row i spans entries
+ * [indptr[i], indptr[i+1]) of indices/values (absolute offsets, so a batch
+ * can be a zero-copy row slice of a larger device-resident dataset whose
+ * indptr[0] is not 0).  nnz is the host's copy of indptr[n_rows] - indptr[0].
+ * Feature rows must have distinct ids per row; label rows must be non-empty
+ * with distinct ids.  values is NULL for label matrices. */
+typedef struct asgd_csr {
+  int32_t n_rows;         /* B */
+  int32_t n_cols;         /* F for features, L for labels */
+  int32_t nnz;            /* entries in the block */
+  const int32_t* indptr;  /* device, [n_rows + 1] */
+  const int32_t* indices; /* device */
+  const float* values;    /* device, or NULL for labels */
+} asgd_csr;
+
+/* Parameter selectors for get/set. */
+enum {
+  ASGD_PARAM_W1 = 0,
+  ASGD_PARAM_B1 = 1,
+  ASGD_PARAM_W2 = 2,
+  ASGD_PARAM_B2 = 3
+};
+
+/* Merge-weight modes (Alg. 2). */
+enum {
+  ASGD_WEIGHTS_ALG2 = 0,   /* by batch size if all u_i are equal, else by update count */
+  ASGD_WEIGHTS_SAMPLES = 1 /* by samples processed (the alternative named in Sec. 3.3) */
+};
+
+/* ------------------------------------------------------------------------ */
+/* Model lifetime                                                            */
+/* ------------------------------------------------------------------------ */
+
+/* Create a model and its workspace (Sec. 4 "Scalable Memory Management":
+ * everything is allocated once, for the largest batch).  W1 and W2 are
+ * Xavier-uniform with half-width a = fl32(sqrt(6/(fan_in+fan_out))), fans
+ * (F,H) and (H,L); element e of tensor t (0 = W1, 1 = W2, row-major) is
+ * fl32(fl32(2u-1) * a) with u = (splitmix64(seed ^ (t << 56) ^ e) >> 40) * 2^-24,
+ * splitmix64 being the published generator's output for that state.  Biases
+ * start at 0.  Initialisation runs on `hip_stream`; the call returns once it
+ * has completed.  *out receives the model; nothing is allocated on error. */
+asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t seed,
+                            void* hip_stream);
+
+/* Free the model (synchronizes its stream first).  NULL is accepted. */
+asgd_status asgd_model_free(asgd_model* m);
+
+/* Move the model to another HIP stream (subsequent work is enqueued there;
+ * the new stream first waits for work already enqueued on the old one). */
+asgd_status asgd_model_set_stream(asgd_model* m, void* hip_stream);
+
+/* Copy all parameters of src into dst (same F, L, H).  Enqueued on dst's
+ * stream after src's pending work. */
+asgd_status asgd_model_copy(asgd_model* dst, const asgd_model* src);
+
+/* Number of parameters P = F*H + H + L*H + L. */
+asgd_status asgd_model_num_params(const asgd_model* m, int64_t* out);
+
+/* Copy one parameter tensor to / from host memory (synchronous).  `bytes`
+ * must equal the tensor's size in bytes (F*H*4, H*4, L*H*4 or L*4). */
+asgd_status asgd_model_get_params(const asgd_model* m, int32_t which, void* host, size_t bytes);
+asgd_status asgd_model_set_params(asgd_model* m, int32_t which, const void* host, size_t bytes);
+
+/* ------------------------------------------------------------------------ */
+/* The per-replica step (Sec. 2.1: forward, backward, update)                */
+/* ------------------------------------------------------------------------ */
+
+/* One SGD step on the batch (x, y), B = x->n_rows = y->n_rows, 1 <= B <= max_batch:
+ * gradients of the mean loss, then theta <- theta - lr * g for W2, b2, b1 and
+ * for the rows of W1 whose feature occurs in the batch; other W1 rows are
+ * not written.  If loss_out is non-NULL the call synchronizes the stream and
+ * stores the batch's mean loss (computed before the update); with NULL the
+ * call is fully asynchronous and the loss stays readable with
+ * asgd_model_last_loss(). */
+asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y, float lr,
+                            float* loss_out);
+
+/* Mean loss of the most recent train step (synchronizes the stream). */
+asgd_status asgd_model_last_loss(asgd_model* m, float* loss_out);
+
+/* Top-k labels per row of x by logit Z (ties: smaller label id first), the
+ * prediction used for the paper's top-1 accuracy (Sec. 5.1 "Methodology").
+ * ids_dev: device int32 [B x k]; scores_dev: device float [B x k] or NULL.
+ * 1 <= k <= 32 and k <= L.  Asynchronous. */
+asgd_status asgd_predict_topk(asgd_model* m, const asgd_csr* x, int32_t k, int32_t* ids_dev,
+                              float* scores_dev);
+
+/* ------------------------------------------------------------------------ */
+/* Normalized model merging (Alg. 2) and batch-size scaling (Alg. 1)         */
+/* ------------------------------------------------------------------------ */
+
+/* The merge step of Alg. 2:  w' = sum_i alpha_i w_i + gamma (w - w_prev);
+ * then w_prev <- w and w <- w'.  `global` holds w, `prev_global` holds
+ * w_prev (NULL = no momentum term and no history), `replicas[0..n-1]` the
+ * w_i, `weights` (host, [n]) the alpha_i.  Sums are formed in float64 per
+ * element and rounded once to float32.  All models must share F, L, H;
+ * 1 <= n <= 16; replicas may include neither global nor prev_global.
+ * broadcast != 0 also writes w' into every replica (replicas restart from the
+ * merged model, Sec. 4).  Enqueued on global's stream after the pending work
+ * of every participant; the replicas' and prev_global's streams then wait for
+ * the merge.  With prev_global, the two models exchange parameter buffers. */
+asgd_status asgd_merge(asgd_model* global, asgd_model* prev_global, asgd_model* const* replicas,
+                       const float* weights, int32_t n, float gamma, int32_t broadcast);
+
+/* L2 norm of all parameters of a model divided by the parameter count
+ * (Alg. 2's regularization gate "||w_i||_2 / |w|").  Synchronous. */
+asgd_status asgd_model_l2_per_param(asgd_model* m, double* out);
+
+/* Alg. 2 weight computation (host only).  u: updates per replica since the
+ * last merge; b: batch sizes; samples: samples processed (used by
+ * ASGD_WEIGHTS_SAMPLES, may be NULL otherwise).  l2_per_param: per-replica
+ * ||w_i||_2/|w| or NULL to disable the perturbation; when every value is
+ * < pert_thr and n > 1, alpha_r *= 1 + delta and alpha_s *= 1 - delta for the
+ * replica r with the most updates (then largest batch, then lowest index)
+ * and s with the fewest (then smallest batch, then highest index).
+ * alpha_out: host [n], float32 rounding of the float64 weights. */
+asgd_status asgd_merge_weights(int32_t n, const int32_t* u, const int32_t* b,
+                               const int64_t* samples, int32_t mode, const double* l2_per_param,
+                               double pert_thr, double delta, float* alpha_out);
+
+/* Alg. 1 batch-size scaling (host only), in place on b and lr.  With
+ * mu = sum(u)/n: if u_i > mu and b_i + beta (u_i - mu) <= b_max the batch grows,
+ * if u_i < mu and b_i - beta (mu - u_i) >= b_min it shrinks, otherwise it is
+ * left alone (no clamping).  The new size is the exact value rounded to the
+ * nearest integer (halves away from zero); lr_i <- fl32(lr_i * b_new / b_old). */
+asgd_status asgd_scale_batches(int32_t n, const int32_t* u, int32_t* b, float* lr, int32_t b_min,
+                               int32_t b_max, double beta);
+
+/* ------------------------------------------------------------------------ */
+/* Inspection of intermediates (parity tests)                                */
+/* ------------------------------------------------------------------------ */
+
+/* Forward pass only (no update): a1_dev [B x H] pre-activation, lse_dev [B]
+ * log-sum-exp of the logits, loss_rows_dev [B] per-row loss (needs y; may be
+ * NULL together with y).  Device outputs, asynchronous. */
+asgd_status asgd_debug_forward(asgd_model* m, const asgd_csr* x, const asgd_csr* y, float* a1_dev,
+                               float* lse_dev, float* loss_rows_dev);
+
+/* Sorted distinct feature ids of the batch (the W1 rows a step writes), as
+ * computed by the step's sort-by-feature pass.  ids_dev: device [>= nnz];
+ * *count_host receives the count.  Synchronous. */
+asgd_status asgd_debug_touched_rows(asgd_model* m, const asgd_csr* x, int32_t* ids_dev,
+                                    int32_t* count_host);
+
+/* ------------------------------------------------------------------------ */
+/* Kernel timing (HIP events on the model's stream)                          */
+/* ------------------------------------------------------------------------ */
+
+/* Kernel groups that can be timed. */
+enum {
+  ASGD_K_GATHER = 0,      /* first-layer gather + sort keys */
+  ASGD_K_SORT = 1,        /* all radix-sort passes of one step */
+  ASGD_K_OUT_FWD = 2,     /* output-layer forward over all labels */
+  ASGD_K_OUT_COMBINE = 3, /* per-row merge of label splits, loss, dA1 */
+  ASGD_K_HIDDEN = 4,      /* b1 gradient / update and mean loss */
+  ASGD_K_OUT_BWD = 5,     /* output-layer backward + W2/b2 update */
+  ASGD_K_W1_UPDATE = 6,   /* sparse W1 gradient + update */
+  ASGD_K_MERGE = 7,       /* normalized merge (timed on the global model) */
+  ASGD_K_COUNT = 8
+};
+
+/* enable != 0: from now on, bracket each kernel group launched for this model
+ * with a pair of HIP events (up to 1024 launches per group are recorded
+ * between two reads; later launches of that group run untimed).  enable == 0
+ * stops recording.  Timing adds two event records per group launch. */
+asgd_status asgd_model_set_timing(asgd_model* m, int32_t enable);
+
+/* Sum of the event-measured durations (ms) and the number of timed launches
+ * of `kernel` since the last read; resets that group's record.  Waits for the
+ * recorded events. */
+asgd_status asgd_model_get_timing(asgd_model* m, int32_t kernel, double* total_ms,
+                                  int64_t* launches);
+
+/* Message describing the last non-OK status returned on this thread. */
+const char* asgd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ASGD_H */

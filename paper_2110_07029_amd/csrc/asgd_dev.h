@@ -1,0 +1,118 @@
+// Device-side building blocks shared by the gfx950 kernels.
+//
+// Matrix-core conventions (CDNA4, wave64):
+//   v_mfma_f32_32x32x16_bf16 : D[32x32] += A[32x16] * B[16x32], 8 bf16 per lane
+//   v_mfma_f32_32x32x2_f32   : D[32x32] += A[32x2]  * B[2x32],  1 fp32 per lane
+// Lane l = 32*g + i (g = l/32).  A lanes own row m = i, B lanes own column
+// n = i; the accumulator register r of lane l holds D[8*(r/4) + 4*g + r%4][i].
+// Any permutation of the K index is allowed as long as A and B agree.  All
+// kernels here use the "accumulator-compatible" K order: inside every block
+// of 32 K values, element j of chunk c of lane group g is
+//     k = 8*(r/4) + 4*g + r%4 with r = c*KL + j      (KL = values per lane).
+// With that order the fp32 accumulators of one product can be fed directly as
+// the K-operand of the next product (no register shuffles), and a lane that
+// loads the 32 weights it multiplies also owns exactly the gradient entries
+// those weights receive.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "asgd_kernels.h"
+
+namespace asgd {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+template <bool BF16>
+struct Mma;
+
+template <>
+struct Mma<true> {
+  static constexpr int KC = 16;  // K per instruction
+  static constexpr int KL = 8;   // K values per lane
+  using frag = bf16x8;
+  using elem = bf16;
+  __device__ static inline f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <>
+struct Mma<false> {
+  static constexpr int KC = 2;
+  static constexpr int KL = 1;
+  using frag = float;
+  using elem = float;
+  __device__ static inline f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+};
+
+// Offset inside a 32-wide K block of element j of chunk c for lane group g.
+template <bool BF16>
+__device__ __forceinline__ int kofs(int c, int g, int j) {
+  const int r = c * Mma<BF16>::KL + j;
+  return 8 * (r >> 2) + 4 * g + (r & 3);
+}
+
+// Fragment of chunk c (inside the 32-block starting at `p`) from a row whose
+// K values are contiguous in memory (global or LDS).
+__device__ __forceinline__ bf16x8 frag_row_bf16(const bf16* p, int c, int g) {
+  const bf16x4 lo = *reinterpret_cast<const bf16x4*>(p + 16 * c + 4 * g);
+  const bf16x4 hi = *reinterpret_cast<const bf16x4*>(p + 16 * c + 8 + 4 * g);
+  bf16x8 f;
+  f[0] = lo[0]; f[1] = lo[1]; f[2] = lo[2]; f[3] = lo[3];
+  f[4] = hi[0]; f[5] = hi[1]; f[6] = hi[2]; f[7] = hi[3];
+  return f;
+}
+
+__device__ __forceinline__ float frag_row_f32(const float* p, int c, int g) {
+  return p[8 * (c >> 2) + 4 * g + (c & 3)];
+}
+
+// Fragment of chunk c built from accumulator registers (K = the accumulator's
+// row index, 32 per block): values r = c*KL + j.
+__device__ __forceinline__ bf16x8 frag_acc_bf16(const float* v, int c) {
+  bf16x8 f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = (bf16)v[8 * c + j];
+  return f;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+constexpr float LOG2E = 1.4426950408889634f;
+
+// e^x through the hardware base-2 exponential.
+__device__ __forceinline__ float exp_fast(float x) { return __builtin_amdgcn_exp2f(x * LOG2E); }
+
+// Device error flags (bitwise OR into the model's flag word).
+enum : int {
+  ERR_FEATURE_ID = 1,   // feature id outside [0, F)
+  ERR_LABEL_ID = 2,     // label id outside [0, L)
+  ERR_INDPTR = 4,       // row extent decreasing or outside [indptr[0], indptr[0] + nnz)
+  ERR_DUPLICATE = 8,    // ids of a row not strictly increasing
+  ERR_EMPTY_LABELS = 16 // a label row without labels
+};
+
+}  // namespace asgd

@@ -1,0 +1,99 @@
+// Host-side launchers of the gfx950 kernels.  Every launcher enqueues on
+// `st` and returns the launch status; no launcher allocates memory.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace asgd {
+
+constexpr int HID = 128;  // hidden width H
+
+// Batch view as the kernels see it (device pointers; base = indptr[0] value
+// is read on the device).
+struct CsrDev {
+  int n_rows, n_cols, nnz;
+  const int32_t* indptr;
+  const int32_t* indices;
+  const float* values;
+};
+
+// ---- initialisation -------------------------------------------------------
+hipError_t launch_init_uniform(float* w, int64_t count, uint64_t key, float bound, hipStream_t st);
+hipError_t launch_fill_int(int32_t* p, int32_t v, int64_t n, hipStream_t st);
+
+// ---- first layer forward + sort keys ---------------------------------------
+// A1 = X W1 + b1 (fp32), H1 = ReLU(A1) as the output layer's operand type in
+// row-major [rows_pad x 128] and transposed [128 x ld_t]; rows in [B, rows_pad)
+// are zero.  With y != NULL also writes the label sort keys.  Keys: feature
+// entry p (0 <= p < x.nnz) -> key[p] = feature id; label entry q -> key[x.nnz + q]
+// = F + label id; invalid ids get key F + L.  row_of[p] / lrow[q] = row index,
+// rw[i] = 1/|Y_i|.
+hipError_t launch_gather_fwd(bool use_bf16, const CsrDev& x, const CsrDev* y, const float* W1,
+                             const float* b1, int F, int L, float* A1, void* H1, void* H1T,
+                             int rows_pad, int ld_t, int32_t* keys, int32_t* row_of,
+                             int32_t* lrow, float* rw, int32_t* err, int validate, hipStream_t st);
+
+// ---- stable LSD radix sort of (key, position) -----------------------------
+constexpr int SORT_CHUNK = 2048;   // keys per workgroup
+constexpr int SORT_MAX_BITS = 11;  // digit width limit per pass
+int sort_blocks(int n);
+// Sorts keys[0..n) (values < 2^key_bits) stably; the payload is the original
+// position.  Result in keys_out / vals_out.  tmp buffers of n entries, hist
+// and offs of sort_blocks(n) << SORT_MAX_BITS entries.
+hipError_t launch_sort(const int32_t* keys_in, int n, int key_bits, int32_t* keys_a,
+                       int32_t* vals_a, int32_t* keys_b, int32_t* vals_b, int32_t* hist,
+                       const int32_t** keys_out, const int32_t** vals_out, hipStream_t st);
+
+// ---- output layer -----------------------------------------------------------
+constexpr int OUT_TILE = 32;  // labels per forward tile
+int out_rows_per_block(bool use_bf16);
+// Forward over label splits: per (split, row) running max, sum of exponentials
+// and sum_l exp(Z - m) W2[l] (flash-style); grid = splits x row blocks.
+hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2, int L, const void* H1,
+                                int B, int splits, float* m_part, float* s_part, float* o_part,
+                                int ld_part, hipStream_t st);
+// Per row: lse, loss_i, dA1 (see kernel); y may be NULL (lse only).
+hipError_t launch_out_combine(bool use_bf16, int B, int splits, const float* m_part,
+                              const float* s_part, const float* o_part, int ld_part,
+                              const float* W2, const float* b2, int L, const void* H1,
+                              const float* A1, const CsrDev* y, float* lse, float* loss_rows,
+                              float* dA1, hipStream_t st);
+// db1 = sum_i dA1[i]; b1 -= lr db1; loss = mean_i loss_rows[i].
+hipError_t launch_hidden_bias(int B, const float* dA1, float* b1, float lr, const float* loss_rows,
+                              float* loss, hipStream_t st);
+// Recompute Z per label tile, dZ = (softmax - T)/B, dW2 = dZ^T H1, db2; update W2, b2 in place.
+hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, int F, const void* H1,
+                          const void* H1T, int ld_t, int B, const float* lse, const float* rw,
+                          const int32_t* skeys, const int32_t* svals, int n_keys, int label_base,
+                          const int32_t* lrow, float lr, hipStream_t st);
+// W1[f] -= lr * sum_{entries of f} x * dA1[row], one segment per distinct f.
+hipError_t launch_w1_update(float* W1, int F, const int32_t* skeys, const int32_t* svals,
+                            int n_feat_keys, const int32_t* row_of, const CsrDev& x,
+                            const float* dA1, float lr, hipStream_t st);
+// Distinct sorted feature ids (compaction of segment heads); count to *count_dev.
+hipError_t launch_touched(const int32_t* skeys, int n_keys, int F, int32_t* ids, int32_t* count_dev,
+                          hipStream_t st);
+
+// ---- prediction ---------------------------------------------------------------
+int topk_splits(int B, int n_tiles);
+hipError_t launch_out_fwd_topk(bool use_bf16, const float* W2, const float* b2, int L, const void* H1,
+                               int B, int splits, int k, float* part_s, int32_t* part_i,
+                               int ld_part, hipStream_t st);
+hipError_t launch_topk_combine(int B, int splits, int k, const float* part_s,
+                               const int32_t* part_i, int ld_part, int32_t* ids, float* scores,
+                               hipStream_t st);
+
+// ---- merge ---------------------------------------------------------------------
+constexpr int MERGE_MAX = 16;
+// out[e] = sum_i a[i] rep_i[e] + gamma (g[e] - gp[e]) in float64, rounded once;
+// out may alias gp.  bcast[i] (nullable array) receives out as well.
+hipError_t launch_merge(float* out, const float* g, const float* gp, const float* const* reps,
+                        const double* alpha, int n, double gamma, float* const* bcast, int nb,
+                        int64_t count, hipStream_t st);
+// Deterministic sum of squares (float64) of w[0..count) into *out (device).
+hipError_t launch_sqnorm(const float* w, int64_t count, double* partial, double* out,
+                         hipStream_t st);
+constexpr int SQNORM_BLOCKS = 1024;
+
+}  // namespace asgd

@@ -1,0 +1,184 @@
+// First layer: CSR batch times W1 as coalesced row gathers (sparse input layer
+// of the paper's MLP, Sec. 5.1), plus the per-entry sort keys used by the
+// backward pass and the model initialisation.
+#include "asgd_dev.h"
+#include "asgd_kernels.h"
+
+namespace asgd {
+
+// ---------------------------------------------------------------------------
+// Xavier-uniform init from the counter-based splitmix64 stream.
+// ---------------------------------------------------------------------------
+__global__ void k_init_uniform(float* __restrict__ w, int64_t count, uint64_t key, float bound) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < count; e += stride) {
+    uint64_t z = (uint64_t)e ^ key;
+    z += 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    z ^= z >> 31;
+    const float u = (float)(uint32_t)(z >> 40) * 0x1p-24f;  // exact: 24-bit grid
+    const float t = 2.0f * u - 1.0f;                          // exact in float32
+    w[e] = t * bound;                                         // the only rounding
+  }
+}
+
+hipError_t launch_init_uniform(float* w, int64_t count, uint64_t key, float bound, hipStream_t st) {
+  if (count <= 0) return hipSuccess;
+  int64_t blocks = (count + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(k_init_uniform, dim3((unsigned)blocks), dim3(256), 0, st, w, count, key, bound);
+  return hipGetLastError();
+}
+
+__global__ void k_fill_int(int32_t* p, int32_t v, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += stride) p[e] = v;
+}
+
+hipError_t launch_fill_int(int32_t* p, int32_t v, int64_t n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_fill_int, dim3((unsigned)blocks), dim3(256), 0, st, p, v, n);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// A1[i] = b1 + sum_{(f, v) in row i} v * W1[f];  H1 = max(A1, 0).
+// One wavefront per sample row; lane l owns hidden units 2l and 2l+1, so every
+// W1 row is read as one coalesced 512-byte access.  The row's (id, value)
+// pairs are loaded 64 at a time (one per lane) and broadcast with readlane.
+// ---------------------------------------------------------------------------
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_gather_fwd(
+    CsrDev x, CsrDev y, int has_y, const float* __restrict__ W1, const float* __restrict__ b1,
+    int F, int L, float* __restrict__ A1, typename Mma<BF16>::elem* __restrict__ H1,
+    typename Mma<BF16>::elem* __restrict__ H1T, int rows_pad, int ld_t, int32_t* __restrict__ keys,
+    int32_t* __restrict__ row_of, int32_t* __restrict__ lrow, float* __restrict__ rw,
+    int32_t* __restrict__ err, int validate) {
+  using E = typename Mma<BF16>::elem;
+  const int lane = threadIdx.x & 63;
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= rows_pad) return;
+  const int h0 = 2 * lane;
+  if (i >= x.n_rows) {  // padding rows of the output-layer operands are zero
+    H1[(size_t)i * HID + h0] = (E)0.0f;
+    H1[(size_t)i * HID + h0 + 1] = (E)0.0f;
+    H1T[(size_t)h0 * ld_t + i] = (E)0.0f;
+    H1T[(size_t)(h0 + 1) * ld_t + i] = (E)0.0f;
+    return;
+  }
+  int bad = 0;
+  const int base = x.indptr[0];
+  int s = x.indptr[i], e = x.indptr[i + 1];
+  if (s < base || e > base + x.nnz || e < s) {
+    bad |= ERR_INDPTR;
+    s = max(s, base);
+    e = min(e, base + x.nnz);
+    if (e < s) e = s;
+  }
+  float2 acc = *reinterpret_cast<const float2*>(b1 + h0);
+  for (int p0 = s; p0 < e; p0 += 64) {
+    const int p = p0 + lane;
+    int f = -1;
+    float v = 0.0f;
+    if (p < e) {
+      f = x.indices[p];
+      v = x.values[p];
+      int key = f;
+      if (f < 0 || f >= F) {
+        bad |= ERR_FEATURE_ID;
+        key = F + L;
+        f = -1;
+      } else if (validate && p > s && x.indices[p - 1] >= f) {
+        bad |= ERR_DUPLICATE;
+      }
+      keys[p - base] = key;
+      row_of[p - base] = i;
+    }
+    const int cnt = min(64, e - p0);
+    int j = 0;
+    for (; j + 4 <= cnt; j += 4) {
+      int fj[4];
+      float vj[4];
+      float2 w[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        fj[u] = __builtin_amdgcn_readlane(f, j + u);
+        vj[u] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), j + u));
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        w[u] = fj[u] >= 0 ? *reinterpret_cast<const float2*>(W1 + (size_t)fj[u] * HID + h0)
+                          : make_float2(0.0f, 0.0f);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (fj[u] >= 0) {
+          acc.x = fmaf(vj[u], w[u].x, acc.x);
+          acc.y = fmaf(vj[u], w[u].y, acc.y);
+        }
+      }
+    }
+    for (; j < cnt; ++j) {
+      const int fj = __builtin_amdgcn_readlane(f, j);
+      const float vj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), j));
+      if (fj >= 0) {
+        const float2 w = *reinterpret_cast<const float2*>(W1 + (size_t)fj * HID + h0);
+        acc.x = fmaf(vj, w.x, acc.x);
+        acc.y = fmaf(vj, w.y, acc.y);
+      }
+    }
+  }
+  *reinterpret_cast<float2*>(A1 + (size_t)i * HID + h0) = acc;
+  const float r0 = fmaxf(acc.x, 0.0f), r1 = fmaxf(acc.y, 0.0f);
+  H1[(size_t)i * HID + h0] = (E)r0;
+  H1[(size_t)i * HID + h0 + 1] = (E)r1;
+  H1T[(size_t)h0 * ld_t + i] = (E)r0;
+  H1T[(size_t)(h0 + 1) * ld_t + i] = (E)r1;
+
+  if (has_y) {
+    const int ybase = y.indptr[0];
+    int ys = y.indptr[i], ye = y.indptr[i + 1];
+    if (ys < ybase || ye > ybase + y.nnz || ye < ys) {
+      bad |= ERR_INDPTR;
+      ys = max(ys, ybase);
+      ye = min(ye, ybase + y.nnz);
+      if (ye < ys) ye = ys;
+    }
+    if (ye == ys) bad |= ERR_EMPTY_LABELS;
+    if (lane == 0) rw[i] = ye > ys ? 1.0f / (float)(ye - ys) : 0.0f;
+    for (int q = ys + lane; q < ye; q += 64) {
+      const int lab = y.indices[q];
+      int key = F + lab;
+      if (lab < 0 || lab >= L) {
+        bad |= ERR_LABEL_ID;
+        key = F + L;
+      } else if (validate && q > ys && y.indices[q - 1] >= lab) {
+        bad |= ERR_DUPLICATE;
+      }
+      keys[x.nnz + (q - ybase)] = key;
+      lrow[q - ybase] = i;
+    }
+  }
+  if (bad) atomicOr(err, bad);
+}
+
+hipError_t launch_gather_fwd(bool use_bf16, const CsrDev& x, const CsrDev* y, const float* W1,
+                             const float* b1, int F, int L, float* A1, void* H1, void* H1T,
+                             int rows_pad, int ld_t, int32_t* keys, int32_t* row_of,
+                             int32_t* lrow, float* rw, int32_t* err, int validate, hipStream_t st) {
+  const dim3 grid((rows_pad + 3) / 4), block(256);
+  CsrDev yy = y ? *y : CsrDev{0, 0, 0, nullptr, nullptr, nullptr};
+  if (use_bf16)
+    hipLaunchKernelGGL(k_gather_fwd<true>, grid, block, 0, st, x, yy, y != nullptr, W1, b1, F, L,
+                       A1, (bf16*)H1, (bf16*)H1T, rows_pad, ld_t, keys, row_of, lrow, rw, err,
+                       validate);
+  else
+    hipLaunchKernelGGL(k_gather_fwd<false>, grid, block, 0, st, x, yy, y != nullptr, W1, b1, F, L,
+                       A1, (float*)H1, (float*)H1T, rows_pad, ld_t, keys, row_of, lrow, rw, err,
+                       validate);
+  return hipGetLastError();
+}
+
+}  // namespace asgd

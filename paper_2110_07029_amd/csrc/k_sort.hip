@@ -1,0 +1,162 @@
+// Stable LSD radix sort of int32 keys with their original positions as the
+// payload.  It orders the batch's (feature id) and (label id) entries so that
+// the sparse W1 gradient becomes a segmented reduction over equal feature ids
+// (no contended atomics, fixed summation order) and so that each output-layer
+// tile can find its true labels with a binary search.
+//
+// One pass over a digit of up to 11 bits = three launches:
+//   hist    : per-workgroup digit counts of a 2048-key chunk (LDS counters)
+//   scan    : exclusive scan over (digit, workgroup) -> global scatter offsets
+//   scatter : stable ranks inside the chunk from 64-lane ballots (lanes with the
+//             same digit in one wave), per-wave running counts, then a prefix
+//             over the four waves; keys land at offset + rank.
+#include "asgd_dev.h"
+#include "asgd_kernels.h"
+
+namespace asgd {
+
+constexpr int SORT_THREADS = 256;
+constexpr int SORT_WAVES = SORT_THREADS / 64;
+constexpr int SORT_PER_WAVE = SORT_CHUNK / SORT_WAVES;  // 512
+constexpr int SORT_ITERS = SORT_PER_WAVE / 64;         // 8
+
+int sort_blocks(int n) { return (n + SORT_CHUNK - 1) / SORT_CHUNK; }
+
+__global__ __launch_bounds__(SORT_THREADS) void k_sort_hist(const int32_t* __restrict__ keys, int n,
+                                                            int shift, int nbits, int nblk,
+                                                            int32_t* __restrict__ hist) {
+  __shared__ int cnt[1 << SORT_MAX_BITS];
+  const int nd = 1 << nbits;
+  for (int d = threadIdx.x; d < nd; d += SORT_THREADS) cnt[d] = 0;
+  __syncthreads();
+  const int b0 = blockIdx.x * SORT_CHUNK;
+  for (int t = threadIdx.x; t < SORT_CHUNK; t += SORT_THREADS) {
+    const int p = b0 + t;
+    if (p < n) atomicAdd(&cnt[(keys[p] >> shift) & (nd - 1)], 1);
+  }
+  __syncthreads();
+  for (int d = threadIdx.x; d < nd; d += SORT_THREADS) hist[d * nblk + blockIdx.x] = cnt[d];
+}
+
+// Exclusive prefix sum of hist[0..total) by one workgroup, 1024 entries per round.
+__global__ __launch_bounds__(1024) void k_sort_scan(const int32_t* __restrict__ hist, int total,
+                                                    int32_t* __restrict__ offs) {
+  __shared__ int wsum[16];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int carry = 0;
+  for (int base = 0; base < total; base += 1024) {
+    const int idx = base + threadIdx.x;
+    const int v = idx < total ? hist[idx] : 0;
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) wsum[w] = x;
+    __syncthreads();
+    if (w == 0) {
+      int s = lane < 16 ? wsum[lane] : 0;
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) {
+        const int y = __shfl_up(s, o);
+        if (lane >= o) s += y;
+      }
+      if (lane < 16) wsum[lane] = s;
+    }
+    __syncthreads();
+    const int wprefix = w > 0 ? wsum[w - 1] : 0;
+    if (idx < total) offs[idx] = carry + wprefix + x - v;
+    carry += wsum[15];
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(SORT_THREADS) void k_sort_scatter(
+    const int32_t* __restrict__ keys_in, const int32_t* __restrict__ vals_in, int n, int shift,
+    int nbits, int nblk, const int32_t* __restrict__ offs, int32_t* __restrict__ keys_out,
+    int32_t* __restrict__ vals_out) {
+  __shared__ int wcnt[SORT_WAVES][1 << SORT_MAX_BITS];
+  const int nd = 1 << nbits;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  for (int d = lane; d < nd; d += 64) wcnt[w][d] = 0;
+  __syncthreads();
+  const int p0 = blockIdx.x * SORT_CHUNK + w * SORT_PER_WAVE;
+  const uint64_t below = (1ull << lane) - 1ull;
+  int key[SORT_ITERS], val[SORT_ITERS], rank[SORT_ITERS];
+#pragma unroll
+  for (int it = 0; it < SORT_ITERS; ++it) {
+    const int p = p0 + it * 64 + lane;
+    const bool valid = p < n;
+    const int k = valid ? keys_in[p] : 0;
+    key[it] = k;
+    val[it] = valid ? (vals_in ? vals_in[p] : p) : 0;
+    const int d = (k >> shift) & (nd - 1);
+    uint64_t peers = __ballot(valid);
+    for (int b = 0; b < nbits; ++b) {
+      const bool bit = (d >> b) & 1;
+      const uint64_t bal = __ballot(bit);
+      peers &= bit ? bal : ~bal;
+    }
+    const int before = __popcll(peers & below);
+    const int c = wcnt[w][d];  // every peer reads the count before the leader updates it
+    rank[it] = c + before;
+    if (valid && before == 0) wcnt[w][d] = c + __popcll(peers);
+  }
+  __syncthreads();
+  for (int d = threadIdx.x; d < nd; d += SORT_THREADS) {
+    int run = 0;
+#pragma unroll
+    for (int ww = 0; ww < SORT_WAVES; ++ww) {
+      const int c = wcnt[ww][d];
+      wcnt[ww][d] = run;
+      run += c;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int it = 0; it < SORT_ITERS; ++it) {
+    const int p = p0 + it * 64 + lane;
+    if (p < n) {
+      const int d = (key[it] >> shift) & (nd - 1);
+      const int pos = offs[d * nblk + blockIdx.x] + wcnt[w][d] + rank[it];
+      keys_out[pos] = key[it];
+      vals_out[pos] = val[it];
+    }
+  }
+}
+
+hipError_t launch_sort(const int32_t* keys_in, int n, int key_bits, int32_t* keys_a,
+                       int32_t* vals_a, int32_t* keys_b, int32_t* vals_b, int32_t* hist,
+                       const int32_t** keys_out, const int32_t** vals_out, hipStream_t st) {
+  *keys_out = keys_a;
+  *vals_out = vals_a;
+  if (n <= 0) return hipSuccess;
+  if (key_bits < 1) key_bits = 1;
+  const int npass = (key_bits + SORT_MAX_BITS - 1) / SORT_MAX_BITS;
+  const int bits = (key_bits + npass - 1) / npass;
+  const int nblk = sort_blocks(n);
+  int32_t* offs = hist + ((size_t)nblk << SORT_MAX_BITS);
+  const int32_t* kin = keys_in;
+  const int32_t* vin = nullptr;
+  int32_t* kout = keys_a;
+  int32_t* vout = vals_a;
+  for (int pass = 0; pass < npass; ++pass) {
+    const int shift = pass * bits;
+    const int nb = key_bits - shift < bits ? key_bits - shift : bits;
+    hipLaunchKernelGGL(k_sort_hist, dim3(nblk), dim3(SORT_THREADS), 0, st, kin, n, shift, nb, nblk,
+                       hist);
+    hipLaunchKernelGGL(k_sort_scan, dim3(1), dim3(1024), 0, st, hist, nblk << nb, offs);
+    hipLaunchKernelGGL(k_sort_scatter, dim3(nblk), dim3(SORT_THREADS), 0, st, kin, vin, n, shift,
+                       nb, nblk, offs, kout, vout);
+    *keys_out = kout;
+    *vals_out = vout;
+    kin = kout;
+    vin = vout;
+    kout = (kout == keys_a) ? keys_b : keys_a;
+    vout = (vout == vals_a) ? vals_b : vals_a;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace asgd

@@ -1,0 +1,161 @@
+"""Helpers shared by the GPU parity tests: stage a synthetic dataset on the
+device, build models through the C ABI, read parameters back and compare
+parameter updates with the oracle's."""
+from __future__ import annotations
+
+import numpy as np
+
+import paper_2110_07029_amd as asgd
+from paper_2110_07029_amd import synth
+
+H = asgd.HIDDEN
+
+# Tolerances of the parity bar: relative 1e-4 for fp32 products and 2e-2 for
+# bf16-operand products.  Elementwise the bound is rtol * (|ref| + mag), where
+# mag is the same sum taken over absolute values (|a|^T |b| for a product):
+# the standard forward-error bound of a dot product, which stays meaningful for
+# entries that cancel to near zero; plus two float32 ulps of the stored weight
+# for the final rounding of the update.  Normwise: ||err|| <= rtol ||ref||.
+RTOL_FP32 = 1e-4
+RTOL_BF16 = 2e-2
+
+
+def flush(msg: str):
+    print(msg, flush=True)
+
+
+def read_params(m, F, L) -> dict:
+    return dict(W1=asgd.asgd_model_get_params(m, asgd.ASGD_PARAM_W1, (F, H)),
+                b1=asgd.asgd_model_get_params(m, asgd.ASGD_PARAM_B1, (H,)),
+                W2=asgd.asgd_model_get_params(m, asgd.ASGD_PARAM_W2, (L, H)),
+                b2=asgd.asgd_model_get_params(m, asgd.ASGD_PARAM_B2, (L,)))
+
+
+def write_params(m, p: dict):
+    asgd.asgd_model_set_params(m, asgd.ASGD_PARAM_W1, p["W1"])
+    asgd.asgd_model_set_params(m, asgd.ASGD_PARAM_B1, p["b1"])
+    asgd.asgd_model_set_params(m, asgd.ASGD_PARAM_W2, p["W2"])
+    asgd.asgd_model_set_params(m, asgd.ASGD_PARAM_B2, p["b2"])
+
+
+def max_batch_nnz(csr, batch: int) -> int:
+    ip = np.asarray(csr.indptr, np.int64)
+    n = len(ip) - 1
+    best = 0
+    for r0 in range(0, n, batch):
+        r1 = min(n, r0 + batch)
+        best = max(best, int(ip[r1] - ip[r0]))
+    return best
+
+
+class Setup:
+    """A dataset staged on the device plus a model sized for it."""
+
+    def __init__(self, w: synth.Workload, n_samples: int, batch: int, bf16=None, flags=0, seed=None,
+                 ds=None, max_batch=None):
+        import torch
+        self.w = w
+        self.ds = ds if ds is not None else synth.generate(w, n_samples=n_samples)
+        self.batch = batch
+        self.bf16 = w.gemm_bf16 if bf16 is None else bf16
+        self.F, self.L = w.n_features, w.n_labels
+        self.dx = asgd.DeviceCSR(self.ds.x)
+        self.dy = asgd.DeviceCSR(self.ds.y)
+        mb = max_batch or batch
+        self.max_nnz = max(max_batch_nnz(self.ds.x, mb), 1)
+        self.max_lnnz = max(max_batch_nnz(self.ds.y, mb), 1)
+        self.seed = w.init_seed if seed is None else seed
+        self.m = asgd.asgd_model_init(self.F, self.L, mb, self.max_nnz, self.max_lnnz,
+                                      gemm_bf16=self.bf16, seed=self.seed, flags=flags,
+                                      stream=torch.cuda.current_stream())
+        self.stream = torch.cuda.current_stream()
+
+    def free(self):
+        if self.m:
+            asgd.asgd_model_free(self.m)
+            self.m = None
+
+    def xb(self, r0, r1):
+        return self.dx.batch(r0, r1)
+
+    def yb(self, r0, r1):
+        return self.dy.batch(r0, r1)
+
+    def host_batch(self, r0, r1):
+        return self.ds.x.rows(r0, r1), self.ds.y.rows(r0, r1)
+
+    def params(self):
+        return read_params(self.m, self.F, self.L)
+
+
+def update_error(before, gpu, ref):
+    """(max elementwise excess ratio, normwise relative error) of the update gpu-before vs ref-before."""
+    b = before.astype(np.float64)
+    d_g = gpu.astype(np.float64) - b
+    d_r = ref.astype(np.float64) - b
+    mag = np.maximum.reduce([np.abs(before), np.abs(gpu), np.abs(ref)]).astype(np.float32)
+    ulp = np.spacing(mag).astype(np.float64)
+    rms = float(np.sqrt(np.mean(d_r * d_r))) if d_r.size else 0.0
+    err = np.abs(d_g - d_r)
+    return err, d_r, ulp, rms
+
+
+def assert_update_close(name, before, gpu, ref, rtol, mag=None):
+    err, d_r, ulp, rms = update_error(before, gpu, ref)
+    floor = 0.1 * rms if mag is None else np.asarray(mag, np.float64)
+    bound = rtol * (np.abs(d_r) + floor) + 2.0 * ulp
+    bad = err > bound
+    nref = float(np.linalg.norm(d_r))
+    nerr = float(np.linalg.norm(err))
+    if bad.any():
+        i = np.unravel_index(np.argmax(err / bound), err.shape)
+        raise AssertionError(f"{name}: {int(bad.sum())} of {err.size} elements outside the bound; worst "
+                             f"at {i}: err {err[i]:.3e} bound {bound[i]:.3e} ref {d_r[i]:.3e}")
+    assert nerr <= rtol * nref + 2.0 * float(np.linalg.norm(ulp)), (name, nerr, nref)
+
+
+def assert_rel_close(name, got, ref, rtol, floor_frac=0.1):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    rms = float(np.sqrt(np.mean(ref * ref))) if ref.size else 0.0
+    err = np.abs(got - ref)
+    bound = rtol * (np.abs(ref) + floor_frac * rms) + 1e-30
+    if (err > bound).any():
+        i = np.unravel_index(np.argmax(err / bound), err.shape)
+        raise AssertionError(f"{name}: worst at {i}: got {got[i]!r} ref {ref[i]!r} err {err[i]:.3e} "
+                             f"bound {bound[i]:.3e}")
+
+
+def step_magnitudes(p, x, y, g, fw, lr):
+    """|lr| times each parameter gradient evaluated on absolute values along the whole
+    chain: |dZ| <= (P + T)/B, |dH1| <= (P + T)|W2|/B, |dA1| <= |dH1| [A1 > 0], then
+    |X|^T |dA1| for W1 and sums over rows for the biases."""
+    from oracle.model import row_ids, targets
+    s0, e0 = int(x.indptr[0]), int(x.indptr[-1])
+    ind = np.asarray(x.indices[s0:e0], np.int64)
+    val = np.abs(np.asarray(x.values[s0:e0], np.float64))
+    rows = row_ids(np.asarray(x.indptr, np.int64) - s0)
+    B, L = fw["Z"].shape
+    P = np.exp(fw["Z"] - fw["lse"][:, None])
+    PT = (P + targets(y, L)) / B
+    dA1m = (PT @ np.abs(p["W2"]).astype(np.float64)) * (fw["A1"] > 0)
+    inv = np.searchsorted(g["touched"], ind)
+    mW1 = np.zeros((len(g["touched"]), dA1m.shape[1]))
+    np.add.at(mW1, inv, val[:, None] * dA1m[rows])
+    lr = abs(float(lr))
+    return dict(W2=lr * (PT.T @ np.abs(fw["H1"])), b2=lr * PT.sum(0), b1=lr * dA1m.sum(0),
+                W1=lr * mW1)
+
+
+def a1_bound(p, x):
+    """Rigorous bound of a float32 fma chain for A1 = b1 + X W1: n u (|b1| + |X| |W1|)."""
+    from oracle.model import row_ids
+    s0, e0 = int(x.indptr[0]), int(x.indptr[-1])
+    ind = np.asarray(x.indices[s0:e0], np.int64)
+    val = np.abs(np.asarray(x.values[s0:e0], np.float64))
+    rows = row_ids(np.asarray(x.indptr, np.int64) - s0)
+    B = len(x.indptr) - 1
+    mag = np.tile(np.abs(p["b1"]).astype(np.float64), (B, 1))
+    np.add.at(mag, rows, val[:, None] * np.abs(p["W1"][ind]).astype(np.float64))
+    n = np.diff(np.asarray(x.indptr, np.int64)).max() + 1
+    return (n + 1) * 2.0 ** -24 * mag

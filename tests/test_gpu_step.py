@@ -1,0 +1,236 @@
+"""GPU parity of the per-replica step (HIP path through the C ABI) against the
+CPU oracle on the same seeded inputs: initialisation, the first-layer gather,
+the output-layer forward (log-sum-exp, loss), the touched-row set, and the
+full SGD update of every parameter tensor."""
+import numpy as np
+import pytest
+
+import paper_2110_07029_amd as asgd
+from oracle import model as om
+from paper_2110_07029_amd import synth
+
+from gpu_util import (RTOL_BF16, RTOL_FP32, Setup, a1_bound, assert_rel_close, assert_update_close,
+                      flush, read_params, step_magnitudes)
+
+pytestmark = pytest.mark.gpu
+
+SMALL_MID = synth.Workload("mid-small", 20_000, 3_000, 4_000, 256, 0.01, True, "lognormal", 4.0,
+                           0.8, 2_000, 1.05, "uniform", "poisson", 4.0, 1.2, 2)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    asgd.load()
+    yield
+    torch.cuda.synchronize()
+
+
+def test_init_bit_exact_against_oracle():
+    flush("init: tiny fp32 and mid-small bf16")
+    for w in (synth.TINY, SMALL_MID):
+        s = Setup(w, 256, 128)
+        try:
+            got = s.params()
+            ref = om.init_params(w.n_features, w.n_labels, 128, w.init_seed)
+            for k in ("W1", "b1", "W2", "b2"):
+                assert np.array_equal(got[k].view(np.uint32), ref[k].view(np.uint32)), (w.name, k)
+        finally:
+            s.free()
+
+
+@pytest.mark.parametrize("w,B,rows", [(synth.TINY, 128, (0, 128)), (synth.TINY, 128, (1920, 2000)),
+                                      (SMALL_MID, 256, (0, 256)), (SMALL_MID, 256, (256, 333)),
+                                      (SMALL_MID, 256, (7, 8))])
+def test_forward_parity(w, B, rows):
+    import torch
+    r0, r1 = rows
+    flush(f"forward: {w.name} rows {r0}..{r1}")
+    s = Setup(w, max(r1, 512), B)
+    try:
+        n = r1 - r0
+        a1 = torch.empty((n, 128), dtype=torch.float32, device="cuda")
+        lse = torch.empty(n, dtype=torch.float32, device="cuda")
+        lr_ = torch.empty(n, dtype=torch.float32, device="cuda")
+        asgd.asgd_debug_forward(s.m, s.xb(r0, r1), s.yb(r0, r1), a1, lse, lr_)
+        torch.cuda.synchronize()
+        xh, yh = s.host_batch(r0, r1)
+        p = s.params()
+        ops = "bf16" if s.bf16 else "fp32"
+        ref = om.forward(p, xh, yh, ops)
+        # A1 is a float32 fma chain: within n*u*(|b1| + |X||W1|) of the exact value
+        err = np.abs(a1.cpu().numpy().astype(np.float64) - ref["A1"])
+        assert np.all(err <= a1_bound(p, xh) + 1e-7 * np.abs(ref["A1"]))
+        rt = RTOL_FP32 if not s.bf16 else 1e-3
+        assert_rel_close("lse", lse.cpu().numpy(), ref["lse"], rt, floor_frac=0.0)
+        assert_rel_close("loss_rows", lr_.cpu().numpy(), ref["loss_rows"], rt, floor_frac=0.0)
+        if s.bf16:  # against the exact (non-emulated) definition, the bf16 bar
+            ex = om.forward(p, xh, yh, "fp32")
+            assert_rel_close("loss_rows(exact)", lr_.cpu().numpy(), ex["loss_rows"], RTOL_BF16, 0.0)
+    finally:
+        s.free()
+
+
+def test_one_hot_rows_are_exact_rows_of_w1():
+    import torch
+    flush("forward: one-hot rows")
+    w = synth.TINY
+    F = w.n_features
+    fs = np.array([0, 17, 4999, 2500, 17], np.int32)
+    x = synth.CSR(np.arange(6), fs, np.ones(5, np.float32), F)
+    y = synth.CSR(np.arange(6), np.array([1, 2, 3, 4, 5], np.int32), None, w.n_labels)
+    ds = synth.Dataset(w, x, y)
+    s = Setup(w, 0, 8, ds=ds)
+    try:
+        b1 = np.linspace(-0.5, 0.5, 128).astype(np.float32)
+        asgd.asgd_model_set_params(s.m, asgd.ASGD_PARAM_B1, b1)
+        a1 = torch.empty((5, 128), dtype=torch.float32, device="cuda")
+        asgd.asgd_debug_forward(s.m, s.xb(0, 5), None, a1, None, None)
+        torch.cuda.synchronize()
+        W1 = s.params()["W1"]
+        want = (W1[fs].astype(np.float64) + b1.astype(np.float64)).astype(np.float32)
+        assert np.array_equal(a1.cpu().numpy().view(np.uint32), want.view(np.uint32))
+    finally:
+        s.free()
+
+
+@pytest.mark.parametrize("w,rows", [(synth.TINY, (0, 128)), (SMALL_MID, (0, 256)), (SMALL_MID, (100, 101))])
+def test_touched_rows_bit_exact(w, rows):
+    import torch
+    flush(f"touched rows: {w.name} {rows}")
+    s = Setup(w, 512, 256)
+    try:
+        r0, r1 = rows
+        ids = torch.empty(s.dx.nnz(r0, r1) + 1, dtype=torch.int32, device="cuda")
+        c = asgd.asgd_debug_touched_rows(s.m, s.xb(r0, r1), ids)
+        xh, _ = s.host_batch(r0, r1)
+        ref = om.touched_features(xh)
+        assert c == len(ref)
+        assert np.array_equal(ids[:c].cpu().numpy(), ref)
+    finally:
+        s.free()
+
+
+def _step_parity(s, r0, r1, lr, rtol, ops):
+    before = s.params()
+    loss = asgd.asgd_train_step(s.m, s.xb(r0, r1), s.yb(r0, r1), lr, want_loss=True)
+    after = s.params()
+    xh, yh = s.host_batch(r0, r1)
+    ref, ref_loss, g, fw = om.train_step(before, xh, yh, lr, ops)
+    assert abs(loss - ref_loss) <= max(rtol, 1e-5) * abs(ref_loss), (loss, ref_loss)
+    mag = step_magnitudes(before, xh, yh, g, fw, lr)
+    for k in ("b1", "W2", "b2"):
+        assert_update_close(k, before[k], after[k], ref[k], rtol, mag[k])
+    t = g["touched"]
+    assert_update_close("W1[touched]", before["W1"][t], after["W1"][t], ref["W1"][t], rtol, mag["W1"])
+    untouched = np.setdiff1d(np.arange(s.F), t)
+    assert np.array_equal(after["W1"][untouched].view(np.uint32), before["W1"][untouched].view(np.uint32))
+    return before, after, ref
+
+
+@pytest.mark.parametrize("rows", [(0, 128), (1920, 2000), (5, 6)])
+def test_step_parity_fp32(rows):
+    flush(f"step fp32 tiny rows {rows}")
+    s = Setup(synth.TINY, 2000, 128)
+    try:
+        _step_parity(s, rows[0], rows[1], 0.01, RTOL_FP32, "fp32")
+    finally:
+        s.free()
+
+
+@pytest.mark.parametrize("rows,B", [((0, 256), 256), ((256, 389), 256), ((0, 600), 600),
+                                    ((3, 4), 256)])
+def test_step_parity_bf16(rows, B):
+    flush(f"step bf16 mid-small rows {rows} max_batch {B}")
+    s = Setup(SMALL_MID, 1024, B)
+    try:
+        before, after, ref_exact = _step_parity(s, rows[0], rows[1], 0.05, RTOL_BF16, "fp32")
+        # tighter against the oracle with bf16-rounded operands
+        xh, yh = s.host_batch(*rows)
+        ref_emu, _, g, fw = om.train_step(before, xh, yh, 0.05, "bf16")
+        mag = step_magnitudes(before, xh, yh, g, fw, 0.05)
+        assert_update_close("W2(bf16 operands)", before["W2"], after["W2"], ref_emu["W2"], 2e-3, mag["W2"])
+        assert_update_close("b2(bf16 operands)", before["b2"], after["b2"], ref_emu["b2"], 2e-3, mag["b2"])
+    finally:
+        s.free()
+
+
+def test_step_with_empty_feature_row_and_single_label_rows():
+    flush("step: empty feature rows")
+    w = synth.TINY
+    x = synth.CSR(np.array([0, 2, 2, 5, 5]), np.array([3, 9, 1, 2, 4999], np.int32),
+                  np.array([0.6, 0.8, 0.5, 0.5, 0.7], np.float32), w.n_features)
+    y = synth.CSR(np.array([0, 1, 3, 4, 5]), np.array([0, 5, 999, 7, 7], np.int32), None, w.n_labels)
+    s = Setup(w, 0, 8, ds=synth.Dataset(w, x, y))
+    try:
+        _step_parity(s, 0, 4, 0.1, RTOL_FP32, "fp32")
+    finally:
+        s.free()
+
+
+def test_epoch_free_running_fp32():
+    flush("epoch: tiny fp32, 16 steps free running")
+    w = synth.TINY
+    s = Setup(w, 2000, 128)
+    try:
+        ref = s.params()
+        for r0, r1 in synth.batches(s.ds, 128):
+            asgd.asgd_train_step(s.m, s.xb(r0, r1), s.yb(r0, r1), w.lr)
+            xh, yh = s.host_batch(r0, r1)
+            ref, *_ = om.train_step(ref, xh, yh, w.lr, "fp32")
+        got = s.params()
+        init = om.init_params(w.n_features, w.n_labels, 128, w.init_seed)
+        for k in ("W1", "b1", "W2", "b2"):
+            assert_update_close(k, init[k], got[k], ref[k], 1e-3)
+    finally:
+        s.free()
+
+
+def test_step_is_deterministic():
+    flush("determinism: same step twice")
+    s = Setup(SMALL_MID, 512, 256)
+    try:
+        p0 = s.params()
+        asgd.asgd_train_step(s.m, s.xb(0, 256), s.yb(0, 256), 0.05)
+        p1 = s.params()
+        from gpu_util import write_params
+        write_params(s.m, p0)
+        asgd.asgd_train_step(s.m, s.xb(0, 256), s.yb(0, 256), 0.05)
+        p2 = s.params()
+        for k in p1:
+            assert np.array_equal(p1[k].view(np.uint32), p2[k].view(np.uint32)), k
+    finally:
+        s.free()
+
+
+def test_argument_errors_leave_model_unchanged():
+    flush("errors: host-side argument checks and device validation")
+    w = synth.TINY
+    s = Setup(w, 512, 64, flags=asgd.ASGD_VALIDATE)
+    try:
+        p0 = s.params()
+        with pytest.raises(asgd.AsgdError) as e:          # batch beyond max_batch
+            asgd.asgd_train_step(s.m, s.xb(0, 100), s.yb(0, 100), 0.1)
+        assert e.value.status in (asgd.ASGD_ERANGE,)
+        with pytest.raises(asgd.AsgdError) as e:          # row count mismatch
+            asgd.asgd_train_step(s.m, s.xb(0, 10), s.yb(0, 11), 0.1)
+        assert e.value.status == asgd.ASGD_EINVAL
+        with pytest.raises(asgd.AsgdError):               # k out of range
+            asgd.asgd_predict_topk(s.m, s.xb(0, 10), 33, 0)
+        # malformed content caught on the device: feature id out of range, duplicate ids,
+        # empty label row -> EINVAL and nothing updated
+        bad_x = synth.CSR(np.array([0, 2, 4]), np.array([1, 5000, 3, 3], np.int32),
+                          np.ones(4, np.float32), w.n_features)
+        bad_y = synth.CSR(np.array([0, 1, 1]), np.array([2], np.int32), None, w.n_labels)
+        bx, by = asgd.DeviceCSR(bad_x), asgd.DeviceCSR(bad_y)
+        with pytest.raises(asgd.AsgdError) as e:
+            asgd.asgd_train_step(s.m, bx.batch(0, 2), by.batch(0, 2), 0.1)
+        assert e.value.status == asgd.ASGD_EINVAL
+        msg = asgd.asgd_last_error()
+        assert "0x1" in msg or "0x" in msg
+        p1 = s.params()
+        for k in p0:
+            assert np.array_equal(p0[k].view(np.uint32), p1[k].view(np.uint32)), k
+    finally:
+        s.free()
