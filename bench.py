@@ -170,7 +170,11 @@ def main():
                          "GB/s": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
                          "TFLOP/s": round(tfs, 2), "mfma_frac": round(tfs / MFMA_PEAK_TFLOPS[dtype], 4),
                          "share_of_step": round(tot / ms, 4)}
-    dom = max(kt, key=lambda k: kt[k][0])
+        if name == "sort":
+            kernels[name]["overlapped"] = True
+    # the sort runs on the library's second stream, overlapped with the output-layer
+    # forward: its event span includes time it waited for CUs, so it is not a candidate
+    dom = max((k for k in kt if k != "sort"), key=lambda k: kt[k][0])
     d = kernels[dom]
     roofline = {"kernel": dom, "bound": "hbm", "achieved": d["GB/s"], "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": d["hbm_frac"], "traffic": None}

@@ -64,6 +64,9 @@ struct asgd_model {
   bool bf16 = true;
   hipStream_t stream = nullptr;
   int device = 0;
+  int n_cu = 256;
+  hipStream_t aux = nullptr;      // internal stream: the sort overlaps the output-layer forward
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   hipEvent_t ev = nullptr;
 
   // parameters
@@ -210,7 +213,7 @@ int fwd_splits(asgd_model* m, int B) {
 }
 
 // Start event of the next timed launch of group k (nullptr when not timing).
-hipEvent_t timer_start(asgd_model* m, int k, hipEvent_t* stop) {
+hipEvent_t timer_start(asgd_model* m, int k, hipStream_t st, hipEvent_t* stop) {
   *stop = nullptr;
   if (!m->timing || m->tused[k] >= asgd_model::kTimerPool) return nullptr;
   std::vector<hipEvent_t>& v = m->tev[k];
@@ -224,7 +227,7 @@ hipEvent_t timer_start(asgd_model* m, int k, hipEvent_t* stop) {
     v.push_back(a);
     v.push_back(b);
   }
-  if (hipEventRecord(v[2 * i], m->stream) != hipSuccess) {
+  if (hipEventRecord(v[2 * i], st) != hipSuccess) {
     --m->tused[k];
     return nullptr;
   }
@@ -232,13 +235,14 @@ hipEvent_t timer_start(asgd_model* m, int k, hipEvent_t* stop) {
   return v[2 * i];
 }
 
-#define TIMED(m, k, expr)                                      \
+#define TIMED_ON(m, k, st, expr)                               \
   do {                                                         \
     hipEvent_t stop_ = nullptr;                                \
-    timer_start((m), (k), &stop_);                             \
+    timer_start((m), (k), (st), &stop_);                       \
     HIP_TRY(expr);                                             \
-    if (stop_) HIP_TRY(hipEventRecord(stop_, (m)->stream));    \
+    if (stop_) HIP_TRY(hipEventRecord(stop_, (st)));           \
   } while (0)
+#define TIMED(m, k, expr) TIMED_ON(m, k, (m)->stream, expr)
 
 // Gather forward (+ keys), optional validation check.  Leaves H1 / A1 ready.
 asgd_status run_gather(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int* rows_pad_out) {
@@ -269,10 +273,11 @@ asgd_status run_gather(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int*
   return ASGD_OK;
 }
 
-asgd_status run_sort(asgd_model* m, int n_keys, const int32_t** sk, const int32_t** sv) {
+asgd_status run_sort(asgd_model* m, hipStream_t st, int n_keys, const int32_t** sk,
+                     const int32_t** sv) {
   const int key_bits = bit_width((uint32_t)(m->F + m->L));
-  TIMED(m, ASGD_K_SORT, launch_sort(m->keys, n_keys, key_bits, m->ka, m->va, m->kb, m->vb, m->hist, sk, sv,
-                      m->stream));
+  TIMED_ON(m, ASGD_K_SORT, st,
+           launch_sort(m->keys, n_keys, key_bits, m->ka, m->va, m->kb, m->vb, m->hist, sk, sv, st));
   return ASGD_OK;
 }
 
@@ -340,7 +345,12 @@ asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t s
   m->n_params = F * HID + HID + L * HID + L;
 
   hipError_t e = hipGetDevice(&m->device);
+  if (e == hipSuccess)
+    e = hipDeviceGetAttribute(&m->n_cu, hipDeviceAttributeMultiprocessorCount, m->device);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_fork, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_join, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&m->aux, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipMalloc((void**)&m->params, m->n_pad * sizeof(float));
   if (e != hipSuccess) {
     asgd_model_free(m);
@@ -374,9 +384,13 @@ asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t s
 asgd_status asgd_model_free(asgd_model* m) {
   if (!m) return ASGD_OK;
   if (m->params || m->ws) (void)hipStreamSynchronize(m->stream);
+  if (m->aux) (void)hipStreamSynchronize(m->aux);
   if (m->params) (void)hipFree(m->params);
   if (m->ws) (void)hipFree(m->ws);
   if (m->ev) (void)hipEventDestroy(m->ev);
+  if (m->ev_fork) (void)hipEventDestroy(m->ev_fork);
+  if (m->ev_join) (void)hipEventDestroy(m->ev_join);
+  if (m->aux) (void)hipStreamDestroy(m->aux);
   for (auto& v : m->tev)
     for (hipEvent_t e : v) (void)hipEventDestroy(e);
   delete m;
@@ -460,15 +474,21 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   int rows_pad = 0;
   s = run_gather(m, x, y, &rows_pad);
   if (s) return s;
+  // the sort depends only on the keys the gather wrote: run it on the internal
+  // stream, concurrently with the output-layer forward and combine
   const int n_keys = x->nnz + y->nnz;
   const int32_t *sk = nullptr, *sv = nullptr;
-  s = run_sort(m, n_keys, &sk, &sv);
+  HIP_TRY(hipEventRecord(m->ev_fork, m->stream));
+  HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_fork, 0));
+  s = run_sort(m, m->aux, n_keys, &sk, &sv);
   if (s) return s;
+  HIP_TRY(hipEventRecord(m->ev_join, m->aux));
   s = run_forward(m, x, y, rows_pad);
   if (s) return s;
   TIMED(m, ASGD_K_HIDDEN, launch_hidden_bias(B, m->dA1, m->b1(), lr, m->loss_rows, m->loss, m->stream));
+  HIP_TRY(hipStreamWaitEvent(m->stream, m->ev_join, 0));
   TIMED(m, ASGD_K_OUT_BWD, launch_out_bwd(m->bf16, m->W2(), m->b2(), m->L, m->F, m->H1, m->H1T, m->rows_pad_max, B,
-                         m->lse, m->rw, sk, sv, n_keys, x->nnz, m->lrow, lr, m->stream));
+                         m->lse, m->rw, sk, sv, n_keys, x->nnz, m->lrow, lr, m->n_cu, m->stream));
   CsrDev xd = dev(x);
   TIMED(m, ASGD_K_W1_UPDATE, launch_w1_update(m->W1(), m->F, sk, sv, x->nnz, m->row_of, xd, m->dA1, lr, m->stream));
   if (loss_out) return asgd_model_last_loss(m, loss_out);
@@ -617,7 +637,7 @@ asgd_status asgd_debug_touched_rows(asgd_model* m, const asgd_csr* x, int32_t* i
   s = run_gather(m, x, nullptr, &rows_pad);
   if (s) return s;
   const int32_t *sk = nullptr, *sv = nullptr;
-  s = run_sort(m, x->nnz, &sk, &sv);
+  s = run_sort(m, m->stream, x->nnz, &sk, &sv);
   if (s) return s;
   HIP_TRY(launch_touched(sk, x->nnz, m->F, ids_dev, m->count, m->stream));
   int32_t c = 0;

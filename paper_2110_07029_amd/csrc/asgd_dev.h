@@ -83,6 +83,35 @@ __device__ __forceinline__ bf16x8 frag_acc_bf16(const float* v, int c) {
   return f;
 }
 
+template <bool BF16>
+__device__ __forceinline__ typename Mma<BF16>::frag frag_row(const typename Mma<BF16>::elem* p,
+                                                             int c, int g) {
+  if constexpr (BF16)
+    return frag_row_bf16(p, c, g);
+  else
+    return frag_row_f32(p, c, g);
+}
+
+template <bool BF16>
+__device__ __forceinline__ typename Mma<BF16>::frag frag_acc(const float* v, int c) {
+  if constexpr (BF16)
+    return frag_acc_bf16(v, c);
+  else
+    return v[c];
+}
+
+__device__ __forceinline__ int lower_bound_dev(const int32_t* __restrict__ a, int n, int key) {
+  int lo = 0, hi = n;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (a[mid] < key)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  return lo;
+}
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));

@@ -35,7 +35,7 @@ hipError_t launch_gather_fwd(bool use_bf16, const CsrDev& x, const CsrDev* y, co
                              int32_t* lrow, float* rw, int32_t* err, int validate, hipStream_t st);
 
 // ---- stable LSD radix sort of (key, position) -----------------------------
-constexpr int SORT_CHUNK = 2048;   // keys per workgroup
+constexpr int SORT_CHUNK = 1024;   // keys per workgroup
 constexpr int SORT_MAX_BITS = 11;  // digit width limit per pass
 int sort_blocks(int n);
 // Sorts keys[0..n) (values < 2^key_bits) stably; the payload is the original
@@ -66,7 +66,7 @@ hipError_t launch_hidden_bias(int B, const float* dA1, float* b1, float lr, cons
 hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, int F, const void* H1,
                           const void* H1T, int ld_t, int B, const float* lse, const float* rw,
                           const int32_t* skeys, const int32_t* svals, int n_keys, int label_base,
-                          const int32_t* lrow, float lr, hipStream_t st);
+                          const int32_t* lrow, float lr, int n_cu, hipStream_t st);
 // W1[f] -= lr * sum_{entries of f} x * dA1[row], one segment per distinct f.
 hipError_t launch_w1_update(float* W1, int F, const int32_t* skeys, const int32_t* svals,
                             int n_feat_keys, const int32_t* row_of, const CsrDev& x,

@@ -46,27 +46,35 @@ hipError_t launch_fill_int(int32_t* p, int32_t v, int64_t n, hipStream_t st) {
 
 // ---------------------------------------------------------------------------
 // A1[i] = b1 + sum_{(f, v) in row i} v * W1[f];  H1 = max(A1, 0).
-// One wavefront per sample row; lane l owns hidden units 2l and 2l+1, so every
-// W1 row is read as one coalesced 512-byte access.  The row's (id, value)
-// pairs are loaded 64 at a time (one per lane) and broadcast with readlane.
+// One workgroup (4 wavefronts) per sample row.  Lane l owns hidden units 2l
+// and 2l+1, so every W1 row is one coalesced 512-byte access.  The row's
+// entries are split into 4 contiguous ranges, one per wavefront; a wavefront
+// loads up to 64 (id, value) pairs at once (one per lane, also writing their
+// sort keys), broadcasts them with readlane and keeps 8 W1 rows in flight.
+// The 4 partial sums are added in wavefront order, then b1.
 // ---------------------------------------------------------------------------
+constexpr int GATHER_WAVES = 4;
+constexpr int GATHER_UNROLL = 8;
+
 template <bool BF16>
-__global__ __launch_bounds__(256) void k_gather_fwd(
+__global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
     CsrDev x, CsrDev y, int has_y, const float* __restrict__ W1, const float* __restrict__ b1,
     int F, int L, float* __restrict__ A1, typename Mma<BF16>::elem* __restrict__ H1,
     typename Mma<BF16>::elem* __restrict__ H1T, int rows_pad, int ld_t, int32_t* __restrict__ keys,
     int32_t* __restrict__ row_of, int32_t* __restrict__ lrow, float* __restrict__ rw,
     int32_t* __restrict__ err, int validate) {
   using E = typename Mma<BF16>::elem;
-  const int lane = threadIdx.x & 63;
-  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (i >= rows_pad) return;
+  __shared__ float2 part[GATHER_WAVES][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = blockIdx.x;
   const int h0 = 2 * lane;
   if (i >= x.n_rows) {  // padding rows of the output-layer operands are zero
-    H1[(size_t)i * HID + h0] = (E)0.0f;
-    H1[(size_t)i * HID + h0 + 1] = (E)0.0f;
-    H1T[(size_t)h0 * ld_t + i] = (E)0.0f;
-    H1T[(size_t)(h0 + 1) * ld_t + i] = (E)0.0f;
+    if (wave == 0) {
+      H1[(size_t)i * HID + h0] = (E)0.0f;
+      H1[(size_t)i * HID + h0 + 1] = (E)0.0f;
+      H1T[(size_t)h0 * ld_t + i] = (E)0.0f;
+      H1T[(size_t)(h0 + 1) * ld_t + i] = (E)0.0f;
+    }
     return;
   }
   int bad = 0;
@@ -78,12 +86,14 @@ __global__ __launch_bounds__(256) void k_gather_fwd(
     e = min(e, base + x.nnz);
     if (e < s) e = s;
   }
-  float2 acc = *reinterpret_cast<const float2*>(b1 + h0);
-  for (int p0 = s; p0 < e; p0 += 64) {
+  const int per = (e - s + GATHER_WAVES - 1) / GATHER_WAVES;
+  const int ws = min(e, s + wave * per), we = min(e, ws + per);
+  float2 acc = make_float2(0.0f, 0.0f);
+  for (int p0 = ws; p0 < we; p0 += 64) {
     const int p = p0 + lane;
     int f = -1;
     float v = 0.0f;
-    if (p < e) {
+    if (p < we) {
       f = x.indices[p];
       v = x.values[p];
       int key = f;
@@ -97,26 +107,26 @@ __global__ __launch_bounds__(256) void k_gather_fwd(
       keys[p - base] = key;
       row_of[p - base] = i;
     }
-    const int cnt = min(64, e - p0);
+    const int cnt = min(64, we - p0);
     int j = 0;
-    for (; j + 4 <= cnt; j += 4) {
-      int fj[4];
-      float vj[4];
-      float2 w[4];
+    for (; j + GATHER_UNROLL <= cnt; j += GATHER_UNROLL) {
+      int fj[GATHER_UNROLL];
+      float vj[GATHER_UNROLL];
+      float2 wv[GATHER_UNROLL];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < GATHER_UNROLL; ++u) {
         fj[u] = __builtin_amdgcn_readlane(f, j + u);
         vj[u] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), j + u));
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        w[u] = fj[u] >= 0 ? *reinterpret_cast<const float2*>(W1 + (size_t)fj[u] * HID + h0)
-                          : make_float2(0.0f, 0.0f);
+      for (int u = 0; u < GATHER_UNROLL; ++u)
+        wv[u] = fj[u] >= 0 ? *reinterpret_cast<const float2*>(W1 + (size_t)fj[u] * HID + h0)
+                           : make_float2(0.0f, 0.0f);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < GATHER_UNROLL; ++u) {
         if (fj[u] >= 0) {
-          acc.x = fmaf(vj[u], w[u].x, acc.x);
-          acc.y = fmaf(vj[u], w[u].y, acc.y);
+          acc.x = fmaf(vj[u], wv[u].x, acc.x);
+          acc.y = fmaf(vj[u], wv[u].y, acc.y);
         }
       }
     }
@@ -124,20 +134,15 @@ __global__ __launch_bounds__(256) void k_gather_fwd(
       const int fj = __builtin_amdgcn_readlane(f, j);
       const float vj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), j));
       if (fj >= 0) {
-        const float2 w = *reinterpret_cast<const float2*>(W1 + (size_t)fj * HID + h0);
-        acc.x = fmaf(vj, w.x, acc.x);
-        acc.y = fmaf(vj, w.y, acc.y);
+        const float2 wv = *reinterpret_cast<const float2*>(W1 + (size_t)fj * HID + h0);
+        acc.x = fmaf(vj, wv.x, acc.x);
+        acc.y = fmaf(vj, wv.y, acc.y);
       }
     }
   }
-  *reinterpret_cast<float2*>(A1 + (size_t)i * HID + h0) = acc;
-  const float r0 = fmaxf(acc.x, 0.0f), r1 = fmaxf(acc.y, 0.0f);
-  H1[(size_t)i * HID + h0] = (E)r0;
-  H1[(size_t)i * HID + h0 + 1] = (E)r1;
-  H1T[(size_t)h0 * ld_t + i] = (E)r0;
-  H1T[(size_t)(h0 + 1) * ld_t + i] = (E)r1;
+  part[wave][lane] = acc;
 
-  if (has_y) {
+  if (has_y && wave == GATHER_WAVES - 1) {
     const int ybase = y.indptr[0];
     int ys = y.indptr[i], ye = y.indptr[i + 1];
     if (ys < ybase || ye > ybase + y.nnz || ye < ys) {
@@ -162,13 +167,31 @@ __global__ __launch_bounds__(256) void k_gather_fwd(
     }
   }
   if (bad) atomicOr(err, bad);
+  __syncthreads();
+  if (wave == 0) {
+    float2 a = part[0][lane];
+#pragma unroll
+    for (int k = 1; k < GATHER_WAVES; ++k) {
+      a.x += part[k][lane].x;
+      a.y += part[k][lane].y;
+    }
+    const float2 bb = *reinterpret_cast<const float2*>(b1 + h0);
+    a.x = bb.x + a.x;
+    a.y = bb.y + a.y;
+    *reinterpret_cast<float2*>(A1 + (size_t)i * HID + h0) = a;
+    const float r0 = fmaxf(a.x, 0.0f), r1 = fmaxf(a.y, 0.0f);
+    H1[(size_t)i * HID + h0] = (E)r0;
+    H1[(size_t)i * HID + h0 + 1] = (E)r1;
+    H1T[(size_t)h0 * ld_t + i] = (E)r0;
+    H1T[(size_t)(h0 + 1) * ld_t + i] = (E)r1;
+  }
 }
 
 hipError_t launch_gather_fwd(bool use_bf16, const CsrDev& x, const CsrDev* y, const float* W1,
                              const float* b1, int F, int L, float* A1, void* H1, void* H1T,
                              int rows_pad, int ld_t, int32_t* keys, int32_t* row_of,
                              int32_t* lrow, float* rw, int32_t* err, int validate, hipStream_t st) {
-  const dim3 grid((rows_pad + 3) / 4), block(256);
+  const dim3 grid(rows_pad), block(64 * GATHER_WAVES);
   CsrDev yy = y ? *y : CsrDev{0, 0, 0, nullptr, nullptr, nullptr};
   if (use_bf16)
     hipLaunchKernelGGL(k_gather_fwd<true>, grid, block, 0, st, x, yy, y != nullptr, W1, b1, F, L,

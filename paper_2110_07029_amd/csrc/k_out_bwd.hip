@@ -1,0 +1,231 @@
+// Output-layer backward and SGD update of W2 / b2 (Sec. 2.1: backward pass,
+// then the update pass), fused so that W2 crosses HBM once in each direction.
+//
+// Work unit = 32 labels (one wavefront).  For each 32-row block of the batch:
+//   Z   = H1 W2_blk^T + b2          (matrix cores, recomputed; logits are never stored)
+//   dZ  = (exp(Z - lse) - T) / B    (T = 1/|Y_i| on true labels, from a bit mask)
+//   dW2_blk^T += H1^T dZ            (dZ fed straight from the accumulators)
+//   db2 += column sums of dZ
+// then W2_blk -= lr dW2_blk and b2 -= lr db2 from the fp32 master values the
+// lane itself loaded (the accumulator-compatible K order makes the lane that
+// loads a weight the lane that owns its gradient).
+//
+// Workgroups are persistent: 8 wavefronts (2 per SIMD) each walk their own
+// sequence of label blocks, so loads of one wave overlap the matrix work of
+// the other with no workgroup barrier inside the loop.  For batches of up to
+// 256 rows with bf16 operands, H1 and H1^T are staged once per workgroup in
+// LDS (padded rows: conflict-free 8-byte fragment reads); otherwise they are
+// read from the L2-resident global copies.
+#include "asgd_dev.h"
+#include "asgd_kernels.h"
+
+namespace asgd {
+
+constexpr int BWD_WAVES = 8;
+constexpr int BWD_STAGE_ROWS = 256;
+constexpr int H1S_LD = HID + 8;             // row-major H1 in LDS (elements)
+constexpr int H1TS_LD = BWD_STAGE_ROWS + 8; // transposed H1 in LDS (elements)
+
+template <bool BF16, bool STAGE>
+__global__ __launch_bounds__(64 * BWD_WAVES) void k_out_bwd(
+    float* __restrict__ W2, float* __restrict__ b2, int L, int F,
+    const typename Mma<BF16>::elem* __restrict__ H1, const typename Mma<BF16>::elem* __restrict__ H1T,
+    int ld_t, int B, const float* __restrict__ lse, const float* __restrict__ rw,
+    const int32_t* __restrict__ skeys, const int32_t* __restrict__ svals, int n_keys,
+    int label_base, const int32_t* __restrict__ lrow, float lr, float invB) {
+  using M = Mma<BF16>;
+  using E = typename M::elem;
+  using Fr = typename M::frag;
+  constexpr int NCH = 32 / M::KC;
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  const int nrb = (B + 31) >> 5;
+  const int bpad = nrb * 32;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, n = lane & 31;
+
+  char* sp = smem_raw;
+  E* h1s = nullptr;
+  E* h1ts = nullptr;
+  if constexpr (STAGE) {
+    h1s = reinterpret_cast<E*>(sp);
+    sp += BWD_STAGE_ROWS * H1S_LD * sizeof(E);
+    h1ts = reinterpret_cast<E*>(sp);
+    sp += HID * H1TS_LD * sizeof(E);
+  }
+  float* lse_s = reinterpret_cast<float*>(sp);
+  sp += bpad * sizeof(float);
+  float* rw_s = reinterpret_cast<float*>(sp);
+  sp += bpad * sizeof(float);
+  uint32_t* mask = reinterpret_cast<uint32_t*>(sp) + wave * 32 * nrb;
+
+  for (int i = tid; i < bpad; i += 64 * BWD_WAVES) {
+    lse_s[i] = i < B ? lse[i] : 0.0f;
+    rw_s[i] = i < B ? rw[i] : 0.0f;
+  }
+  if constexpr (STAGE) {
+    for (int e = tid; e < bpad * 16; e += 64 * BWD_WAVES) {
+      const int r = e >> 4, c = e & 15;
+      *reinterpret_cast<uint4*>(h1s + r * H1S_LD + c * 8) =
+          *reinterpret_cast<const uint4*>(H1 + (size_t)r * HID + c * 8);
+    }
+    const int cpr = bpad >> 3;
+    for (int e = tid; e < HID * cpr; e += 64 * BWD_WAVES) {
+      const int h = e / cpr, c = e - h * cpr;
+      *reinterpret_cast<uint4*>(h1ts + h * H1TS_LD + c * 8) =
+          *reinterpret_cast<const uint4*>(H1T + (size_t)h * ld_t + c * 8);
+    }
+  }
+  __syncthreads();
+  const E* h1 = STAGE ? h1s : H1;
+  const int ldh = STAGE ? H1S_LD : HID;
+  const E* h1t = STAGE ? h1ts : H1T;
+  const int ldht = STAGE ? H1TS_LD : ld_t;
+
+  const int n_blocks = (L + 31) >> 5;
+  for (int blk = blockIdx.x * BWD_WAVES + wave; blk < n_blocks; blk += gridDim.x * BWD_WAVES) {
+    const int l0 = blk * 32;
+    const int label = l0 + n;
+    const bool lvalid = label < L;
+    // W2 rows of this block (fp32 master): hidden 32*kb + 8*q + 4*g + (0..3) per lane
+    // branch-free loads (clamped row, zeroed by a select) keep the wait counters exact
+    float4 wreg[4][4];
+    const float* wrow = W2 + (size_t)min(label, L - 1) * HID;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 v = *reinterpret_cast<const float4*>(wrow + 32 * kb + 8 * q + 4 * g);
+        wreg[kb][q] = make_float4(lvalid ? v.x : 0.f, lvalid ? v.y : 0.f, lvalid ? v.z : 0.f,
+                                  lvalid ? v.w : 0.f);
+      }
+    const float bv = b2[min(label, L - 1)];
+    const float bias = lvalid ? bv : 0.0f;
+
+    // true (row, label) pairs of these 32 labels -> bit mask [label][row block]
+    for (int k = lane; k < 32 * nrb; k += 64) mask[k] = 0u;
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    const int lo = lower_bound_dev(skeys, n_keys, F + l0);
+    const int hi = lower_bound_dev(skeys, n_keys, F + min(l0 + 32, L));
+    for (int q = lo + lane; q < hi; q += 64) {
+      const int row = lrow[svals[q] - label_base];
+      atomicOr(&mask[(skeys[q] - F - l0) * nrb + (row >> 5)], 1u << (row & 31));
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+
+    f32x16 accw[4];
+#pragma unroll
+    for (int hb = 0; hb < 4; ++hb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) accw[hb][r] = 0.0f;
+    float db2p = 0.0f;
+
+    for (int rb = 0; rb < nrb; ++rb) {
+      f32x16 z;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) z[r] = 0.0f;
+      const E* hrow = h1 + (size_t)(rb * 32 + n) * ldh;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+          Fr wb;
+          if constexpr (BF16) {
+            const float4 lo4 = wreg[kb][2 * c], hi4 = wreg[kb][2 * c + 1];
+            wb[0] = (bf16)lo4.x; wb[1] = (bf16)lo4.y; wb[2] = (bf16)lo4.z; wb[3] = (bf16)lo4.w;
+            wb[4] = (bf16)hi4.x; wb[5] = (bf16)hi4.y; wb[6] = (bf16)hi4.z; wb[7] = (bf16)hi4.w;
+          } else {
+            const float4 v = wreg[kb][c >> 2];
+            const float vs[4] = {v.x, v.y, v.z, v.w};
+            wb = vs[c & 3];
+          }
+          z = M::mma(frag_row<BF16>(hrow + 32 * kb, c, g), wb, z);
+        }
+      const uint32_t mw = mask[n * nrb + rb];
+      float dz[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rl = 8 * (r >> 2) + 4 * g + (r & 3);
+        const int row = rb * 32 + rl;
+        float d = 0.0f;
+        if (row < B && lvalid) {
+          const float pr = exp_fast(z[r] + bias - lse_s[row]);
+          const float t = ((mw >> rl) & 1u) ? rw_s[row] : 0.0f;
+          d = (pr - t) * invB;
+        }
+        dz[r] = d;
+        db2p += d;
+      }
+      Fr df[NCH];
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) df[c] = frag_acc<BF16>(dz, c);
+#pragma unroll
+      for (int hb = 0; hb < 4; ++hb) {
+        const E* trow = h1t + (size_t)(32 * hb + n) * ldht + rb * 32;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) accw[hb] = M::mma(frag_row<BF16>(trow, c, g), df[c], accw[hb]);
+      }
+    }
+    const float db2 = db2p + __shfl_xor(db2p, 32);
+    if (lvalid) {
+      float* wout = W2 + (size_t)label * HID;
+#pragma unroll
+      for (int hb = 0; hb < 4; ++hb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 w = wreg[hb][q];
+          float4 o;
+          o.x = fmaf(-lr, accw[hb][4 * q + 0], w.x);
+          o.y = fmaf(-lr, accw[hb][4 * q + 1], w.y);
+          o.z = fmaf(-lr, accw[hb][4 * q + 2], w.z);
+          o.w = fmaf(-lr, accw[hb][4 * q + 3], w.w);
+          *reinterpret_cast<float4*>(wout + 32 * hb + 8 * q + 4 * g) = o;
+        }
+      if (g == 0) b2[label] = fmaf(-lr, db2, bias);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  }
+}
+
+template <bool BF16, bool STAGE>
+static hipError_t launch_bwd(int grid, size_t shm, hipStream_t st, float* W2, float* b2, int L, int F,
+                             const void* H1, const void* H1T, int ld_t, int B, const float* lse,
+                             const float* rw, const int32_t* skeys, const int32_t* svals, int n_keys,
+                             int label_base, const int32_t* lrow, float lr, float invB) {
+  using E = typename Mma<BF16>::elem;
+  static bool attr_done = false;
+  if (!attr_done) {
+    hipError_t e = hipFuncSetAttribute((const void*)k_out_bwd<BF16, STAGE>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr_done = true;
+  }
+  hipLaunchKernelGGL((k_out_bwd<BF16, STAGE>), dim3(grid), dim3(64 * BWD_WAVES), shm, st, W2, b2, L,
+                     F, (const E*)H1, (const E*)H1T, ld_t, B, lse, rw, skeys, svals, n_keys,
+                     label_base, lrow, lr, invB);
+  return hipGetLastError();
+}
+
+hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, int F, const void* H1,
+                          const void* H1T, int ld_t, int B, const float* lse, const float* rw,
+                          const int32_t* skeys, const int32_t* svals, int n_keys, int label_base,
+                          const int32_t* lrow, float lr, int n_cu, hipStream_t st) {
+  const int nrb = (B + 31) / 32;
+  const bool stage = use_bf16 && B <= BWD_STAGE_ROWS;
+  size_t shm = (size_t)2 * nrb * 32 * sizeof(float) + (size_t)BWD_WAVES * 32 * nrb * sizeof(uint32_t);
+  if (stage) shm += (size_t)BWD_STAGE_ROWS * H1S_LD * 2 + (size_t)HID * H1TS_LD * 2;
+  const int n_blocks = (L + 31) / 32;
+  int grid = (n_blocks + BWD_WAVES - 1) / BWD_WAVES;
+  const int cap = stage ? n_cu : 2 * n_cu;
+  if (grid > cap) grid = cap;
+  const float invB = 1.0f / (float)B;
+  if (use_bf16) {
+    if (stage)
+      return launch_bwd<true, true>(grid, shm, st, W2, b2, L, F, H1, H1T, ld_t, B, lse, rw, skeys,
+                                    svals, n_keys, label_base, lrow, lr, invB);
+    return launch_bwd<true, false>(grid, shm, st, W2, b2, L, F, H1, H1T, ld_t, B, lse, rw, skeys,
+                                   svals, n_keys, label_base, lrow, lr, invB);
+  }
+  return launch_bwd<false, false>(grid, shm, st, W2, b2, L, F, H1, H1T, ld_t, B, lse, rw, skeys,
+                                  svals, n_keys, label_base, lrow, lr, invB);
+}
+
+}  // namespace asgd

@@ -11,9 +11,7 @@
 // per-row state (running max, rescale factor) is per lane.
 // Combine (k_out_combine): merges the splits of a row (log-sum-exp, loss,
 // dH1 = (O/s - mean_{y in Y_i} W2[y]) / B, dA1 = dH1 * [A1 > 0]).
-// Backward (k_out_bwd): workgroup = 128 labels; recompute Z per 32-row block,
-// dZ = (softmax - T)/B, dW2 = dZ^T H1, db2 = colsum dZ, and update the fp32
-// master W2 / b2 in place from the registers the lane loaded.
+// The backward with the W2 / b2 update is in k_out_bwd.hip.
 #include <float.h>
 #include <math.h>
 
@@ -26,98 +24,86 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 template <bool BF16>
 struct FwdShape {
-  static constexpr int NB = BF16 ? 2 : 1;     // 32-row blocks per wave
-  static constexpr int RB = 4 * 32 * NB;      // rows per workgroup
+  static constexpr int NB = 1;                // 32-row blocks per wave
+  static constexpr int WAVES = 8;             // wavefronts per workgroup (2 per SIMD)
+  static constexpr int RB = WAVES * 32 * NB;  // rows per workgroup
   static constexpr int WR = BF16 ? 136 : 132; // leading dim of the row-major tile (elements)
   static constexpr int WT = 36;               // leading dim of the transposed tile (elements)
 };
 
 int out_rows_per_block(bool use_bf16) { return use_bf16 ? FwdShape<true>::RB : FwdShape<false>::RB; }
 
-// Cooperative load of one 32-label tile of W2 (fp32 in HBM) by 256 threads:
-// thread t reads hidden chunk 4*(t%32) of labels 2a, 2a+1, 2a+16, 2a+17
-// (a = t/32), so every load instruction reads whole 512-byte label rows.
+// Cooperative load of one 32-label tile of W2 (fp32 in HBM) by 512 threads:
+// thread t reads hidden chunk 4*(t%32) of labels 2a and 2a+1 (a = t/32), so
+// every load instruction reads whole 512-byte label rows and each thread holds
+// a label pair for the transposed LDS copy.
+constexpr int FWD_THREADS = 512;
+
 struct TileRegs {
-  float4 v[4];
+  float4 v[2];
   float bias;
 };
 
 __device__ __forceinline__ void tile_load(const float* __restrict__ W2, const float* __restrict__ b2,
                                           int L, int tile, TileRegs& r) {
+  // Out-of-range labels read the last row (always valid); their values are
+  // zeroed only when the tile is stored to LDS, so nothing consumes the loaded
+  // registers before the prefetch distance has elapsed.
   const int tid = threadIdx.x, a = tid >> 5, q = tid & 31;
 #pragma unroll
-  for (int it = 0; it < 4; ++it) {
-    const int lab = tile * OUT_TILE + 2 * a + (it & 1) + 16 * (it >> 1);
-    r.v[it] = lab < L ? *reinterpret_cast<const float4*>(W2 + (size_t)lab * HID + 4 * q)
-                      : make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int it = 0; it < 2; ++it) {
+    const int lab = tile * OUT_TILE + 2 * a + it;
+    r.v[it] = *reinterpret_cast<const float4*>(W2 + (size_t)min(lab, L - 1) * HID + 4 * q);
   }
-  const int lb = tile * OUT_TILE + tid;
-  r.bias = (tid < OUT_TILE && lb < L) ? b2[lb] : 0.0f;
+  r.bias = b2[min(tile * OUT_TILE + (tid & (OUT_TILE - 1)), L - 1)];
 }
 
 template <bool BF16, bool TRANSPOSED>
-__device__ __forceinline__ void tile_store(const TileRegs& r, typename Mma<BF16>::elem* wr,
+__device__ __forceinline__ void tile_store(const TileRegs& r, int L, int tile,
+                                           typename Mma<BF16>::elem* wr,
                                            typename Mma<BF16>::elem* wt, float* bt) {
   using E = typename Mma<BF16>::elem;
   constexpr int WR = FwdShape<BF16>::WR, WT = FwdShape<BF16>::WT;
   const int tid = threadIdx.x, a = tid >> 5, q = tid & 31;
+  float x[2][4];
 #pragma unroll
-  for (int it = 0; it < 4; ++it) {
-    const int ll = 2 * a + (it & 1) + 16 * (it >> 1);
-    E* d = wr + ll * WR + 4 * q;
+  for (int it = 0; it < 2; ++it) {
+    const bool ok = tile * OUT_TILE + 2 * a + it < L;
+    x[it][0] = ok ? r.v[it].x : 0.0f;
+    x[it][1] = ok ? r.v[it].y : 0.0f;
+    x[it][2] = ok ? r.v[it].z : 0.0f;
+    x[it][3] = ok ? r.v[it].w : 0.0f;
+    E* d = wr + (2 * a + it) * WR + 4 * q;
     if constexpr (BF16) {
       bf16x4 p;
-      p[0] = (bf16)r.v[it].x; p[1] = (bf16)r.v[it].y; p[2] = (bf16)r.v[it].z; p[3] = (bf16)r.v[it].w;
+      p[0] = (bf16)x[it][0]; p[1] = (bf16)x[it][1]; p[2] = (bf16)x[it][2]; p[3] = (bf16)x[it][3];
       *reinterpret_cast<bf16x4*>(d) = p;
     } else {
-      *reinterpret_cast<float4*>(d) = r.v[it];
+      *reinterpret_cast<float4*>(d) = make_float4(x[it][0], x[it][1], x[it][2], x[it][3]);
     }
   }
   if constexpr (TRANSPOSED) {
 #pragma unroll
-    for (int pr = 0; pr < 2; ++pr) {
-      const int ll = 2 * a + 16 * pr;  // even label of the pair
-      const float4 x0 = r.v[2 * pr], x1 = r.v[2 * pr + 1];
-      const float a0[4] = {x0.x, x0.y, x0.z, x0.w}, a1[4] = {x1.x, x1.y, x1.z, x1.w};
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        E* d = wt + (4 * q + k) * WT + ll;
-        if constexpr (BF16) {
-          bf16x2 p;
-          p[0] = (bf16)a0[k];
-          p[1] = (bf16)a1[k];
-          *reinterpret_cast<bf16x2*>(d) = p;
-        } else {
-          *reinterpret_cast<float2*>(d) = make_float2(a0[k], a1[k]);
-        }
+    for (int k = 0; k < 4; ++k) {
+      E* d = wt + (4 * q + k) * WT + 2 * a;
+      if constexpr (BF16) {
+        bf16x2 p;
+        p[0] = (bf16)x[0][k];
+        p[1] = (bf16)x[1][k];
+        *reinterpret_cast<bf16x2*>(d) = p;
+      } else {
+        *reinterpret_cast<float2*>(d) = make_float2(x[0][k], x[1][k]);
       }
     }
   }
-  if (threadIdx.x < OUT_TILE) bt[threadIdx.x] = r.bias;
-}
-
-template <bool BF16>
-__device__ __forceinline__ typename Mma<BF16>::frag frag_row(const typename Mma<BF16>::elem* p,
-                                                             int c, int g) {
-  if constexpr (BF16)
-    return frag_row_bf16(p, c, g);
-  else
-    return frag_row_f32(p, c, g);
-}
-
-template <bool BF16>
-__device__ __forceinline__ typename Mma<BF16>::frag frag_acc(const float* v, int c) {
-  if constexpr (BF16)
-    return frag_acc_bf16(v, c);
-  else
-    return v[c];
+  if (threadIdx.x < OUT_TILE) bt[threadIdx.x] = tile * OUT_TILE + (int)threadIdx.x < L ? r.bias : 0.0f;
 }
 
 // ---------------------------------------------------------------------------
 // Forward, training: per (split, row) partial max, sum of exponentials and O.
 // ---------------------------------------------------------------------------
 template <bool BF16>
-__global__ __launch_bounds__(256, 1) void k_out_fwd_train(
+__global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
     const float* __restrict__ W2, const float* __restrict__ b2, int L,
     const typename Mma<BF16>::elem* __restrict__ H1, int B, int tiles_per_split, int n_tiles,
     float* __restrict__ m_part, float* __restrict__ s_part, float* __restrict__ o_part,
@@ -149,6 +135,15 @@ __global__ __launch_bounds__(256, 1) void k_out_fwd_train(
 #pragma unroll
       for (int c = 0; c < NCH; ++c) hf[nb][kb][c] = frag_row<BF16>(hrow + 32 * kb, c, g);
   }
+  // Redefine the fragments once they have arrived (empty asm), so the loop below
+  // never waits on these loads again and its wait counters track only the W2
+  // prefetch.
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) asm volatile("" : "+v"(hf[nb][kb][c]));
 
   float m_run[NB], s_run[NB];
   f32x16 acc_o[NB][4];
@@ -162,78 +157,90 @@ __global__ __launch_bounds__(256, 1) void k_out_fwd_train(
       for (int r = 0; r < 16; ++r) acc_o[nb][hb][r] = 0.0f;
   }
 
-  TileRegs tr;
-  if (t_begin < t_end) {
-    tile_load(W2, b2, L, t_begin, tr);
-    tile_store<BF16, true>(tr, wr[0], wt[0], bt[0]);
-  }
+  // Two tiles in flight: tile i+2 is loaded into registers while tile i is
+  // computed from LDS and tile i+1 (loaded one iteration earlier) is stored.
+  // The loop is unrolled by two so the register buffers are static.
+  TileRegs tr0, tr1;
+  // every split has at least one tile (the host sizes splits that way)
+  tile_load(W2, b2, L, t_begin, tr0);
+  tile_store<BF16, true>(tr0, L, t_begin, wr[0], wt[0], bt[0]);
+  tile_load(W2, b2, L, min(t_begin + 1, t_end - 1), tr1);
   __syncthreads();
 
-  for (int t = t_begin; t < t_end; ++t) {
-    const int buf = (t - t_begin) & 1;
-    const bool has_next = t + 1 < t_end;
-    if (has_next) tile_load(W2, b2, L, t + 1, tr);
-    if (active) {
-      const E* wrb = wr[buf];
-      const E* wtb = wt[buf];
-      // Z^T tile: A = W2 rows (M = labels, K = hidden), B = H1^T.
-      f32x16 z[NB];
+  auto compute = [&](int t, int buf) {
+    const E* wrb = wr[buf];
+    const E* wtb = wt[buf];
+    // Z^T tile: A = W2 rows (M = labels, K = hidden), B = H1^T.
+    f32x16 z[NB];
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) z[nb][r] = 0.0f;
+      for (int r = 0; r < 16; ++r) z[nb][r] = 0.0f;
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
+    for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-          const Fr a = frag_row<BF16>(wrb + n * WR + 32 * kb, c, g);
+      for (int c = 0; c < NCH; ++c) {
+        const Fr a = frag_row<BF16>(wrb + n * WR + 32 * kb, c, g);
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) z[nb] = M::mma(a, hf[nb][kb][c], z[nb]);
-        }
-      // bias, label mask, online softmax; probabilities become the K operand of O^T.
-      Fr pf[NB][NCH];
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        float zz[16];
-        float tmax = -INFINITY;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int ll = 8 * (r >> 2) + 4 * g + (r & 3);
-          zz[r] = (t * OUT_TILE + ll < L) ? z[nb][r] + bt[buf][ll] : -INFINITY;
-          tmax = fmaxf(tmax, zz[r]);
-        }
-        tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-        const float mnew = fmaxf(m_run[nb], tmax);
-        const float scale = exp_fast(m_run[nb] - mnew);
-        float p[16];
-        float ps = 0.0f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          p[r] = exp_fast(zz[r] - mnew);
-          ps += p[r];
-        }
-        s_run[nb] = s_run[nb] * scale + ps;
-        if (__any(mnew > m_run[nb])) {
-#pragma unroll
-          for (int hb = 0; hb < 4; ++hb)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc_o[nb][hb][r] *= scale;
-        }
-        m_run[nb] = mnew;
-#pragma unroll
-        for (int c = 0; c < NCH; ++c) pf[nb][c] = frag_acc<BF16>(p, c);
+        for (int nb = 0; nb < NB; ++nb) z[nb] = M::mma(a, hf[nb][kb][c], z[nb]);
       }
-      // O^T += W2_tile^T P^T : A = W2^T rows (M = hidden, K = labels).
+    // bias, label mask, online softmax; probabilities become the K operand of O^T.
+    Fr pf[NB][NCH];
 #pragma unroll
-      for (int hb = 0; hb < 4; ++hb)
+    for (int nb = 0; nb < NB; ++nb) {
+      float zz[16];
+      float tmax = -INFINITY;
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-          const Fr a = frag_row<BF16>(wtb + (32 * hb + n) * WT, c, g);
+      for (int r = 0; r < 16; ++r) {
+        const int ll = 8 * (r >> 2) + 4 * g + (r & 3);
+        zz[r] = (t * OUT_TILE + ll < L) ? z[nb][r] + bt[buf][ll] : -INFINITY;
+        tmax = fmaxf(tmax, zz[r]);
+      }
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+      const float mnew = fmaxf(m_run[nb], tmax);
+      const float scale = exp_fast(m_run[nb] - mnew);
+      float p[16];
+      float ps = 0.0f;
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) acc_o[nb][hb] = M::mma(a, pf[nb][c], acc_o[nb][hb]);
-        }
+      for (int r = 0; r < 16; ++r) {
+        p[r] = exp_fast(zz[r] - mnew);
+        ps += p[r];
+      }
+      s_run[nb] = s_run[nb] * scale + ps;
+      if (__any(mnew > m_run[nb])) {
+#pragma unroll
+        for (int hb = 0; hb < 4; ++hb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc_o[nb][hb][r] *= scale;
+      }
+      m_run[nb] = mnew;
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) pf[nb][c] = frag_acc<BF16>(p, c);
     }
-    if (has_next) tile_store<BF16, true>(tr, wr[buf ^ 1], wt[buf ^ 1], bt[buf ^ 1]);
+    // O^T += W2_tile^T P^T : A = W2^T rows (M = hidden, K = labels).
+#pragma unroll
+    for (int hb = 0; hb < 4; ++hb)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        const Fr a = frag_row<BF16>(wtb + (32 * hb + n) * WT, c, g);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc_o[nb][hb] = M::mma(a, pf[nb][c], acc_o[nb][hb]);
+      }
+  };
+
+  // Loads and stores are unconditional (tile index clamped to the last tile; a
+  // redundant copy lands in the buffer nobody reads next), so no branch sits
+  // between a prefetch and its use.
+  const int t_last = t_end - 1;
+  for (int t = t_begin; t < t_end; t += 2) {
+    tile_load(W2, b2, L, min(t + 2, t_last), tr0);
+    if (active) compute(t, 0);
+    tile_store<BF16, true>(tr1, L, min(t + 1, t_last), wr[1], wt[1], bt[1]);
+    __syncthreads();
+    if (t + 1 >= t_end) break;
+    tile_load(W2, b2, L, min(t + 3, t_last), tr1);
+    if (active) compute(t + 1, 1);
+    tile_store<BF16, true>(tr0, L, min(t + 2, t_last), wr[0], wt[0], bt[0]);
     __syncthreads();
   }
 
@@ -267,7 +274,7 @@ hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2,
   const int tps = (n_tiles + splits - 1) / splits;
   const int s_eff = (n_tiles + tps - 1) / tps;
   const int RB = out_rows_per_block(use_bf16);
-  const dim3 grid(s_eff, (B + RB - 1) / RB), block(256);
+  const dim3 grid(s_eff, (B + RB - 1) / RB), block(FWD_THREADS);
   if (use_bf16)
     hipLaunchKernelGGL(k_out_fwd_train<true>, grid, block, 0, st, W2, b2, L, (const bf16*)H1, B,
                        tps, n_tiles, m_part, s_part, o_part, ld_part);
@@ -278,64 +285,103 @@ hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2,
 }
 
 // ---------------------------------------------------------------------------
-// Sum over the 128 threads of a workgroup in a fixed order.
+// Per row: merge the splits, log-sum-exp, loss, dA1.  512 threads = 4 split
+// groups x 128 hidden units for the softmax-weighted sums, 8 wavefronts x
+// the row's labels for the target terms; every partial is combined in a fixed
+// order, so the result does not depend on scheduling.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float block_sum_128(float v, float* red) {
-  v = wave_sum(v);
-  const int w = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) red[w] = v;
-  __syncthreads();
-  const float t = red[0] + red[1];
-  __syncthreads();
-  return t;
-}
+constexpr int CMB_THREADS = 512;
+constexpr int CMB_GROUPS = CMB_THREADS / HID;  // 4
+constexpr int CMB_WAVES = CMB_THREADS / 64;    // 8
 
-// ---------------------------------------------------------------------------
-// Per row: merge the splits, log-sum-exp, loss, dA1.
-// ---------------------------------------------------------------------------
 template <bool BF16>
-__global__ __launch_bounds__(128) void k_out_combine(
+__global__ __launch_bounds__(CMB_THREADS) void k_out_combine(
     int B, int splits, const float* __restrict__ m_part, const float* __restrict__ s_part,
     const float* __restrict__ o_part, int ld_part, const float* __restrict__ W2,
     const float* __restrict__ b2, int L, const typename Mma<BF16>::elem* __restrict__ H1,
     const float* __restrict__ A1, CsrDev y, int has_y, float invB, float* __restrict__ lse_out,
     float* __restrict__ loss_rows, float* __restrict__ dA1) {
-  __shared__ float red[2];
-  const int i = blockIdx.x, h = threadIdx.x;
-  float M = -INFINITY;
-  for (int s = 0; s < splits; ++s) M = fmaxf(M, m_part[(size_t)s * ld_part + i]);
+  __shared__ float red_o[CMB_GROUPS][HID];
+  __shared__ float red_s[CMB_GROUPS];
+  __shared__ float red_m[CMB_WAVES];
+  __shared__ float red_t[CMB_WAVES][HID];
+  __shared__ float red_z[CMB_WAVES];
+  const int i = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int h = t & (HID - 1), grp = t >> 7;
+
+  float mloc = -INFINITY;
+  for (int s = t; s < splits; s += CMB_THREADS) mloc = fmaxf(mloc, m_part[(size_t)s * ld_part + i]);
+  mloc = wave_max(mloc);
+  if (lane == 0) red_m[w] = mloc;
+  __syncthreads();
+  float M = red_m[0];
+#pragma unroll
+  for (int k = 1; k < CMB_WAVES; ++k) M = fmaxf(M, red_m[k]);
+
   float St = 0.0f, O = 0.0f;
-  for (int s = 0; s < splits; ++s) {
-    const float e = exp_fast(m_part[(size_t)s * ld_part + i] - M);
-    St = fmaf(e, s_part[(size_t)s * ld_part + i], St);
-    O = fmaf(e, o_part[((size_t)s * ld_part + i) * HID + h], O);
+#pragma unroll 4
+  for (int s = grp; s < splits; s += CMB_GROUPS) {
+    const size_t r = (size_t)s * ld_part + i;
+    const float e = exp_fast(m_part[r] - M);
+    St = fmaf(e, s_part[r], St);
+    O = fmaf(e, o_part[r * HID + h], O);
   }
-  const float lse = M + logf(St);
-  if (h == 0) lse_out[i] = lse;
-  if (!has_y) return;
-  const int ybase = y.indptr[0];
-  int ys = y.indptr[i], ye = y.indptr[i + 1];
-  ys = max(ys, ybase);
-  ye = min(ye, ybase + y.nnz);
-  if (ye < ys) ye = ys;
-  const float hv = (float)H1[(size_t)i * HID + h];
-  float tw = 0.0f, zsum = 0.0f;
+  red_o[grp][h] = O;
+  if (h == 0) red_s[grp] = St;
+
+  // target terms: wave w takes labels q = w, w + 8, ... of row i; lane owns hidden 2l, 2l+1
+  float tw0 = 0.0f, tw1 = 0.0f, zw = 0.0f;
   int cnt = 0;
-  for (int q = ys; q < ye; ++q) {
-    const int lab = y.indices[q];
-    if (lab < 0 || lab >= L) continue;
-    ++cnt;
-    const float w = W2[(size_t)lab * HID + h];
-    tw += w;
-    float wop = w;
-    if constexpr (BF16) wop = (float)(bf16)w;
-    const float z = block_sum_128(hv * wop, red);
-    zsum += z + b2[lab];
+  if (has_y) {
+    const int ybase = y.indptr[0];
+    int ys = y.indptr[i], ye = y.indptr[i + 1];
+    ys = max(ys, ybase);
+    ye = min(ye, ybase + y.nnz);
+    if (ye < ys) ye = ys;
+    const float h0 = (float)H1[(size_t)i * HID + 2 * lane];
+    const float h1v = (float)H1[(size_t)i * HID + 2 * lane + 1];
+    for (int q = ys; q < ye; ++q) {
+      const int lab = y.indices[q];
+      if (lab < 0 || lab >= L) continue;
+      ++cnt;
+      if (((q - ys) & (CMB_WAVES - 1)) != w) continue;
+      const float2 wv = *reinterpret_cast<const float2*>(W2 + (size_t)lab * HID + 2 * lane);
+      tw0 += wv.x;
+      tw1 += wv.y;
+      float o0 = wv.x, o1 = wv.y;
+      if constexpr (BF16) {
+        o0 = (float)(bf16)wv.x;
+        o1 = (float)(bf16)wv.y;
+      }
+      zw += wave_sum(fmaf(h0, o0, h1v * o1)) + b2[lab];
+    }
+    red_t[w][2 * lane] = tw0;
+    red_t[w][2 * lane + 1] = tw1;
+    if (lane == 0) red_z[w] = zw;
   }
-  const float inv_cnt = cnt > 0 ? 1.0f / (float)cnt : 0.0f;
-  const float dh = (O / St - tw * inv_cnt) * invB;
-  dA1[(size_t)i * HID + h] = A1[(size_t)i * HID + h] > 0.0f ? dh : 0.0f;
-  if (h == 0) loss_rows[i] = lse - zsum * inv_cnt;
+  __syncthreads();
+  if (t < HID) {
+    float Ot = red_o[0][t], Stot = red_s[0];
+#pragma unroll
+    for (int k = 1; k < CMB_GROUPS; ++k) {
+      Ot += red_o[k][t];
+      Stot += red_s[k];
+    }
+    const float lse = M + logf(Stot);
+    if (t == 0) lse_out[i] = lse;
+    if (has_y) {
+      float tw = red_t[0][t], zs = red_z[0];
+#pragma unroll
+      for (int k = 1; k < CMB_WAVES; ++k) {
+        tw += red_t[k][t];
+        zs += red_z[k];
+      }
+      const float inv_cnt = cnt > 0 ? 1.0f / (float)cnt : 0.0f;
+      const float dh = (Ot / Stot - tw * inv_cnt) * invB;
+      dA1[(size_t)i * HID + t] = A1[(size_t)i * HID + t] > 0.0f ? dh : 0.0f;
+      if (t == 0) loss_rows[i] = lse - zs * inv_cnt;
+    }
+  }
 }
 
 hipError_t launch_out_combine(bool use_bf16, int B, int splits, const float* m_part,
@@ -346,201 +392,53 @@ hipError_t launch_out_combine(bool use_bf16, int B, int splits, const float* m_p
   CsrDev yy = y ? *y : CsrDev{0, 0, 0, nullptr, nullptr, nullptr};
   const float invB = 1.0f / (float)B;
   if (use_bf16)
-    hipLaunchKernelGGL(k_out_combine<true>, dim3(B), dim3(128), 0, st, B, splits, m_part, s_part,
-                       o_part, ld_part, W2, b2, L, (const bf16*)H1, A1, yy, y != nullptr, invB,
-                       lse, loss_rows, dA1);
+    hipLaunchKernelGGL(k_out_combine<true>, dim3(B), dim3(CMB_THREADS), 0, st, B, splits, m_part,
+                       s_part, o_part, ld_part, W2, b2, L, (const bf16*)H1, A1, yy, y != nullptr,
+                       invB, lse, loss_rows, dA1);
   else
-    hipLaunchKernelGGL(k_out_combine<false>, dim3(B), dim3(128), 0, st, B, splits, m_part, s_part,
-                       o_part, ld_part, W2, b2, L, (const float*)H1, A1, yy, y != nullptr, invB,
-                       lse, loss_rows, dA1);
+    hipLaunchKernelGGL(k_out_combine<false>, dim3(B), dim3(CMB_THREADS), 0, st, B, splits, m_part,
+                       s_part, o_part, ld_part, W2, b2, L, (const float*)H1, A1, yy, y != nullptr,
+                       invB, lse, loss_rows, dA1);
   return hipGetLastError();
 }
 
-// db1 = sum_i dA1[i, :] (fixed order); b1 -= lr db1; mean loss.
-__global__ __launch_bounds__(128) void k_hidden_bias(int B, const float* __restrict__ dA1,
-                                                     float* __restrict__ b1, float lr,
-                                                     const float* __restrict__ loss_rows,
-                                                     float* __restrict__ loss) {
-  __shared__ float red[2];
-  const int h = threadIdx.x;
+// db1 = sum_i dA1[i, :] and the mean loss, 8 row groups x 128 hidden units,
+// groups combined in a fixed order; then b1 -= lr db1.
+constexpr int HB_THREADS = 1024;
+constexpr int HB_GROUPS = HB_THREADS / HID;  // 8
+
+__global__ __launch_bounds__(HB_THREADS) void k_hidden_bias(int B, const float* __restrict__ dA1,
+                                                            float* __restrict__ b1, float lr,
+                                                            const float* __restrict__ loss_rows,
+                                                            float* __restrict__ loss) {
+  __shared__ float red[HB_GROUPS][HID];
+  __shared__ float red_l[HB_THREADS / 64];
+  const int t = threadIdx.x, h = t & (HID - 1), grp = t >> 7;
   float s = 0.0f;
-  for (int i = 0; i < B; ++i) s += dA1[(size_t)i * HID + h];
-  b1[h] = fmaf(-lr, s, b1[h]);
+#pragma unroll 4
+  for (int i = grp; i < B; i += HB_GROUPS) s += dA1[(size_t)i * HID + h];
+  red[grp][h] = s;
   float ls = 0.0f;
-  for (int i = h; i < B; i += 128) ls += loss_rows[i];
-  const float tot = block_sum_128(ls, red);
-  if (h == 0) *loss = tot / (float)B;
+  for (int i = t; i < B; i += HB_THREADS) ls += loss_rows[i];
+  ls = wave_sum(ls);
+  if ((t & 63) == 0) red_l[t >> 6] = ls;
+  __syncthreads();
+  if (t < HID) {
+    float tot = red[0][t];
+#pragma unroll
+    for (int k = 1; k < HB_GROUPS; ++k) tot += red[k][t];
+    b1[t] = fmaf(-lr, tot, b1[t]);
+  }
+  if (t == 0) {
+    float l = red_l[0];
+    for (int k = 1; k < HB_THREADS / 64; ++k) l += red_l[k];
+    *loss = l / (float)B;
+  }
 }
 
 hipError_t launch_hidden_bias(int B, const float* dA1, float* b1, float lr, const float* loss_rows,
                               float* loss, hipStream_t st) {
-  hipLaunchKernelGGL(k_hidden_bias, dim3(1), dim3(128), 0, st, B, dA1, b1, lr, loss_rows, loss);
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------------------
-// Backward + update of W2 and b2.
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ int lower_bound_dev(const int32_t* __restrict__ a, int n, int key) {
-  int lo = 0, hi = n;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (a[mid] < key)
-      lo = mid + 1;
-    else
-      hi = mid;
-  }
-  return lo;
-}
-
-template <bool BF16>
-__global__ __launch_bounds__(256) void k_out_bwd(
-    float* __restrict__ W2, float* __restrict__ b2, int L, int F,
-    const typename Mma<BF16>::elem* __restrict__ H1, const typename Mma<BF16>::elem* __restrict__ H1T,
-    int ld_t, int B, const float* __restrict__ lse, const float* __restrict__ rw,
-    const int32_t* __restrict__ skeys, const int32_t* __restrict__ svals, int n_keys,
-    int label_base, const int32_t* __restrict__ lrow, float lr, float invB) {
-  using M = Mma<BF16>;
-  using E = typename M::elem;
-  using Fr = typename M::frag;
-  constexpr int NCH = 32 / M::KC;
-  extern __shared__ float smem[];
-  const int nrb = (B + 31) >> 5;
-  const int bpad = nrb * 32;
-  float* lse_s = smem;
-  float* rw_s = smem + bpad;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, g = lane >> 5, n = lane & 31;
-  uint32_t* mask = reinterpret_cast<uint32_t*>(smem + 2 * bpad) + wave * 32 * nrb;
-
-  for (int i = threadIdx.x; i < bpad; i += 256) {
-    lse_s[i] = i < B ? lse[i] : 0.0f;
-    rw_s[i] = i < B ? rw[i] : 0.0f;
-  }
-  for (int k = lane; k < 32 * nrb; k += 64) mask[k] = 0u;
-  __syncthreads();
-
-  const int l0 = blockIdx.x * 128 + wave * 32;
-  // true (row, label) pairs of this wave's 32 labels -> bit mask [label][row]
-  if (l0 < L) {
-    const int lo = lower_bound_dev(skeys, n_keys, F + l0);
-    const int hi = lower_bound_dev(skeys, n_keys, F + min(l0 + 32, L));
-    for (int q = lo + lane; q < hi; q += 64) {
-      const int e = svals[q] - label_base;
-      const int row = lrow[e];
-      const int ll = skeys[q] - F - l0;
-      atomicOr(&mask[ll * nrb + (row >> 5)], 1u << (row & 31));
-    }
-  }
-  __syncthreads();
-
-  const int label = l0 + n;
-  const bool lvalid = label < L;
-  // The 64 fp32 weights of this lane: hidden 32*kb + 8*q + 4*g + (0..3).
-  float4 wreg[4][4];
-  const float* wrow = W2 + (size_t)(lvalid ? label : 0) * HID;
-#pragma unroll
-  for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      wreg[kb][q] = lvalid ? *reinterpret_cast<const float4*>(wrow + 32 * kb + 8 * q + 4 * g)
-                           : make_float4(0.f, 0.f, 0.f, 0.f);
-  const float bias = lvalid ? b2[label] : 0.0f;
-  Fr wf[4][NCH];
-#pragma unroll
-  for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      if constexpr (BF16) {
-        const float4 lo = wreg[kb][2 * c], hi = wreg[kb][2 * c + 1];
-        Fr f;
-        f[0] = (bf16)lo.x; f[1] = (bf16)lo.y; f[2] = (bf16)lo.z; f[3] = (bf16)lo.w;
-        f[4] = (bf16)hi.x; f[5] = (bf16)hi.y; f[6] = (bf16)hi.z; f[7] = (bf16)hi.w;
-        wf[kb][c] = f;
-      } else {
-        const float4 v = wreg[kb][c >> 2];
-        const float vs[4] = {v.x, v.y, v.z, v.w};
-        wf[kb][c] = vs[c & 3];
-      }
-    }
-
-  f32x16 accw[4];
-#pragma unroll
-  for (int hb = 0; hb < 4; ++hb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) accw[hb][r] = 0.0f;
-  float db2p = 0.0f;
-
-  for (int rb = 0; rb < nrb; ++rb) {
-    // Z block: A = H1 rows (M = rows, K = hidden), B = W2^T.
-    f32x16 z;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) z[r] = 0.0f;
-    const E* hrow = H1 + (size_t)(rb * 32 + n) * HID;
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-      for (int c = 0; c < NCH; ++c) z = M::mma(frag_row<BF16>(hrow + 32 * kb, c, g), wf[kb][c], z);
-    const uint32_t mw = mask[n * nrb + rb];
-    float dz[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int rl = 8 * (r >> 2) + 4 * g + (r & 3);
-      const int row = rb * 32 + rl;
-      float d = 0.0f;
-      if (row < B && lvalid) {
-        const float p = exp_fast(z[r] + bias - lse_s[row]);
-        const float t = ((mw >> rl) & 1u) ? rw_s[row] : 0.0f;
-        d = (p - t) * invB;
-      }
-      dz[r] = d;
-      db2p += d;
-    }
-    // dW2^T += H1^T dZ : A = H1^T rows (M = hidden, K = rows), B = dZ from the accumulators.
-    Fr df[NCH];
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) df[c] = frag_acc<BF16>(dz, c);
-#pragma unroll
-    for (int hb = 0; hb < 4; ++hb) {
-      const E* trow = H1T + (size_t)(32 * hb + n) * ld_t + rb * 32;
-#pragma unroll
-      for (int c = 0; c < NCH; ++c) accw[hb] = M::mma(frag_row<BF16>(trow, c, g), df[c], accw[hb]);
-    }
-  }
-  const float db2 = db2p + __shfl_xor(db2p, 32);
-  if (lvalid) {
-    float* wout = W2 + (size_t)label * HID;
-#pragma unroll
-    for (int hb = 0; hb < 4; ++hb)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float4 w = wreg[hb][q];
-        float4 o;
-        o.x = fmaf(-lr, accw[hb][4 * q + 0], w.x);
-        o.y = fmaf(-lr, accw[hb][4 * q + 1], w.y);
-        o.z = fmaf(-lr, accw[hb][4 * q + 2], w.z);
-        o.w = fmaf(-lr, accw[hb][4 * q + 3], w.w);
-        *reinterpret_cast<float4*>(wout + 32 * hb + 8 * q + 4 * g) = o;
-      }
-    if (g == 0) b2[label] = fmaf(-lr, db2, bias);
-  }
-}
-
-hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, int F, const void* H1,
-                          const void* H1T, int ld_t, int B, const float* lse, const float* rw,
-                          const int32_t* skeys, const int32_t* svals, int n_keys, int label_base,
-                          const int32_t* lrow, float lr, hipStream_t st) {
-  const int nrb = (B + 31) / 32;
-  const size_t shm = (size_t)(2 * nrb * 32) * sizeof(float) + (size_t)4 * 32 * nrb * sizeof(uint32_t);
-  const dim3 grid((L + 127) / 128), block(256);
-  const float invB = 1.0f / (float)B;
-  if (use_bf16)
-    hipLaunchKernelGGL(k_out_bwd<true>, grid, block, shm, st, W2, b2, L, F, (const bf16*)H1,
-                       (const bf16*)H1T, ld_t, B, lse, rw, skeys, svals, n_keys, label_base, lrow,
-                       lr, invB);
-  else
-    hipLaunchKernelGGL(k_out_bwd<false>, grid, block, shm, st, W2, b2, L, F, (const float*)H1,
-                       (const float*)H1T, ld_t, B, lse, rw, skeys, svals, n_keys, label_base, lrow,
-                       lr, invB);
+  hipLaunchKernelGGL(k_hidden_bias, dim3(1), dim3(HB_THREADS), 0, st, B, dA1, b1, lr, loss_rows, loss);
   return hipGetLastError();
 }
 
@@ -554,7 +452,7 @@ __device__ __forceinline__ bool better(float s, int i, float ts, int ti) {
 }
 
 template <bool BF16>
-__global__ __launch_bounds__(256, 1) void k_out_fwd_topk(
+__global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_topk(
     const float* __restrict__ W2, const float* __restrict__ b2, int L,
     const typename Mma<BF16>::elem* __restrict__ H1, int B, int tiles_per_split, int n_tiles,
     int k, float* __restrict__ part_s, int32_t* __restrict__ part_i, int ld_part) {
@@ -567,8 +465,8 @@ __global__ __launch_bounds__(256, 1) void k_out_fwd_topk(
   constexpr int WROWS = 32 * NB;
   __shared__ __attribute__((aligned(16))) E wr[2][OUT_TILE * WR];
   __shared__ float bt[2][OUT_TILE];
-  __shared__ float ls[4][WROWS][TOPK_MAX];
-  __shared__ int li[4][WROWS][TOPK_MAX];
+  __shared__ float ls[FwdShape<BF16>::WAVES][WROWS][TOPK_MAX];
+  __shared__ int li[FwdShape<BF16>::WAVES][WROWS][TOPK_MAX];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, g = lane >> 5, n = lane & 31;
   const int split = blockIdx.x;
@@ -593,7 +491,7 @@ __global__ __launch_bounds__(256, 1) void k_out_fwd_topk(
   TileRegs tr;
   if (t_begin < t_end) {
     tile_load(W2, b2, L, t_begin, tr);
-    tile_store<BF16, false>(tr, wr[0], nullptr, bt[0]);
+    tile_store<BF16, false>(tr, L, t_begin, wr[0], nullptr, bt[0]);
   }
   __syncthreads();
   for (int t = t_begin; t < t_end; ++t) {
@@ -643,7 +541,7 @@ __global__ __launch_bounds__(256, 1) void k_out_fwd_topk(
         }
       }
     }
-    if (has_next) tile_store<BF16, false>(tr, wr[buf ^ 1], nullptr, bt[buf ^ 1]);
+    if (has_next) tile_store<BF16, false>(tr, L, t + 1, wr[buf ^ 1], nullptr, bt[buf ^ 1]);
     __syncthreads();
   }
   if (active) {
@@ -674,7 +572,7 @@ hipError_t launch_out_fwd_topk(bool use_bf16, const float* W2, const float* b2, 
   const int tps = (n_tiles + splits - 1) / splits;
   const int s_eff = (n_tiles + tps - 1) / tps;
   const int RB = out_rows_per_block(use_bf16);
-  const dim3 grid(s_eff, (B + RB - 1) / RB), block(256);
+  const dim3 grid(s_eff, (B + RB - 1) / RB), block(FWD_THREADS);
   if (use_bf16)
     hipLaunchKernelGGL(k_out_fwd_topk<true>, grid, block, 0, st, W2, b2, L, (const bf16*)H1, B,
                        tps, n_tiles, k, part_s, part_i, ld_part);

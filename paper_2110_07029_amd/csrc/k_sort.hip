@@ -5,7 +5,7 @@
 // tile can find its true labels with a binary search.
 //
 // One pass over a digit of up to 11 bits = three launches:
-//   hist    : per-workgroup digit counts of a 2048-key chunk (LDS counters)
+//   hist    : per-workgroup digit counts of a 1024-key chunk (LDS counters)
 //   scan    : exclusive scan over (digit, workgroup) -> global scatter offsets
 //   scatter : stable ranks inside the chunk from 64-lane ballots (lanes with the
 //             same digit in one wave), per-wave running counts, then a prefix
@@ -17,8 +17,8 @@ namespace asgd {
 
 constexpr int SORT_THREADS = 256;
 constexpr int SORT_WAVES = SORT_THREADS / 64;
-constexpr int SORT_PER_WAVE = SORT_CHUNK / SORT_WAVES;  // 512
-constexpr int SORT_ITERS = SORT_PER_WAVE / 64;         // 8
+constexpr int SORT_PER_WAVE = SORT_CHUNK / SORT_WAVES;  // 256
+constexpr int SORT_ITERS = SORT_PER_WAVE / 64;         // 4
 
 int sort_blocks(int n) { return (n + SORT_CHUNK - 1) / SORT_CHUNK; }
 
@@ -38,37 +38,53 @@ __global__ __launch_bounds__(SORT_THREADS) void k_sort_hist(const int32_t* __res
   for (int d = threadIdx.x; d < nd; d += SORT_THREADS) hist[d * nblk + blockIdx.x] = cnt[d];
 }
 
-// Exclusive prefix sum of hist[0..total) by one workgroup, 1024 entries per round.
-__global__ __launch_bounds__(1024) void k_sort_scan(const int32_t* __restrict__ hist, int total,
-                                                    int32_t* __restrict__ offs) {
-  __shared__ int wsum[16];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int carry = 0;
-  for (int base = 0; base < total; base += 1024) {
-    const int idx = base + threadIdx.x;
-    const int v = idx < total ? hist[idx] : 0;
-    int x = v;
+// Scatter offsets offs[d * nblk + b] = (keys with a smaller digit) + (keys with
+// digit d in earlier chunks), by one workgroup: thread t owns digits 2t, 2t+1
+// and their nblk chunk counts; one block-wide exclusive scan of the per-thread
+// totals gives every digit's base.
+constexpr int SCAN_THREADS = 1024;
+constexpr int SCAN_DPT = (1 << SORT_MAX_BITS) / SCAN_THREADS;  // digits per thread
+
+__global__ __launch_bounds__(SCAN_THREADS) void k_sort_scan(const int32_t* __restrict__ hist,
+                                                            int nblk, int ndig,
+                                                            int32_t* __restrict__ offs) {
+  __shared__ int wsum[SCAN_THREADS / 64];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  int local = 0;
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(x, o);
-      if (lane >= o) x += y;
+  for (int k = 0; k < SCAN_DPT; ++k) {
+    const int d = SCAN_DPT * t + k;
+    if (d < ndig)
+      for (int b = 0; b < nblk; ++b) local += hist[d * nblk + b];
+  }
+  int x = local;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[w] = x;
+  __syncthreads();
+  if (w == 0) {
+    int s = lane < SCAN_THREADS / 64 ? wsum[lane] : 0;
+#pragma unroll
+    for (int o = 1; o < SCAN_THREADS / 64; o <<= 1) {
+      const int y = __shfl_up(s, o);
+      if (lane >= o) s += y;
     }
-    if (lane == 63) wsum[w] = x;
-    __syncthreads();
-    if (w == 0) {
-      int s = lane < 16 ? wsum[lane] : 0;
+    if (lane < SCAN_THREADS / 64) wsum[lane] = s;
+  }
+  __syncthreads();
+  int run = (w > 0 ? wsum[w - 1] : 0) + x - local;
 #pragma unroll
-      for (int o = 1; o < 16; o <<= 1) {
-        const int y = __shfl_up(s, o);
-        if (lane >= o) s += y;
+  for (int k = 0; k < SCAN_DPT; ++k) {
+    const int d = SCAN_DPT * t + k;
+    if (d < ndig)
+      for (int b = 0; b < nblk; ++b) {
+        const int c = hist[d * nblk + b];
+        offs[d * nblk + b] = run;
+        run += c;
       }
-      if (lane < 16) wsum[lane] = s;
-    }
-    __syncthreads();
-    const int wprefix = w > 0 ? wsum[w - 1] : 0;
-    if (idx < total) offs[idx] = carry + wprefix + x - v;
-    carry += wsum[15];
-    __syncthreads();
   }
 }
 
@@ -146,7 +162,7 @@ hipError_t launch_sort(const int32_t* keys_in, int n, int key_bits, int32_t* key
     const int nb = key_bits - shift < bits ? key_bits - shift : bits;
     hipLaunchKernelGGL(k_sort_hist, dim3(nblk), dim3(SORT_THREADS), 0, st, kin, n, shift, nb, nblk,
                        hist);
-    hipLaunchKernelGGL(k_sort_scan, dim3(1), dim3(1024), 0, st, hist, nblk << nb, offs);
+    hipLaunchKernelGGL(k_sort_scan, dim3(1), dim3(SCAN_THREADS), 0, st, hist, nblk, 1 << nb, offs);
     hipLaunchKernelGGL(k_sort_scatter, dim3(nblk), dim3(SORT_THREADS), 0, st, kin, vin, n, shift,
                        nb, nblk, offs, kout, vout);
     *keys_out = kout;

@@ -9,6 +9,8 @@
 
 namespace asgd {
 
+constexpr int W1_UNROLL = 16;  // dA1 rows in flight per wavefront
+
 __global__ __launch_bounds__(256) void k_w1_update(float* __restrict__ W1, int F,
                                                    const int32_t* __restrict__ skeys,
                                                    const int32_t* __restrict__ svals, int n_keys,
@@ -34,19 +36,20 @@ __global__ __launch_bounds__(256) void k_w1_update(float* __restrict__ W1, int F
     }
     const int cnt = __popcll(__ballot(in));  // a segment is contiguous: lanes 0..cnt-1
     int u = 0;
-    for (; u + 4 <= cnt; u += 4) {
-      int ru[4];
-      float xu[4];
-      float2 d[4];
+    for (; u + W1_UNROLL <= cnt; u += W1_UNROLL) {
+      int ru[W1_UNROLL];
+      float xu[W1_UNROLL];
+      float2 d[W1_UNROLL];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
+      for (int k = 0; k < W1_UNROLL; ++k) {
         ru[k] = __builtin_amdgcn_readlane(row, u + k);
         xu[k] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, xv), u + k));
       }
 #pragma unroll
-      for (int k = 0; k < 4; ++k) d[k] = *reinterpret_cast<const float2*>(dA1 + (size_t)ru[k] * HID + 2 * lane);
+      for (int k = 0; k < W1_UNROLL; ++k)
+        d[k] = *reinterpret_cast<const float2*>(dA1 + (size_t)ru[k] * HID + 2 * lane);
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
+      for (int k = 0; k < W1_UNROLL; ++k) {
         acc.x = fmaf(xu[k], d[k].x, acc.x);
         acc.y = fmaf(xu[k], d[k].y, acc.y);
       }
