@@ -131,6 +131,7 @@ __device__ __forceinline__ double wave_sum_d(double v) {
 }
 
 constexpr float LOG2E = 1.4426950408889634f;
+constexpr float LN2 = 0.6931471805599453f;
 
 // e^x through the hardware base-2 exponential.
 __device__ __forceinline__ float exp_fast(float x) { return __builtin_amdgcn_exp2f(x * LOG2E); }

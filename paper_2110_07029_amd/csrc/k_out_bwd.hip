@@ -16,6 +16,8 @@
 // 256 rows with bf16 operands, H1 and H1^T are staged once per workgroup in
 // LDS (padded rows: conflict-free 8-byte fragment reads); otherwise they are
 // read from the L2-resident global copies.
+#include <math.h>
+
 #include "asgd_dev.h"
 #include "asgd_kernels.h"
 
@@ -23,8 +25,10 @@ namespace asgd {
 
 constexpr int BWD_WAVES = 8;
 constexpr int BWD_STAGE_ROWS = 256;
-constexpr int H1S_LD = HID + 8;             // row-major H1 in LDS (elements)
-constexpr int H1TS_LD = BWD_STAGE_ROWS + 8; // transposed H1 in LDS (elements)
+// LDS row strides of 66 and 130 dwords (2 mod 4, odd half): the 8-byte fragment
+// reads of 16 consecutive lanes cover all 32 banks.
+constexpr int H1S_LD = HID + 4;             // row-major H1 in LDS (elements)
+constexpr int H1TS_LD = BWD_STAGE_ROWS + 4; // transposed H1 in LDS (elements)
 
 template <bool BF16, bool STAGE>
 __global__ __launch_bounds__(64 * BWD_WAVES) void k_out_bwd(
@@ -32,7 +36,7 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void k_out_bwd(
     const typename Mma<BF16>::elem* __restrict__ H1, const typename Mma<BF16>::elem* __restrict__ H1T,
     int ld_t, int B, const float* __restrict__ lse, const float* __restrict__ rw,
     const int32_t* __restrict__ skeys, const int32_t* __restrict__ svals, int n_keys,
-    int label_base, const int32_t* __restrict__ lrow, float lr, float invB) {
+    int label_base, const int32_t* __restrict__ lrow, float lr, float invB, float log2_invB) {
   using M = Mma<BF16>;
   using E = typename M::elem;
   using Fr = typename M::frag;
@@ -51,27 +55,33 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void k_out_bwd(
     h1ts = reinterpret_cast<E*>(sp);
     sp += HID * H1TS_LD * sizeof(E);
   }
-  float* lse_s = reinterpret_cast<float*>(sp);
+  // per row: crow = log2(1/B) - lse*log2(e) (-inf for rows past B) so that
+  // dZ = 2^(z*log2(e) + bias*log2(e) + crow) = softmax/B; tw = (1/|Y_i|)/B
+  float* crow_s = reinterpret_cast<float*>(sp);
   sp += bpad * sizeof(float);
-  float* rw_s = reinterpret_cast<float*>(sp);
+  float* tw_s = reinterpret_cast<float*>(sp);
   sp += bpad * sizeof(float);
   uint32_t* mask = reinterpret_cast<uint32_t*>(sp) + wave * 32 * nrb;
 
   for (int i = tid; i < bpad; i += 64 * BWD_WAVES) {
-    lse_s[i] = i < B ? lse[i] : 0.0f;
-    rw_s[i] = i < B ? rw[i] : 0.0f;
+    crow_s[i] = i < B ? log2_invB - lse[i] * LOG2E : -INFINITY;
+    tw_s[i] = i < B ? rw[i] * invB : 0.0f;
   }
   if constexpr (STAGE) {
     for (int e = tid; e < bpad * 16; e += 64 * BWD_WAVES) {
       const int r = e >> 4, c = e & 15;
-      *reinterpret_cast<uint4*>(h1s + r * H1S_LD + c * 8) =
-          *reinterpret_cast<const uint4*>(H1 + (size_t)r * HID + c * 8);
+      *reinterpret_cast<uint2*>(h1s + r * H1S_LD + c * 8) =
+          *reinterpret_cast<const uint2*>(H1 + (size_t)r * HID + c * 8);
+      *reinterpret_cast<uint2*>(h1s + r * H1S_LD + c * 8 + 4) =
+          *reinterpret_cast<const uint2*>(H1 + (size_t)r * HID + c * 8 + 4);
     }
     const int cpr = bpad >> 3;
     for (int e = tid; e < HID * cpr; e += 64 * BWD_WAVES) {
       const int h = e / cpr, c = e - h * cpr;
-      *reinterpret_cast<uint4*>(h1ts + h * H1TS_LD + c * 8) =
-          *reinterpret_cast<const uint4*>(H1T + (size_t)h * ld_t + c * 8);
+      *reinterpret_cast<uint2*>(h1ts + h * H1TS_LD + c * 8) =
+          *reinterpret_cast<const uint2*>(H1T + (size_t)h * ld_t + c * 8);
+      *reinterpret_cast<uint2*>(h1ts + h * H1TS_LD + c * 8 + 4) =
+          *reinterpret_cast<const uint2*>(H1T + (size_t)h * ld_t + c * 8 + 4);
     }
   }
   __syncthreads();
@@ -85,31 +95,49 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void k_out_bwd(
     const int l0 = blk * 32;
     const int label = l0 + n;
     const bool lvalid = label < L;
-    // W2 rows of this block (fp32 master): hidden 32*kb + 8*q + 4*g + (0..3) per lane
-    // branch-free loads (clamped row, zeroed by a select) keep the wait counters exact
+    // W2 rows of this block (fp32 master): hidden 32*kb + 8*q + 4*g + (0..3) per lane.
+    // Loads of labels past L read the last row (valid memory) and are never stored.
     float4 wreg[4][4];
     const float* wrow = W2 + (size_t)min(label, L - 1) * HID;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float4 v = *reinterpret_cast<const float4*>(wrow + 32 * kb + 8 * q + 4 * g);
-        wreg[kb][q] = make_float4(lvalid ? v.x : 0.f, lvalid ? v.y : 0.f, lvalid ? v.z : 0.f,
-                                  lvalid ? v.w : 0.f);
+      for (int q = 0; q < 4; ++q)
+        wreg[kb][q] = *reinterpret_cast<const float4*>(wrow + 32 * kb + 8 * q + 4 * g);
+    const float bias = b2[min(label, L - 1)];
+    const float bb = lvalid ? bias * LOG2E : -INFINITY;
+    // operand fragments of W2 (K = hidden), converted once per block
+    Fr wf[4][NCH];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        if constexpr (BF16) {
+          const float4 lo4 = wreg[kb][2 * c], hi4 = wreg[kb][2 * c + 1];
+          Fr f;
+          f[0] = (bf16)lo4.x; f[1] = (bf16)lo4.y; f[2] = (bf16)lo4.z; f[3] = (bf16)lo4.w;
+          f[4] = (bf16)hi4.x; f[5] = (bf16)hi4.y; f[6] = (bf16)hi4.z; f[7] = (bf16)hi4.w;
+          wf[kb][c] = f;
+        } else {
+          const float4 v = wreg[kb][c >> 2];
+          const float vs[4] = {v.x, v.y, v.z, v.w};
+          wf[kb][c] = vs[c & 3];
+        }
       }
-    const float bv = b2[min(label, L - 1)];
-    const float bias = lvalid ? bv : 0.0f;
 
     // true (row, label) pairs of these 32 labels -> bit mask [label][row block]
-    for (int k = lane; k < 32 * nrb; k += 64) mask[k] = 0u;
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     const int lo = lower_bound_dev(skeys, n_keys, F + l0);
     const int hi = lower_bound_dev(skeys, n_keys, F + min(l0 + 32, L));
-    for (int q = lo + lane; q < hi; q += 64) {
-      const int row = lrow[svals[q] - label_base];
-      atomicOr(&mask[(skeys[q] - F - l0) * nrb + (row >> 5)], 1u << (row & 31));
+    const bool has_targets = hi > lo;
+    if (has_targets) {
+      for (int k = lane; k < 32 * nrb; k += 64) mask[k] = 0u;
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      for (int q = lo + lane; q < hi; q += 64) {
+        const int row = lrow[svals[q] - label_base];
+        atomicOr(&mask[(skeys[q] - F - l0) * nrb + (row >> 5)], 1u << (row & 31));
+      }
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     }
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
 
     f32x16 accw[4];
 #pragma unroll
@@ -126,34 +154,32 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void k_out_bwd(
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-          Fr wb;
-          if constexpr (BF16) {
-            const float4 lo4 = wreg[kb][2 * c], hi4 = wreg[kb][2 * c + 1];
-            wb[0] = (bf16)lo4.x; wb[1] = (bf16)lo4.y; wb[2] = (bf16)lo4.z; wb[3] = (bf16)lo4.w;
-            wb[4] = (bf16)hi4.x; wb[5] = (bf16)hi4.y; wb[6] = (bf16)hi4.z; wb[7] = (bf16)hi4.w;
-          } else {
-            const float4 v = wreg[kb][c >> 2];
-            const float vs[4] = {v.x, v.y, v.z, v.w};
-            wb = vs[c & 3];
-          }
-          z = M::mma(frag_row<BF16>(hrow + 32 * kb, c, g), wb, z);
-        }
-      const uint32_t mw = mask[n * nrb + rb];
+        for (int c = 0; c < NCH; ++c) z = M::mma(frag_row<BF16>(hrow + 32 * kb, c, g), wf[kb][c], z);
+      // rows 8*q + 4*g + (0..3) of this block: one float4 of row constants each
+      float cr[16];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 c4 = *reinterpret_cast<const float4*>(crow_s + rb * 32 + 8 * q + 4 * g);
+        cr[4 * q + 0] = c4.x; cr[4 * q + 1] = c4.y; cr[4 * q + 2] = c4.z; cr[4 * q + 3] = c4.w;
+      }
       float dz[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int rl = 8 * (r >> 2) + 4 * g + (r & 3);
-        const int row = rb * 32 + rl;
-        float d = 0.0f;
-        if (row < B && lvalid) {
-          const float pr = exp_fast(z[r] + bias - lse_s[row]);
-          const float t = ((mw >> rl) & 1u) ? rw_s[row] : 0.0f;
-          d = (pr - t) * invB;
-        }
-        dz[r] = d;
-        db2p += d;
+        dz[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, bb) + cr[r]);
       }
+      if (has_targets) {
+        const uint32_t mw = mask[n * nrb + rb];
+        if (__any(mw != 0u)) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int rl = 8 * (r >> 2) + 4 * g + (r & 3);
+            if ((mw >> rl) & 1u) dz[r] -= tw_s[rb * 32 + rl];
+          }
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) db2p += dz[r];
+      // dW2^T += H1^T dZ : A = H1^T rows (M = hidden, K = rows), B = dZ from the accumulators.
       Fr df[NCH];
 #pragma unroll
       for (int c = 0; c < NCH; ++c) df[c] = frag_acc<BF16>(dz, c);
@@ -191,6 +217,7 @@ static hipError_t launch_bwd(int grid, size_t shm, hipStream_t st, float* W2, fl
                              const float* rw, const int32_t* skeys, const int32_t* svals, int n_keys,
                              int label_base, const int32_t* lrow, float lr, float invB) {
   using E = typename Mma<BF16>::elem;
+  const float log2_invB = (float)log2((double)invB);
   static bool attr_done = false;
   if (!attr_done) {
     hipError_t e = hipFuncSetAttribute((const void*)k_out_bwd<BF16, STAGE>,
@@ -200,7 +227,7 @@ static hipError_t launch_bwd(int grid, size_t shm, hipStream_t st, float* W2, fl
   }
   hipLaunchKernelGGL((k_out_bwd<BF16, STAGE>), dim3(grid), dim3(64 * BWD_WAVES), shm, st, W2, b2, L,
                      F, (const E*)H1, (const E*)H1T, ld_t, B, lse, rw, skeys, svals, n_keys,
-                     label_base, lrow, lr, invB);
+                     label_base, lrow, lr, invB, log2_invB);
   return hipGetLastError();
 }
 

@@ -27,7 +27,9 @@ struct FwdShape {
   static constexpr int NB = 1;                // 32-row blocks per wave
   static constexpr int WAVES = 8;             // wavefronts per workgroup (2 per SIMD)
   static constexpr int RB = WAVES * 32 * NB;  // rows per workgroup
-  static constexpr int WR = BF16 ? 136 : 132; // leading dim of the row-major tile (elements)
+  // leading dims chosen so a row step is 2 (mod 4) dwords with an odd half: the
+  // 8-byte fragment reads of 16 consecutive lanes then cover all 32 banks
+  static constexpr int WR = 132;              // leading dim of the row-major tile (elements)
   static constexpr int WT = 36;               // leading dim of the transposed tile (elements)
 };
 
@@ -96,7 +98,7 @@ __device__ __forceinline__ void tile_store(const TileRegs& r, int L, int tile,
       }
     }
   }
-  if (threadIdx.x < OUT_TILE) bt[threadIdx.x] = tile * OUT_TILE + (int)threadIdx.x < L ? r.bias : 0.0f;
+  if (threadIdx.x < OUT_TILE) bt[threadIdx.x] = tile * OUT_TILE + (int)threadIdx.x < L ? r.bias : -INFINITY;
 }
 
 // ---------------------------------------------------------------------------
@@ -116,7 +118,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
   constexpr int NCH = 32 / M::KC;
   __shared__ __attribute__((aligned(16))) E wr[2][OUT_TILE * WR];
   __shared__ __attribute__((aligned(16))) E wt[2][HID * WT];
-  __shared__ float bt[2][OUT_TILE];
+  __shared__ __attribute__((aligned(16))) float bt[2][OUT_TILE];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, g = lane >> 5, n = lane & 31;
   const int split = blockIdx.x;
@@ -167,15 +169,25 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
   tile_load(W2, b2, L, min(t_begin + 1, t_end - 1), tr1);
   __syncthreads();
 
+  // Online softmax in base 2 with lazy rescaling: p = 2^(z log2e - m2) where m2
+  // is a per-row reference that is raised only when a tile's maximum exceeds it
+  // by more than LAZY (so p <= 2^LAZY); the final normalisation uses the same
+  // reference, so the result is exact up to rounding.
+  constexpr float LAZY = 8.0f;
   auto compute = [&](int t, int buf) {
     const E* wrb = wr[buf];
     const E* wtb = wt[buf];
-    // Z^T tile: A = W2 rows (M = labels, K = hidden), B = H1^T.
+    // Z^T tile: A = W2 rows (M = labels, K = hidden), B = H1^T; the accumulator
+    // starts at the labels' biases (-inf for labels past L).
+    const float4* bq = reinterpret_cast<const float4*>(bt[buf]);
     f32x16 z[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) z[nb][r] = 0.0f;
+      for (int q = 0; q < 4; ++q) {
+        const float4 b = bq[2 * q + g];
+        z[nb][4 * q + 0] = b.x; z[nb][4 * q + 1] = b.y; z[nb][4 * q + 2] = b.z; z[nb][4 * q + 3] = b.w;
+      }
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -184,36 +196,32 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) z[nb] = M::mma(a, hf[nb][kb][c], z[nb]);
       }
-    // bias, label mask, online softmax; probabilities become the K operand of O^T.
     Fr pf[NB][NCH];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      float zz[16];
-      float tmax = -INFINITY;
+      float tmax = z[nb][0];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int ll = 8 * (r >> 2) + 4 * g + (r & 3);
-        zz[r] = (t * OUT_TILE + ll < L) ? z[nb][r] + bt[buf][ll] : -INFINITY;
-        tmax = fmaxf(tmax, zz[r]);
-      }
+      for (int r = 1; r < 16; ++r) tmax = fmaxf(tmax, z[nb][r]);
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-      const float mnew = fmaxf(m_run[nb], tmax);
-      const float scale = exp_fast(m_run[nb] - mnew);
-      float p[16];
-      float ps = 0.0f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        p[r] = exp_fast(zz[r] - mnew);
-        ps += p[r];
-      }
-      s_run[nb] = s_run[nb] * scale + ps;
-      if (__any(mnew > m_run[nb])) {
+      const float m2c = tmax * LOG2E;
+      if (__any(m2c > m_run[nb] + LAZY)) {
+        const float m2n = m2c > m_run[nb] + LAZY ? m2c : m_run[nb];
+        const float scale = __builtin_amdgcn_exp2f(m_run[nb] - m2n);
+        s_run[nb] *= scale;
 #pragma unroll
         for (int hb = 0; hb < 4; ++hb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) acc_o[nb][hb][r] *= scale;
+        m_run[nb] = m2n;
       }
-      m_run[nb] = mnew;
+      float p[16];
+      float ps = 0.0f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        p[r] = __builtin_amdgcn_exp2f(fmaf(z[nb][r], LOG2E, -m_run[nb]));
+        ps += p[r];
+      }
+      s_run[nb] += ps;
 #pragma unroll
       for (int c = 0; c < NCH; ++c) pf[nb][c] = frag_acc<BF16>(p, c);
     }
@@ -251,7 +259,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
       const float stot = s_run[nb] + __shfl_xor(s_run[nb], 32);
       if (row < B) {
         if (g == 0) {
-          m_part[(size_t)split * ld_part + row] = m_run[nb];
+          m_part[(size_t)split * ld_part + row] = m_run[nb] * LN2;
           s_part[(size_t)split * ld_part + row] = stot;
         }
         float* o = o_part + ((size_t)split * ld_part + row) * HID;
