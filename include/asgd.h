@@ -200,6 +200,84 @@ asgd_status asgd_scale_batches(int32_t n, const int32_t* u, int32_t* b, float* l
                                int32_t b_max, double beta);
 
 /* ------------------------------------------------------------------------ */
+/* Elastic rounds: n replicas on their own HIP streams of one device          */
+/* ------------------------------------------------------------------------ */
+
+/* Adaptive SGD's mega-batch loop (Sec. 3.1-3.3) with replicas standing in for
+ * GPUs.  One round: batches of consecutive dataset rows are dispatched one at
+ * a time to whichever replica is free (dynamic scheduling, Sec. 3.1) until a
+ * fixed sample budget (the mega-batch) is spent; a batch never wraps past the
+ * dataset end (it is cut there and the cursor restarts at row 0) and the last
+ * batch is cut to the remaining budget.  Then Alg. 2 weights the replicas,
+ * the merge of Alg. 2 updates the global model (with momentum) and is
+ * broadcast to every replica, and Alg. 1 rescales each replica's batch size
+ * and learning rate from its update count. */
+typedef struct asgd_elastic asgd_elastic; /* opaque */
+
+enum {
+  ASGD_CLOCK_TIMED = 0,  /* a replica is free when its last step's HIP event completed */
+  ASGD_CLOCK_VIRTUAL = 1 /* deterministic: replica i's clock advances by
+                            slow[i] * (c0 + c1 * rows + c2 * nnz) per step; the
+                            replica with the smallest clock (lowest index on
+                            ties) takes the next batch */
+};
+
+typedef struct asgd_elastic_config {
+  int32_t n_replicas;      /* 1..16 */
+  int32_t b_min, b_max;    /* batch-size bounds of Alg. 1; every replica starts at b_max */
+  double beta;             /* Alg. 1 scaling parameter */
+  float lr;                /* learning rate at b_max (linear scaling below) */
+  float gamma;             /* momentum of the merge (Alg. 2) */
+  int32_t weight_mode;     /* ASGD_WEIGHTS_ALG2 or ASGD_WEIGHTS_SAMPLES */
+  int32_t perturb;         /* 1: Alg. 2 perturbation with the L2-per-parameter gate */
+  double pert_thr, delta;  /* perturbation threshold and factor */
+  int64_t megabatch;       /* samples per round */
+  int32_t clock;           /* ASGD_CLOCK_TIMED or ASGD_CLOCK_VIRTUAL */
+  double c0, c1, c2;       /* virtual clock cost model */
+  double slow[16];         /* virtual clock per-replica multipliers (0 -> 1) */
+} asgd_elastic_config;
+
+/* Per-round record (host memory, filled by asgd_elastic_round). */
+typedef struct asgd_elastic_log {
+  int32_t n_dispatch;      /* batches dispatched this round */
+  int32_t max_dispatch;    /* capacity of the arrays below (set by the caller) */
+  int32_t* replica;        /* [max_dispatch] replica of each batch, in dispatch order */
+  int32_t* row0;           /* [max_dispatch] first dataset row */
+  int32_t* row1;           /* [max_dispatch] one past the last row */
+  int32_t u[16];           /* updates per replica this round */
+  int64_t samples[16];     /* samples per replica this round */
+  int32_t b_used[16];      /* batch sizes used this round */
+  float lr_used[16];       /* learning rates used this round */
+  float alpha[16];         /* merge weights */
+  double l2_per_param[16]; /* replica L2 norm per parameter (perturb only) */
+  int32_t b_next[16];      /* batch sizes after Alg. 1 */
+  float lr_next[16];       /* learning rates after Alg. 1 */
+  int32_t cursor;          /* dataset row the next round starts at */
+} asgd_elastic_log;
+
+/* Create n replicas and a global / previous-global model pair, all from the
+ * same seed (identical initial models), sized by `model_cfg` (whose
+ * max_batch must be >= b_max).  replica_streams: n HIP streams (the
+ * replicas' work queues); global_stream: the merge's stream. */
+asgd_status asgd_elastic_create(asgd_elastic** out, const asgd_elastic_config* cfg,
+                                const asgd_config* model_cfg, uint64_t seed,
+                                void* const* replica_streams, void* global_stream);
+asgd_status asgd_elastic_free(asgd_elastic* e);
+
+/* One round over the device-resident dataset (x_all, y_all: all rows, the
+ * batches are zero-copy row slices; x_indptr_host / y_indptr_host: host
+ * copies of the indptr arrays, used for batch nnz counts).  Fills *log (if
+ * non-NULL).  Returns after the merge has been enqueued; the replicas'
+ * streams wait for it. */
+asgd_status asgd_elastic_round(asgd_elastic* e, const asgd_csr* x_all, const asgd_csr* y_all,
+                               const int32_t* x_indptr_host, const int32_t* y_indptr_host,
+                               asgd_elastic_log* log);
+
+/* Borrow the global model (owned by e) or replica i. */
+asgd_status asgd_elastic_model(asgd_elastic* e, int32_t which /* -1 global, else replica */,
+                               asgd_model** out);
+
+/* ------------------------------------------------------------------------ */
 /* Inspection of intermediates (parity tests)                                */
 /* ------------------------------------------------------------------------ */
 

@@ -29,8 +29,10 @@ EXPORTS = (
     "asgd_train_step", "asgd_model_last_loss", "asgd_predict_topk", "asgd_merge",
     "asgd_model_l2_per_param", "asgd_merge_weights", "asgd_scale_batches",
     "asgd_debug_forward", "asgd_debug_touched_rows", "asgd_model_set_timing",
-    "asgd_model_get_timing", "asgd_last_error",
+    "asgd_model_get_timing", "asgd_elastic_create", "asgd_elastic_free", "asgd_elastic_round",
+    "asgd_elastic_model", "asgd_last_error",
 )
+ASGD_CLOCK_TIMED, ASGD_CLOCK_VIRTUAL = 0, 1
 
 # Kernel groups of asgd_model_get_timing.
 KERNELS = ("gather", "sort", "out_fwd", "out_combine", "hidden", "out_bwd", "w1_update", "merge")
@@ -51,6 +53,21 @@ class asgd_config(ctypes.Structure):
 class asgd_csr(ctypes.Structure):
     _fields_ = [("n_rows", c_int32), ("n_cols", c_int32), ("nnz", c_int32),
                 ("indptr", c_void_p), ("indices", c_void_p), ("values", c_void_p)]
+
+
+class asgd_elastic_config(ctypes.Structure):
+    _fields_ = [("n_replicas", c_int32), ("b_min", c_int32), ("b_max", c_int32), ("beta", c_double),
+                ("lr", c_float), ("gamma", c_float), ("weight_mode", c_int32), ("perturb", c_int32),
+                ("pert_thr", c_double), ("delta", c_double), ("megabatch", c_int64), ("clock", c_int32),
+                ("c0", c_double), ("c1", c_double), ("c2", c_double), ("slow", c_double * 16)]
+
+
+class asgd_elastic_log(ctypes.Structure):
+    _fields_ = [("n_dispatch", c_int32), ("max_dispatch", c_int32), ("replica", POINTER(c_int32)),
+                ("row0", POINTER(c_int32)), ("row1", POINTER(c_int32)), ("u", c_int32 * 16),
+                ("samples", c_int64 * 16), ("b_used", c_int32 * 16), ("lr_used", c_float * 16),
+                ("alpha", c_float * 16), ("l2_per_param", c_double * 16), ("b_next", c_int32 * 16),
+                ("lr_next", c_float * 16), ("cursor", c_int32)]
 
 
 _lib = None
@@ -79,6 +96,12 @@ def _declare(lib):
         "asgd_debug_touched_rows": (c_int32, [P, POINTER(asgd_csr), P, POINTER(c_int32)]),
         "asgd_model_set_timing": (c_int32, [P, c_int32]),
         "asgd_model_get_timing": (c_int32, [P, c_int32, POINTER(c_double), POINTER(c_int64)]),
+        "asgd_elastic_create": (c_int32, [POINTER(c_void_p), POINTER(asgd_elastic_config),
+                                          POINTER(asgd_config), c_uint64, POINTER(c_void_p), P]),
+        "asgd_elastic_free": (c_int32, [P]),
+        "asgd_elastic_round": (c_int32, [P, POINTER(asgd_csr), POINTER(asgd_csr), P, P,
+                                         POINTER(asgd_elastic_log)]),
+        "asgd_elastic_model": (c_int32, [P, c_int32, POINTER(c_void_p)]),
         "asgd_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -255,3 +278,48 @@ def asgd_model_get_timing(m: int, kernel: int):
     t, n = c_double(), c_int64()
     _check(load().asgd_model_get_timing(m, kernel, byref(t), byref(n)), "asgd_model_get_timing")
     return t.value, n.value
+
+
+def asgd_elastic_create(cfg: asgd_elastic_config, model_cfg: asgd_config, seed: int, replica_streams,
+                        global_stream) -> int:
+    n = len(replica_streams)
+    arr = (c_void_p * n)(*[_stream(s) for s in replica_streams])
+    h = c_void_p()
+    _check(load().asgd_elastic_create(byref(h), byref(cfg), byref(model_cfg), c_uint64(seed), arr,
+                                      _stream(global_stream)), "asgd_elastic_create")
+    return h.value
+
+
+def asgd_elastic_free(e: int):
+    _check(load().asgd_elastic_free(e), "asgd_elastic_free")
+
+
+def asgd_elastic_round(e: int, x_all: asgd_csr, y_all: asgd_csr, x_indptr_host: np.ndarray,
+                       y_indptr_host: np.ndarray, max_dispatch: int = 4096) -> dict:
+    """One round; returns the round record as a dict of numpy arrays / lists."""
+    xi = np.ascontiguousarray(x_indptr_host, np.int32)
+    yi = np.ascontiguousarray(y_indptr_host, np.int32)
+    rep = np.zeros(max_dispatch, np.int32)
+    r0 = np.zeros(max_dispatch, np.int32)
+    r1 = np.zeros(max_dispatch, np.int32)
+    log = asgd_elastic_log()
+    log.max_dispatch = max_dispatch
+    log.replica = rep.ctypes.data_as(POINTER(c_int32))
+    log.row0 = r0.ctypes.data_as(POINTER(c_int32))
+    log.row1 = r1.ctypes.data_as(POINTER(c_int32))
+    _check(load().asgd_elastic_round(e, byref(x_all), byref(y_all), xi.ctypes.data, yi.ctypes.data,
+                                     byref(log)), "asgd_elastic_round")
+    nd = log.n_dispatch
+    if nd > max_dispatch:
+        raise AsgdError(ASGD_ERANGE, "asgd_elastic_round", "dispatch log capacity exceeded")
+    return dict(schedule=[(int(rep[i]), int(r0[i]), int(r1[i])) for i in range(nd)],
+                u=list(log.u), samples=list(log.samples), b_used=list(log.b_used),
+                lr_used=list(log.lr_used), alpha=np.array(log.alpha[:], np.float32),
+                l2_per_param=list(log.l2_per_param), b_next=list(log.b_next),
+                lr_next=list(log.lr_next), cursor=log.cursor)
+
+
+def asgd_elastic_model(e: int, which: int) -> int:
+    h = c_void_p()
+    _check(load().asgd_elastic_model(e, which, byref(h)), "asgd_elastic_model")
+    return h.value
