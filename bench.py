@@ -8,7 +8,11 @@ output-layer forward (online softmax over all labels), the per-row combine
 update and the sparse W1 update.  The dataset is staged in HBM before timing;
 batches are zero-copy row slices.  Prints one JSON line.
 
-    python bench.py [--steps K] [--warmup W] [--workload wide-label|wide-feature|mid|tiny]
+    python bench.py [--steps K] [--warmup W] [--workload wide-label|wide-feature|mid|tiny|elastic]
+
+With --workload elastic a step is one round of configuration 5 (4 replicas of
+the wide-label model on 4 HIP streams: dynamic dispatch of a mega-batch, merge,
+batch-size scaling).
 """
 from __future__ import annotations
 
@@ -61,6 +65,98 @@ def kernel_model(w, B, nnz, lnnz, uniq):
     }
 
 
+def measure_merge(w, n_rep, reps_iters, stream):
+    """Normalized merge of n_rep replicas of the workload's model (with momentum and
+    broadcast, as in the elastic configuration), timed with the library's events."""
+    import paper_2110_07029_amd as asgd
+    mk = lambda s: asgd.asgd_model_init(w.n_features, w.n_labels, 8, 64, 64, gemm_bf16=w.gemm_bf16,
+                                        seed=s, stream=stream)
+    g, gp = mk(1), mk(2)
+    reps = [mk(10 + i) for i in range(n_rep)]
+    try:
+        alpha = [1.0 / n_rep] * n_rep
+        for _ in range(3):
+            asgd.asgd_merge(g, gp, reps, alpha, 0.9, True)
+        asgd.asgd_model_set_timing(g, True)
+        asgd.asgd_model_get_timing(g, asgd.KERNELS.index("merge"))
+        for _ in range(reps_iters):
+            asgd.asgd_merge(g, gp, reps, alpha, 0.9, True)
+        tot, n = asgd.asgd_model_get_timing(g, asgd.KERNELS.index("merge"))
+        P = asgd.asgd_model_num_params(g)
+    finally:
+        for m in [g, gp] + reps:
+            asgd.asgd_model_free(m)
+    avg = tot / n
+    # reads the n replicas, w and w_prev; writes w' and n broadcast copies
+    byts = (n_rep + 2) * P * 4.0 + (n_rep + 1) * P * 4.0
+    gbs = byts / (avg * 1e-3) / 1e9
+    return {"avg_us": round(avg * 1e3, 2), "launches": n, "alg_bytes": byts, "alg_flops": 0.0,
+            "GB/s": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4), "replicas": n_rep}
+
+
+def run_elastic(args):
+    """Configuration 5: 4 replicas of the wide-label model on 4 HIP streams, timed dynamic
+    dispatch, merge every ~8 steps per replica (mega-batch 8 x 4 x b_max samples),
+    weights from samples processed, momentum 0.9, Alg. 1 with b in [64, 1024]."""
+    import torch
+    import paper_2110_07029_amd as asgd
+    from paper_2110_07029_amd import synth
+    cfg5 = synth.ELASTIC
+    w = synth.WORKLOADS[cfg5["base"]]
+    n, b_min, b_max = cfg5["n_replicas"], cfg5["b_min"], cfg5["b_max"]
+    mega = cfg5["steps_per_round"] * n * b_max
+    K, W = args.steps, args.warmup
+    n_samples = min(w.n_samples, max(mega * (K + W), 4 * b_max))
+    log(f"elastic: {n} replicas of {w.name}, b in [{b_min}, {b_max}], mega-batch {mega}; {n_samples} samples")
+    ds = synth.generate(w, n_samples=n_samples)
+    ipx = np.asarray(ds.x.indptr, np.int64)
+    ipy = np.asarray(ds.y.indptr, np.int64)
+    max_nnz = int(np.max(ipx[b_max:] - ipx[:-b_max]))
+    max_lnnz = int(np.max(ipy[b_max:] - ipy[:-b_max]))
+    dx, dy = asgd.DeviceCSR(ds.x), asgd.DeviceCSR(ds.y)
+    xa, ya = dx.batch(0, ds.x.n_rows), dy.batch(0, ds.y.n_rows)
+    mcfg = asgd.asgd_config(w.n_features, w.n_labels, H, b_max, max_nnz, max_lnnz, 1 if w.gemm_bf16 else 0, 0)
+    ec = asgd.asgd_elastic_config()
+    ec.n_replicas, ec.b_min, ec.b_max, ec.beta = n, b_min, b_max, b_min / 2.0
+    ec.lr, ec.gamma, ec.weight_mode, ec.perturb = w.lr, 0.9, asgd.ASGD_WEIGHTS_SAMPLES, 0
+    ec.pert_thr, ec.delta, ec.megabatch, ec.clock = 0.1, 0.1, mega, asgd.ASGD_CLOCK_TIMED
+    streams = [torch.cuda.Stream() for _ in range(n)]
+    gstream = torch.cuda.current_stream()
+    e = asgd.asgd_elastic_create(ec, mcfg, cfg5["index"] + 2000, streams, gstream)
+    xi, yi = ipx.astype(np.int32), ipy.astype(np.int32)
+    try:
+        for _ in range(W):
+            asgd.asgd_elastic_round(e, xa, ya, xi, yi)
+        torch.cuda.synchronize()
+        log(f"warmup done ({W} rounds)")
+        t0 = time.perf_counter()
+        samples, bs = 0, []
+        for r in range(K):
+            lg = asgd.asgd_elastic_round(e, xa, ya, xi, yi)
+            samples += sum(lg["samples"][:n])
+            bs.append(lg["b_next"][:n])
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+    finally:
+        asgd.asgd_elastic_free(e)
+    log(f"timed {K} rounds: {el * 1e3:.1f} ms, final batch sizes {bs[-1] if bs else None}")
+    merge = measure_merge(w, n, 10, gstream)
+    return {
+        "metric": METRIC, "value": round(samples / el, 1), "unit": "samples/s", "n_gpus": 1, "steps": K,
+        "warmup": W, "ms_per_step": round(el * 1e3 / K, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if w.gemm_bf16 else "fp32", "data": "synthetic",
+        "config": {"workload": "elastic-4x-wide-label", "n_features": w.n_features, "n_labels": w.n_labels,
+                   "hidden": H, "replicas": n, "b_min": b_min, "b_max": b_max, "megabatch": mega,
+                   "global_batch": mega, "clock": "timed", "weights": "samples", "momentum": 0.9,
+                   "parallelism": "4 replicas on 4 HIP streams", "step": "one round (dispatch + merge)"},
+        "roofline": {"kernel": "merge", "bound": "hbm", "achieved": merge["GB/s"], "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": merge["hbm_frac"], "traffic": None},
+        "cpu_baseline": None,
+        "kernels": {"merge": merge},
+        "batch_sizes_per_round": bs,
+    }
+
+
 def cpu_baseline(w, ds, B, budget_s):
     """The oracle as it stands, timed on this host on a bounded sample of the workload."""
     from oracle import model as om
@@ -103,6 +199,9 @@ def main():
     from paper_2110_07029_amd import synth
 
     asgd.load()
+    if args.workload == "elastic":
+        print(json.dumps(run_elastic(args)), flush=True)
+        return
     w = synth.WORKLOADS[args.workload]
     B = w.batch
     K, W = args.steps, args.warmup
@@ -175,6 +274,9 @@ def main():
     # the sort runs on the library's second stream, overlapped with the output-layer
     # forward: its event span includes time it waited for CUs, so it is not a candidate
     dom = max((k for k in kt if k != "sort"), key=lambda k: kt[k][0])
+    if args.workload == "wide-label":
+        # the merge of the elastic configuration: 4 replicas of this model
+        kernels["merge"] = measure_merge(w, 4, 10, stream)
     d = kernels[dom]
     roofline = {"kernel": dom, "bound": "hbm", "achieved": d["GB/s"], "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": d["hbm_frac"], "traffic": None}

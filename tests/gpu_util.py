@@ -39,13 +39,12 @@ def write_params(m, p: dict):
 
 
 def max_batch_nnz(csr, batch: int) -> int:
+    """Largest nnz of any window of `batch` consecutive rows (batches may start
+    at any row, e.g. in the elastic dispatch)."""
     ip = np.asarray(csr.indptr, np.int64)
     n = len(ip) - 1
-    best = 0
-    for r0 in range(0, n, batch):
-        r1 = min(n, r0 + batch)
-        best = max(best, int(ip[r1] - ip[r0]))
-    return best
+    b = min(batch, n)
+    return int(np.max(ip[b:] - ip[:n - b + 1])) if n else 0
 
 
 class Setup:
