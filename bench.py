@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="wide-label")
+    ap.add_argument("--batch", type=int, default=0,
+                    help="override the workload's batch size (e.g. 1024, the elastic b_max)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="budget of the oracle CPU baseline (0 disables it)")
     return ap.parse_args()
@@ -203,7 +205,7 @@ def main():
         print(json.dumps(run_elastic(args)), flush=True)
         return
     w = synth.WORKLOADS[args.workload]
-    B = w.batch
+    B = args.batch or w.batch
     K, W = args.steps, args.warmup
     n_samples = min(w.n_samples, (K + W) * B)
     log(f"workload {w.name}: F={w.n_features} L={w.n_labels} B={B}; generating {n_samples} samples")
