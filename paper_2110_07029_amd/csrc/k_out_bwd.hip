@@ -10,12 +10,16 @@
 // lane itself loaded (the accumulator-compatible K order makes the lane that
 // loads a weight the lane that owns its gradient).
 //
-// Workgroups are persistent: 8 wavefronts (2 per SIMD) each walk their own
-// sequence of label blocks, so loads of one wave overlap the matrix work of
-// the other with no workgroup barrier inside the loop.  For batches of up to
-// 256 rows with bf16 operands, H1 and H1^T are staged once per workgroup in
-// LDS (padded rows: conflict-free 8-byte fragment reads); otherwise they are
-// read from the L2-resident global copies.
+// Workgroups are persistent, 8 wavefronts (2 per SIMD).  H1 is read by every
+// label block, so with bf16 operands it is staged in LDS in both layouts
+// (padded rows: conflict-free 8-byte fragment reads):
+//   staged  (B <= 256): the whole batch once per workgroup; each wave then
+//           walks its own sequence of label blocks with no barrier inside
+//           the loop, so loads of one wave overlap the matrix work of another;
+//   chunked (B > 256):  the workgroup takes 8 label blocks at a time and
+//           streams the batch through LDS in 256-row chunks, the dW2
+//           accumulators staying in registers across chunks.
+// fp32 operands read H1 from its L2-resident global copies.
 #include <math.h>
 
 #include "asgd_dev.h"
@@ -24,14 +28,37 @@
 namespace asgd {
 
 constexpr int BWD_WAVES = 8;
-constexpr int BWD_STAGE_ROWS = 256;
+constexpr int BWD_THREADS = 64 * BWD_WAVES;
+constexpr int BWD_CHUNK = 256;  // rows staged in LDS at a time
 // LDS row strides of 66 and 130 dwords (2 mod 4, odd half): the 8-byte fragment
 // reads of 16 consecutive lanes cover all 32 banks.
-constexpr int H1S_LD = HID + 4;             // row-major H1 in LDS (elements)
-constexpr int H1TS_LD = BWD_STAGE_ROWS + 4; // transposed H1 in LDS (elements)
+constexpr int H1S_LD = HID + 4;        // row-major H1 in LDS (elements)
+constexpr int H1TS_LD = BWD_CHUNK + 4; // transposed H1 in LDS (elements)
 
-template <bool BF16, bool STAGE>
-__global__ __launch_bounds__(64 * BWD_WAVES) void k_out_bwd(
+enum BwdMode { BWD_GLOBAL = 0, BWD_STAGED = 1, BWD_CHUNKED = 2 };
+
+// Copy rows [r0, r0 + nrows) of H1 (row-major, ld HID) and the same columns of
+// H1^T (ld ld_t) into LDS; nrows is a multiple of 32 and inside the padded
+// batch (rows past B are zero in both copies).
+__device__ __forceinline__ void stage_h1(bf16* h1s, bf16* h1ts, const bf16* __restrict__ H1,
+                                         const bf16* __restrict__ H1T, int ld_t, int r0, int nrows) {
+  for (int e = threadIdx.x; e < nrows * 16; e += BWD_THREADS) {
+    const int r = e >> 4, c = e & 15;
+    const uint4 v = *reinterpret_cast<const uint4*>(H1 + (size_t)(r0 + r) * HID + c * 8);
+    *reinterpret_cast<uint2*>(h1s + r * H1S_LD + c * 8) = make_uint2(v.x, v.y);
+    *reinterpret_cast<uint2*>(h1s + r * H1S_LD + c * 8 + 4) = make_uint2(v.z, v.w);
+  }
+  const int cpr = nrows >> 3;
+  for (int e = threadIdx.x; e < HID * cpr; e += BWD_THREADS) {
+    const int h = e / cpr, c = e - h * cpr;
+    const uint4 v = *reinterpret_cast<const uint4*>(H1T + (size_t)h * ld_t + r0 + c * 8);
+    *reinterpret_cast<uint2*>(h1ts + h * H1TS_LD + c * 8) = make_uint2(v.x, v.y);
+    *reinterpret_cast<uint2*>(h1ts + h * H1TS_LD + c * 8 + 4) = make_uint2(v.z, v.w);
+  }
+}
+
+template <bool BF16, int MODE>
+__global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
     float* __restrict__ W2, float* __restrict__ b2, int L, int F,
     const typename Mma<BF16>::elem* __restrict__ H1, const typename Mma<BF16>::elem* __restrict__ H1T,
     int ld_t, int B, const float* __restrict__ lse, const float* __restrict__ rw,
@@ -41,57 +68,75 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void k_out_bwd(
   using E = typename M::elem;
   using Fr = typename M::frag;
   constexpr int NCH = 32 / M::KC;
+  constexpr bool LDS_H1 = MODE != BWD_GLOBAL;
+  static_assert(!LDS_H1 || BF16, "LDS staging is for bf16 operands");
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   const int nrb = (B + 31) >> 5;
   const int bpad = nrb * 32;
+  // rows whose constants and target bits are held at once
+  const int span = MODE == BWD_CHUNKED ? BWD_CHUNK : bpad;
+  const int mstride = span >> 5;  // mask words per label
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, n = lane & 31;
 
   char* sp = smem_raw;
   E* h1s = nullptr;
   E* h1ts = nullptr;
-  if constexpr (STAGE) {
+  if constexpr (LDS_H1) {
     h1s = reinterpret_cast<E*>(sp);
-    sp += BWD_STAGE_ROWS * H1S_LD * sizeof(E);
+    sp += BWD_CHUNK * H1S_LD * sizeof(E);
     h1ts = reinterpret_cast<E*>(sp);
     sp += HID * H1TS_LD * sizeof(E);
   }
   // per row: crow = log2(1/B) - lse*log2(e) (-inf for rows past B) so that
   // dZ = 2^(z*log2(e) + bias*log2(e) + crow) = softmax/B; tw = (1/|Y_i|)/B
   float* crow_s = reinterpret_cast<float*>(sp);
-  sp += bpad * sizeof(float);
+  sp += span * sizeof(float);
   float* tw_s = reinterpret_cast<float*>(sp);
-  sp += bpad * sizeof(float);
-  uint32_t* mask = reinterpret_cast<uint32_t*>(sp) + wave * 32 * nrb;
+  sp += span * sizeof(float);
+  uint32_t* mask = reinterpret_cast<uint32_t*>(sp) + wave * 32 * mstride;
 
-  for (int i = tid; i < bpad; i += 64 * BWD_WAVES) {
-    crow_s[i] = i < B ? log2_invB - lse[i] * LOG2E : -INFINITY;
-    tw_s[i] = i < B ? rw[i] * invB : 0.0f;
-  }
-  if constexpr (STAGE) {
-    for (int e = tid; e < bpad * 16; e += 64 * BWD_WAVES) {
-      const int r = e >> 4, c = e & 15;
-      *reinterpret_cast<uint2*>(h1s + r * H1S_LD + c * 8) =
-          *reinterpret_cast<const uint2*>(H1 + (size_t)r * HID + c * 8);
-      *reinterpret_cast<uint2*>(h1s + r * H1S_LD + c * 8 + 4) =
-          *reinterpret_cast<const uint2*>(H1 + (size_t)r * HID + c * 8 + 4);
+  // Row constants of rows [r0, r0 + nrows) at LDS index (row - r0).
+  auto stage_rows = [&](int r0, int nrows) {
+    for (int i = tid; i < nrows; i += BWD_THREADS) {
+      const int r = r0 + i;
+      crow_s[i] = r < B ? log2_invB - lse[r] * LOG2E : -INFINITY;
+      tw_s[i] = r < B ? rw[r] * invB : 0.0f;
     }
-    const int cpr = bpad >> 3;
-    for (int e = tid; e < HID * cpr; e += 64 * BWD_WAVES) {
-      const int h = e / cpr, c = e - h * cpr;
-      *reinterpret_cast<uint2*>(h1ts + h * H1TS_LD + c * 8) =
-          *reinterpret_cast<const uint2*>(H1T + (size_t)h * ld_t + c * 8);
-      *reinterpret_cast<uint2*>(h1ts + h * H1TS_LD + c * 8 + 4) =
-          *reinterpret_cast<const uint2*>(H1T + (size_t)h * ld_t + c * 8 + 4);
+  };
+  // Target bits of this wave's labels for rows [r0, r0 + nrows): mask[label][row block].
+  auto build_mask = [&](int l0, int lo, int hi, int r0, int nrows) {
+    for (int k = lane; k < 32 * mstride; k += 64) mask[k] = 0u;
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    for (int q = lo + lane; q < hi; q += 64) {
+      const int row = lrow[svals[q] - label_base] - r0;
+      if (row >= 0 && row < nrows)
+        atomicOr(&mask[(skeys[q] - F - l0) * mstride + (row >> 5)], 1u << (row & 31));
     }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  };
+
+  if constexpr (MODE == BWD_STAGED) {
+    stage_h1(h1s, h1ts, H1, H1T, ld_t, 0, bpad);
+    stage_rows(0, bpad);
+    __syncthreads();
+  } else if constexpr (MODE == BWD_GLOBAL) {
+    stage_rows(0, bpad);
+    __syncthreads();
   }
-  __syncthreads();
-  const E* h1 = STAGE ? h1s : H1;
-  const int ldh = STAGE ? H1S_LD : HID;
-  const E* h1t = STAGE ? h1ts : H1T;
-  const int ldht = STAGE ? H1TS_LD : ld_t;
+  const E* h1 = LDS_H1 ? h1s : H1;
+  const int ldh = LDS_H1 ? H1S_LD : HID;
+  const E* h1t = LDS_H1 ? h1ts : H1T;
+  const int ldht = LDS_H1 ? H1TS_LD : ld_t;
 
   const int n_blocks = (L + 31) >> 5;
-  for (int blk = blockIdx.x * BWD_WAVES + wave; blk < n_blocks; blk += gridDim.x * BWD_WAVES) {
+  // staged / global: each wave walks its own blocks; chunked: the workgroup
+  // walks groups of 8 blocks together (a uniform trip count for the barriers)
+  const int n_iter_units = MODE == BWD_CHUNKED ? (n_blocks + BWD_WAVES - 1) / BWD_WAVES : n_blocks;
+  const int first = MODE == BWD_CHUNKED ? blockIdx.x : blockIdx.x * BWD_WAVES + wave;
+  const int step = MODE == BWD_CHUNKED ? gridDim.x : gridDim.x * BWD_WAVES;
+  for (int unit = first; unit < n_iter_units; unit += step) {
+    const int blk = MODE == BWD_CHUNKED ? unit * BWD_WAVES + wave : unit;
+    const bool bactive = blk < n_blocks;
     const int l0 = blk * 32;
     const int label = l0 + n;
     const bool lvalid = label < L;
@@ -125,19 +170,13 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void k_out_bwd(
         }
       }
 
-    // true (row, label) pairs of these 32 labels -> bit mask [label][row block]
-    const int lo = lower_bound_dev(skeys, n_keys, F + l0);
-    const int hi = lower_bound_dev(skeys, n_keys, F + min(l0 + 32, L));
-    const bool has_targets = hi > lo;
-    if (has_targets) {
-      for (int k = lane; k < 32 * nrb; k += 64) mask[k] = 0u;
-      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-      for (int q = lo + lane; q < hi; q += 64) {
-        const int row = lrow[svals[q] - label_base];
-        atomicOr(&mask[(skeys[q] - F - l0) * nrb + (row >> 5)], 1u << (row & 31));
-      }
-      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    // true (row, label) pairs of these 32 labels: a range of the sorted keys
+    int lo = 0, hi = 0;
+    if (bactive) {
+      lo = lower_bound_dev(skeys, n_keys, F + l0);
+      hi = lower_bound_dev(skeys, n_keys, F + min(l0 + 32, L));
     }
+    const bool has_targets = hi > lo;
 
     f32x16 accw[4];
 #pragma unroll
@@ -146,11 +185,12 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void k_out_bwd(
       for (int r = 0; r < 16; ++r) accw[hb][r] = 0.0f;
     float db2p = 0.0f;
 
-    for (int rb = 0; rb < nrb; ++rb) {
+    // one 32-row block: rb indexes the rows held in LDS / the row constants
+    auto row_block = [&](int rb, int grow0) {
       f32x16 z;
 #pragma unroll
       for (int r = 0; r < 16; ++r) z[r] = 0.0f;
-      const E* hrow = h1 + (size_t)(rb * 32 + n) * ldh;
+      const E* hrow = h1 + (size_t)((LDS_H1 ? rb * 32 : grow0) + n) * ldh;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -164,11 +204,9 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void k_out_bwd(
       }
       float dz[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        dz[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, bb) + cr[r]);
-      }
+      for (int r = 0; r < 16; ++r) dz[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, bb) + cr[r]);
       if (has_targets) {
-        const uint32_t mw = mask[n * nrb + rb];
+        const uint32_t mw = mask[n * mstride + rb];
         if (__any(mw != 0u)) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
@@ -185,13 +223,30 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void k_out_bwd(
       for (int c = 0; c < NCH; ++c) df[c] = frag_acc<BF16>(dz, c);
 #pragma unroll
       for (int hb = 0; hb < 4; ++hb) {
-        const E* trow = h1t + (size_t)(32 * hb + n) * ldht + rb * 32;
+        const E* trow = h1t + (size_t)(32 * hb + n) * ldht + (LDS_H1 ? rb * 32 : grow0);
 #pragma unroll
         for (int c = 0; c < NCH; ++c) accw[hb] = M::mma(frag_row<BF16>(trow, c, g), df[c], accw[hb]);
       }
+    };
+
+    if constexpr (MODE == BWD_CHUNKED) {
+      for (int c0 = 0; c0 < bpad; c0 += BWD_CHUNK) {
+        const int crows = min(BWD_CHUNK, bpad - c0);
+        __syncthreads();  // every wave is done with the previous chunk
+        stage_h1(h1s, h1ts, H1, H1T, ld_t, c0, crows);
+        stage_rows(c0, crows);
+        if (has_targets) build_mask(l0, lo, hi, c0, crows);
+        __syncthreads();
+        if (bactive)
+          for (int rb = 0; rb < (crows >> 5); ++rb) row_block(rb, c0 + rb * 32);
+      }
+    } else {
+      if (has_targets) build_mask(l0, lo, hi, 0, bpad);
+      for (int rb = 0; rb < nrb; ++rb) row_block(rb, rb * 32);
     }
+
     const float db2 = db2p + __shfl_xor(db2p, 32);
-    if (lvalid) {
+    if (bactive && lvalid) {
       float* wout = W2 + (size_t)label * HID;
 #pragma unroll
       for (int hb = 0; hb < 4; ++hb)
@@ -211,7 +266,7 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void k_out_bwd(
   }
 }
 
-template <bool BF16, bool STAGE>
+template <bool BF16, int MODE>
 static hipError_t launch_bwd(int grid, size_t shm, hipStream_t st, float* W2, float* b2, int L, int F,
                              const void* H1, const void* H1T, int ld_t, int B, const float* lse,
                              const float* rw, const int32_t* skeys, const int32_t* svals, int n_keys,
@@ -220,14 +275,14 @@ static hipError_t launch_bwd(int grid, size_t shm, hipStream_t st, float* W2, fl
   const float log2_invB = (float)log2((double)invB);
   static bool attr_done = false;
   if (!attr_done) {
-    hipError_t e = hipFuncSetAttribute((const void*)k_out_bwd<BF16, STAGE>,
+    hipError_t e = hipFuncSetAttribute((const void*)k_out_bwd<BF16, MODE>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (e != hipSuccess) return e;
     attr_done = true;
   }
-  hipLaunchKernelGGL((k_out_bwd<BF16, STAGE>), dim3(grid), dim3(64 * BWD_WAVES), shm, st, W2, b2, L,
-                     F, (const E*)H1, (const E*)H1T, ld_t, B, lse, rw, skeys, svals, n_keys,
-                     label_base, lrow, lr, invB, log2_invB);
+  hipLaunchKernelGGL((k_out_bwd<BF16, MODE>), dim3(grid), dim3(BWD_THREADS), shm, st, W2, b2, L, F,
+                     (const E*)H1, (const E*)H1T, ld_t, B, lse, rw, skeys, svals, n_keys, label_base,
+                     lrow, lr, invB, log2_invB);
   return hipGetLastError();
 }
 
@@ -236,23 +291,23 @@ hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, int F, con
                           const int32_t* skeys, const int32_t* svals, int n_keys, int label_base,
                           const int32_t* lrow, float lr, int n_cu, hipStream_t st) {
   const int nrb = (B + 31) / 32;
-  const bool stage = use_bf16 && B <= BWD_STAGE_ROWS;
-  size_t shm = (size_t)2 * nrb * 32 * sizeof(float) + (size_t)BWD_WAVES * 32 * nrb * sizeof(uint32_t);
-  if (stage) shm += (size_t)BWD_STAGE_ROWS * H1S_LD * 2 + (size_t)HID * H1TS_LD * 2;
+  const int mode = !use_bf16 ? BWD_GLOBAL : (B <= BWD_CHUNK ? BWD_STAGED : BWD_CHUNKED);
+  const int span = mode == BWD_CHUNKED ? BWD_CHUNK : nrb * 32;
+  size_t shm = (size_t)2 * span * sizeof(float) + (size_t)BWD_WAVES * 32 * (span / 32) * sizeof(uint32_t);
+  if (mode != BWD_GLOBAL) shm += (size_t)BWD_CHUNK * H1S_LD * 2 + (size_t)HID * H1TS_LD * 2;
   const int n_blocks = (L + 31) / 32;
   int grid = (n_blocks + BWD_WAVES - 1) / BWD_WAVES;
-  const int cap = stage ? n_cu : 2 * n_cu;
+  const int cap = mode == BWD_GLOBAL ? 2 * n_cu : n_cu;
   if (grid > cap) grid = cap;
   const float invB = 1.0f / (float)B;
-  if (use_bf16) {
-    if (stage)
-      return launch_bwd<true, true>(grid, shm, st, W2, b2, L, F, H1, H1T, ld_t, B, lse, rw, skeys,
-                                    svals, n_keys, label_base, lrow, lr, invB);
-    return launch_bwd<true, false>(grid, shm, st, W2, b2, L, F, H1, H1T, ld_t, B, lse, rw, skeys,
-                                   svals, n_keys, label_base, lrow, lr, invB);
-  }
-  return launch_bwd<false, false>(grid, shm, st, W2, b2, L, F, H1, H1T, ld_t, B, lse, rw, skeys,
-                                  svals, n_keys, label_base, lrow, lr, invB);
+  if (mode == BWD_STAGED)
+    return launch_bwd<true, BWD_STAGED>(grid, shm, st, W2, b2, L, F, H1, H1T, ld_t, B, lse, rw, skeys,
+                                        svals, n_keys, label_base, lrow, lr, invB);
+  if (mode == BWD_CHUNKED)
+    return launch_bwd<true, BWD_CHUNKED>(grid, shm, st, W2, b2, L, F, H1, H1T, ld_t, B, lse, rw, skeys,
+                                         svals, n_keys, label_base, lrow, lr, invB);
+  return launch_bwd<false, BWD_GLOBAL>(grid, shm, st, W2, b2, L, F, H1, H1T, ld_t, B, lse, rw, skeys,
+                                       svals, n_keys, label_base, lrow, lr, invB);
 }
 
 }  // namespace asgd
