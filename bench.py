@@ -54,8 +54,10 @@ def kernel_model(w, B, nnz, lnnz, uniq):
     return {
         # reads the touched W1 rows once, the batch's (id, value) pairs; writes A1 and H1 (2 layouts)
         "gather": dict(bytes=uniq * H * 4 + nnz * 8 + B * H * (4 + 2 * op), flops=2.0 * nnz * H),
-        # two radix passes over (key, position) of every feature and label entry
-        "sort": dict(bytes=2 * (nnz + lnnz) * 4 * 5, flops=0.0),
+        # two radix passes over (key, position) of every feature entry
+        "sort": dict(bytes=2 * nnz * 4 * 5, flops=0.0),
+        # label entries: read (label, row), write the grouped pairs and the block offsets
+        "labels": dict(bytes=lnnz * 12 + (L // 32 + 1) * 4, flops=0.0),
         # reads W2 and b2 once; Z = H1 W2^T and O = P W2 (the dense part of dH1)
         "out_fwd": dict(bytes=4.0 * L * (H + 1), flops=4.0 * B * H * L),
         "out_combine": dict(bytes=B * H * 4 * 2 + lnnz * H * 4, flops=2.0 * lnnz * H),
@@ -271,11 +273,12 @@ def main():
                          "GB/s": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
                          "TFLOP/s": round(tfs, 2), "mfma_frac": round(tfs / MFMA_PEAK_TFLOPS[dtype], 4),
                          "share_of_step": round(tot / ms, 4)}
-        if name == "sort":
+        if name in ("sort", "labels"):
             kernels[name]["overlapped"] = True
-    # the sort runs on the library's second stream, overlapped with the output-layer
-    # forward: its event span includes time it waited for CUs, so it is not a candidate
-    dom = max((k for k in kt if k != "sort"), key=lambda k: kt[k][0])
+    # the sort and the label grouping run on the library's second stream, overlapped
+    # with the output layer: their event spans include time spent waiting for CUs,
+    # so they are not candidates
+    dom = max((k for k in kt if k not in ("sort", "labels")), key=lambda k: kt[k][0])
     if args.workload == "wide-label":
         # the merge of the elastic configuration: 4 replicas of this model
         kernels["merge"] = measure_merge(w, 4, 10, stream)

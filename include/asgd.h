@@ -61,7 +61,7 @@ typedef enum asgd_status {
 
 typedef struct asgd_config {
   int32_t n_features;    /* F >= 1 */
-  int32_t n_labels;      /* L >= 1 */
+  int32_t n_labels;      /* L in [1, 2^22) */
   int32_t hidden;        /* H; must be 128 */
   int32_t max_batch;     /* largest B any call will use (memory pool sized for it, Sec. 4) */
   int32_t max_nnz;       /* largest sum of nnz over the rows of one batch */
@@ -300,14 +300,15 @@ asgd_status asgd_debug_touched_rows(asgd_model* m, const asgd_csr* x, int32_t* i
 /* Kernel groups that can be timed. */
 enum {
   ASGD_K_GATHER = 0,      /* first-layer gather + sort keys */
-  ASGD_K_SORT = 1,        /* all radix-sort passes of one step */
+  ASGD_K_SORT = 1,        /* radix sort of the batch's feature ids (internal stream) */
   ASGD_K_OUT_FWD = 2,     /* output-layer forward over all labels */
   ASGD_K_OUT_COMBINE = 3, /* per-row merge of label splits, loss, dA1 */
   ASGD_K_HIDDEN = 4,      /* b1 gradient / update and mean loss */
   ASGD_K_OUT_BWD = 5,     /* output-layer backward + W2/b2 update */
   ASGD_K_W1_UPDATE = 6,   /* sparse W1 gradient + update */
   ASGD_K_MERGE = 7,       /* normalized merge (timed on the global model) */
-  ASGD_K_COUNT = 8
+  ASGD_K_LABELS = 8,      /* (label, row) pairs grouped by label block (internal stream) */
+  ASGD_K_COUNT = 9
 };
 
 /* enable != 0: from now on, bracket each kernel group launched for this model

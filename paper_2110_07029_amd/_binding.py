@@ -35,7 +35,7 @@ EXPORTS = (
 ASGD_CLOCK_TIMED, ASGD_CLOCK_VIRTUAL = 0, 1
 
 # Kernel groups of asgd_model_get_timing.
-KERNELS = ("gather", "sort", "out_fwd", "out_combine", "hidden", "out_bwd", "w1_update", "merge")
+KERNELS = ("gather", "sort", "out_fwd", "out_combine", "hidden", "out_bwd", "w1_update", "merge", "labels")
 
 
 class AsgdError(RuntimeError):

@@ -65,8 +65,9 @@ struct asgd_model {
   hipStream_t stream = nullptr;
   int device = 0;
   int n_cu = 256;
-  hipStream_t aux = nullptr;      // internal stream: the sort overlaps the output-layer forward
-  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  // internal stream: the label grouping and the feature sort overlap the output layer
+  hipStream_t aux = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_labels = nullptr, ev_join = nullptr;
   hipEvent_t ev = nullptr;
 
   // parameters
@@ -98,6 +99,10 @@ struct asgd_model {
   int32_t* hist = nullptr;
   int32_t* row_of = nullptr;
   int32_t* lrow = nullptr;
+  int32_t* lkeys = nullptr;
+  int32_t* lpair = nullptr;
+  int32_t* lbeg = nullptr;
+  int32_t* lcnt = nullptr;
   float* m_part = nullptr;
   float* s_part = nullptr;
   float* o_part = nullptr;
@@ -127,8 +132,9 @@ int64_t layout_workspace(asgd_model* m, char* base) {
   const asgd_config& c = m->cfg;
   const int RB = out_rows_per_block(m->bf16);
   const int rp = m->rows_pad_max;
-  const int64_t n_keys = (int64_t)c.max_nnz + c.max_label_nnz;
+  const int64_t n_keys = c.max_nnz;  // the radix sort orders feature entries only
   const int nblk = sort_blocks((int)std::max<int64_t>(n_keys, 1));
+  const int64_t n_lblocks = (m->L + 31) / 32;
   const int nrb = rp / RB;
   const int n_tiles = (m->L + OUT_TILE - 1) / OUT_TILE;
   // (split, row) pairs: splits <= min(n_tiles, ceil(kFwdWgs / nRB)) for every nRB <= nrb
@@ -163,6 +169,10 @@ int64_t layout_workspace(asgd_model* m, char* base) {
   m->hist = carve<int32_t>(p, 2 * ((int64_t)nblk << SORT_MAX_BITS));
   m->row_of = carve<int32_t>(p, (int64_t)c.max_nnz + 1);
   m->lrow = carve<int32_t>(p, (int64_t)c.max_label_nnz + 1);
+  m->lkeys = carve<int32_t>(p, (int64_t)c.max_label_nnz + 1);
+  m->lpair = carve<int32_t>(p, (int64_t)c.max_label_nnz + 1);
+  m->lbeg = carve<int32_t>(p, n_lblocks + 1);
+  m->lcnt = carve<int32_t>(p, n_lblocks + 1);
   m->m_part = carve<float>(p, part_rows);
   m->s_part = carve<float>(p, part_rows);
   m->o_part = carve<float>(p, part_rows * HID);
@@ -254,7 +264,7 @@ asgd_status run_gather(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int*
   CsrDev xd = dev(x);
   CsrDev yd = y ? dev(y) : CsrDev{};
   TIMED(m, ASGD_K_GATHER, launch_gather_fwd(m->bf16, xd, y ? &yd : nullptr, m->W1(), m->b1(), m->F, m->L, m->A1,
-                            m->H1, m->H1T, rows_pad, m->rows_pad_max, m->keys, m->row_of, m->lrow,
+                            m->H1, m->H1T, rows_pad, m->rows_pad_max, m->keys, m->row_of, m->lkeys, m->lrow,
                             m->rw, m->err, validate ? 1 : 0, m->stream));
   if (validate) {
     int32_t e = 0;
@@ -275,7 +285,7 @@ asgd_status run_gather(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int*
 
 asgd_status run_sort(asgd_model* m, hipStream_t st, int n_keys, const int32_t** sk,
                      const int32_t** sv) {
-  const int key_bits = bit_width((uint32_t)(m->F + m->L));
+  const int key_bits = bit_width((uint32_t)m->F);  // invalid ids carry key F
   TIMED_ON(m, ASGD_K_SORT, st,
            launch_sort(m->keys, n_keys, key_bits, m->ka, m->va, m->kb, m->vb, m->hist, sk, sv, st));
   return ASGD_OK;
@@ -319,6 +329,8 @@ asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t s
     return fail(ASGD_EINVAL, "n_features and n_labels must be >= 1");
   if ((int64_t)cfg->n_features + cfg->n_labels >= (1 << 30))
     return fail(ASGD_ERANGE, "n_features + n_labels must be < 2^30");
+  if (cfg->n_labels >= (1 << 22))  // W2 is read through 32-bit buffer offsets
+    return fail(ASGD_ERANGE, "n_labels must be < 2^22");
   if (cfg->max_batch < 1 || cfg->max_batch > kMaxBatch)
     return fail(ASGD_ERANGE, "max_batch must be in [1, 2048]");
   if (cfg->max_nnz < 0 || cfg->max_label_nnz < 0)
@@ -349,6 +361,7 @@ asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t s
     e = hipDeviceGetAttribute(&m->n_cu, hipDeviceAttributeMultiprocessorCount, m->device);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_fork, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_labels, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_join, hipEventDisableTiming);
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&m->aux, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipMalloc((void**)&m->params, m->n_pad * sizeof(float));
@@ -389,6 +402,7 @@ asgd_status asgd_model_free(asgd_model* m) {
   if (m->ws) (void)hipFree(m->ws);
   if (m->ev) (void)hipEventDestroy(m->ev);
   if (m->ev_fork) (void)hipEventDestroy(m->ev_fork);
+  if (m->ev_labels) (void)hipEventDestroy(m->ev_labels);
   if (m->ev_join) (void)hipEventDestroy(m->ev_join);
   if (m->aux) (void)hipStreamDestroy(m->aux);
   for (auto& v : m->tev)
@@ -474,21 +488,25 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   int rows_pad = 0;
   s = run_gather(m, x, y, &rows_pad);
   if (s) return s;
-  // the sort depends only on the keys the gather wrote: run it on the internal
-  // stream, concurrently with the output-layer forward and combine
-  const int n_keys = x->nnz + y->nnz;
+  // The label grouping and the feature sort depend only on what the gather
+  // wrote: they run on the internal stream, overlapped with the output-layer
+  // forward; the backward waits for the label groups, the W1 update for the sort.
   const int32_t *sk = nullptr, *sv = nullptr;
   HIP_TRY(hipEventRecord(m->ev_fork, m->stream));
   HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_fork, 0));
-  s = run_sort(m, m->aux, n_keys, &sk, &sv);
+  TIMED_ON(m, ASGD_K_LABELS, m->aux,
+           launch_label_blocks(m->lkeys, y->nnz, m->L, m->lrow, m->lbeg, m->lpair, m->lcnt, m->aux));
+  HIP_TRY(hipEventRecord(m->ev_labels, m->aux));
+  s = run_sort(m, m->aux, x->nnz, &sk, &sv);
   if (s) return s;
   HIP_TRY(hipEventRecord(m->ev_join, m->aux));
   s = run_forward(m, x, y, rows_pad);
   if (s) return s;
   TIMED(m, ASGD_K_HIDDEN, launch_hidden_bias(B, m->dA1, m->b1(), lr, m->loss_rows, m->loss, m->stream));
+  HIP_TRY(hipStreamWaitEvent(m->stream, m->ev_labels, 0));
+  TIMED(m, ASGD_K_OUT_BWD, launch_out_bwd(m->bf16, m->W2(), m->b2(), m->L, m->H1, m->H1T, m->rows_pad_max, B,
+                         m->lse, m->rw, m->lbeg, m->lpair, lr, m->n_cu, m->stream));
   HIP_TRY(hipStreamWaitEvent(m->stream, m->ev_join, 0));
-  TIMED(m, ASGD_K_OUT_BWD, launch_out_bwd(m->bf16, m->W2(), m->b2(), m->L, m->F, m->H1, m->H1T, m->rows_pad_max, B,
-                         m->lse, m->rw, sk, sv, n_keys, x->nnz, m->lrow, lr, m->n_cu, m->stream));
   CsrDev xd = dev(x);
   TIMED(m, ASGD_K_W1_UPDATE, launch_w1_update(m->W1(), m->F, sk, sv, x->nnz, m->row_of, xd, m->dA1, lr, m->stream));
   if (loss_out) return asgd_model_last_loss(m, loss_out);

@@ -25,14 +25,14 @@ hipError_t launch_fill_int(int32_t* p, int32_t v, int64_t n, hipStream_t st);
 // ---- first layer forward + sort keys ---------------------------------------
 // A1 = X W1 + b1 (fp32), H1 = ReLU(A1) as the output layer's operand type in
 // row-major [rows_pad x 128] and transposed [128 x ld_t]; rows in [B, rows_pad)
-// are zero.  With y != NULL also writes the label sort keys.  Keys: feature
-// entry p (0 <= p < x.nnz) -> key[p] = feature id; label entry q -> key[x.nnz + q]
-// = F + label id; invalid ids get key F + L.  row_of[p] / lrow[q] = row index,
-// rw[i] = 1/|Y_i|.
+// are zero.  Feature entry p (0 <= p < x.nnz): keys[p] = feature id (F if
+// invalid), row_of[p] = its row.  With y != NULL, label entry q: lkeys[q] =
+// label id (L if invalid), lrow[q] = its row, and rw[i] = 1/|Y_i|.
 hipError_t launch_gather_fwd(bool use_bf16, const CsrDev& x, const CsrDev* y, const float* W1,
                              const float* b1, int F, int L, float* A1, void* H1, void* H1T,
                              int rows_pad, int ld_t, int32_t* keys, int32_t* row_of,
-                             int32_t* lrow, float* rw, int32_t* err, int validate, hipStream_t st);
+                             int32_t* lkeys, int32_t* lrow, float* rw, int32_t* err, int validate,
+                             hipStream_t st);
 
 // ---- stable LSD radix sort of (key, position) -----------------------------
 constexpr int SORT_CHUNK = 1024;   // keys per workgroup
@@ -44,6 +44,14 @@ int sort_blocks(int n);
 hipError_t launch_sort(const int32_t* keys_in, int n, int key_bits, int32_t* keys_a,
                        int32_t* vals_a, int32_t* keys_b, int32_t* vals_b, int32_t* hist,
                        const int32_t** keys_out, const int32_t** vals_out, hipStream_t st);
+
+// ---- (label, row) pairs grouped by 32-label block ---------------------------
+// For the m label entries: lbeg[b] .. lbeg[b+1] (b < ceil(L/32)) is the range
+// of block b's pairs in lpair, each (row << 5) | (label % 32); invalid labels
+// (key L) are dropped.  gcnt: ceil(L/32) ints of scratch, used only when the
+// counters do not fit in LDS.
+hipError_t launch_label_blocks(const int32_t* lkeys, int m, int L, const int32_t* lrow, int32_t* lbeg,
+                               int32_t* lpair, int32_t* gcnt, hipStream_t st);
 
 // ---- output layer -----------------------------------------------------------
 constexpr int OUT_TILE = 32;  // labels per forward tile
@@ -63,10 +71,10 @@ hipError_t launch_out_combine(bool use_bf16, int B, int splits, const float* m_p
 hipError_t launch_hidden_bias(int B, const float* dA1, float* b1, float lr, const float* loss_rows,
                               float* loss, hipStream_t st);
 // Recompute Z per label tile, dZ = (softmax - T)/B, dW2 = dZ^T H1, db2; update W2, b2 in place.
-hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, int F, const void* H1,
+hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, const void* H1,
                           const void* H1T, int ld_t, int B, const float* lse, const float* rw,
-                          const int32_t* skeys, const int32_t* svals, int n_keys, int label_base,
-                          const int32_t* lrow, float lr, int n_cu, hipStream_t st);
+                          const int32_t* lbeg, const int32_t* lpair, float lr, int n_cu,
+                          hipStream_t st);
 // W1[f] -= lr * sum_{entries of f} x * dA1[row], one segment per distinct f.
 hipError_t launch_w1_update(float* W1, int F, const int32_t* skeys, const int32_t* svals,
                             int n_feat_keys, const int32_t* row_of, const CsrDev& x,

@@ -61,7 +61,8 @@ __global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
     CsrDev x, CsrDev y, int has_y, const float* __restrict__ W1, const float* __restrict__ b1,
     int F, int L, float* __restrict__ A1, typename Mma<BF16>::elem* __restrict__ H1,
     typename Mma<BF16>::elem* __restrict__ H1T, int rows_pad, int ld_t, int32_t* __restrict__ keys,
-    int32_t* __restrict__ row_of, int32_t* __restrict__ lrow, float* __restrict__ rw,
+    int32_t* __restrict__ row_of, int32_t* __restrict__ lkeys, int32_t* __restrict__ lrow,
+    float* __restrict__ rw,
     int32_t* __restrict__ err, int validate) {
   using E = typename Mma<BF16>::elem;
   __shared__ float2 part[GATHER_WAVES][64];
@@ -99,7 +100,7 @@ __global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
       int key = f;
       if (f < 0 || f >= F) {
         bad |= ERR_FEATURE_ID;
-        key = F + L;
+        key = F;  // sorts after every feature; the W1 update skips it
         f = -1;
       } else if (validate && p > s && x.indices[p - 1] >= f) {
         bad |= ERR_DUPLICATE;
@@ -155,14 +156,14 @@ __global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
     if (lane == 0) rw[i] = ye > ys ? 1.0f / (float)(ye - ys) : 0.0f;
     for (int q = ys + lane; q < ye; q += 64) {
       const int lab = y.indices[q];
-      int key = F + lab;
+      int key = lab;
       if (lab < 0 || lab >= L) {
         bad |= ERR_LABEL_ID;
-        key = F + L;
+        key = L;  // dropped when the pairs are grouped by label block
       } else if (validate && q > ys && y.indices[q - 1] >= lab) {
         bad |= ERR_DUPLICATE;
       }
-      keys[x.nnz + (q - ybase)] = key;
+      lkeys[q - ybase] = key;
       lrow[q - ybase] = i;
     }
   }
@@ -190,16 +191,17 @@ __global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
 hipError_t launch_gather_fwd(bool use_bf16, const CsrDev& x, const CsrDev* y, const float* W1,
                              const float* b1, int F, int L, float* A1, void* H1, void* H1T,
                              int rows_pad, int ld_t, int32_t* keys, int32_t* row_of,
-                             int32_t* lrow, float* rw, int32_t* err, int validate, hipStream_t st) {
+                             int32_t* lkeys, int32_t* lrow, float* rw, int32_t* err, int validate,
+                             hipStream_t st) {
   const dim3 grid(rows_pad), block(64 * GATHER_WAVES);
   CsrDev yy = y ? *y : CsrDev{0, 0, 0, nullptr, nullptr, nullptr};
   if (use_bf16)
     hipLaunchKernelGGL(k_gather_fwd<true>, grid, block, 0, st, x, yy, y != nullptr, W1, b1, F, L,
-                       A1, (bf16*)H1, (bf16*)H1T, rows_pad, ld_t, keys, row_of, lrow, rw, err,
+                       A1, (bf16*)H1, (bf16*)H1T, rows_pad, ld_t, keys, row_of, lkeys, lrow, rw, err,
                        validate);
   else
     hipLaunchKernelGGL(k_gather_fwd<false>, grid, block, 0, st, x, yy, y != nullptr, W1, b1, F, L,
-                       A1, (float*)H1, (float*)H1T, rows_pad, ld_t, keys, row_of, lrow, rw, err,
+                       A1, (float*)H1, (float*)H1T, rows_pad, ld_t, keys, row_of, lkeys, lrow, rw, err,
                        validate);
   return hipGetLastError();
 }

@@ -59,11 +59,11 @@ __device__ __forceinline__ void stage_h1(bf16* h1s, bf16* h1ts, const bf16* __re
 
 template <bool BF16, int MODE>
 __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
-    float* __restrict__ W2, float* __restrict__ b2, int L, int F,
+    float* __restrict__ W2, float* __restrict__ b2, int L,
     const typename Mma<BF16>::elem* __restrict__ H1, const typename Mma<BF16>::elem* __restrict__ H1T,
     int ld_t, int B, const float* __restrict__ lse, const float* __restrict__ rw,
-    const int32_t* __restrict__ skeys, const int32_t* __restrict__ svals, int n_keys,
-    int label_base, const int32_t* __restrict__ lrow, float lr, float invB, float log2_invB) {
+    const int32_t* __restrict__ lbeg, const int32_t* __restrict__ lpair, float lr, float invB,
+    float log2_invB) {
   using M = Mma<BF16>;
   using E = typename M::elem;
   using Fr = typename M::frag;
@@ -103,14 +103,16 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
       tw_s[i] = r < B ? rw[r] * invB : 0.0f;
     }
   };
-  // Target bits of this wave's labels for rows [r0, r0 + nrows): mask[label][row block].
-  auto build_mask = [&](int l0, int lo, int hi, int r0, int nrows) {
+  // Target bits of this wave's labels for rows [r0, r0 + nrows): mask[label][row block],
+  // from the block's (row << 5 | label % 32) pairs in lpair[lo, hi).
+  auto build_mask = [&](int lo, int hi, int r0, int nrows) {
     for (int k = lane; k < 32 * mstride; k += 64) mask[k] = 0u;
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     for (int q = lo + lane; q < hi; q += 64) {
-      const int row = lrow[svals[q] - label_base] - r0;
+      const int pr = lpair[q];
+      const int row = (pr >> 5) - r0;
       if (row >= 0 && row < nrows)
-        atomicOr(&mask[(skeys[q] - F - l0) * mstride + (row >> 5)], 1u << (row & 31));
+        atomicOr(&mask[(pr & 31) * mstride + (row >> 5)], 1u << (row & 31));
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   };
@@ -170,11 +172,11 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
         }
       }
 
-    // true (row, label) pairs of these 32 labels: a range of the sorted keys
+    // true (row, label) pairs of these 32 labels
     int lo = 0, hi = 0;
     if (bactive) {
-      lo = lower_bound_dev(skeys, n_keys, F + l0);
-      hi = lower_bound_dev(skeys, n_keys, F + min(l0 + 32, L));
+      lo = lbeg[blk];
+      hi = lbeg[blk + 1];
     }
     const bool has_targets = hi > lo;
 
@@ -235,13 +237,13 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
         __syncthreads();  // every wave is done with the previous chunk
         stage_h1(h1s, h1ts, H1, H1T, ld_t, c0, crows);
         stage_rows(c0, crows);
-        if (has_targets) build_mask(l0, lo, hi, c0, crows);
+        if (has_targets) build_mask(lo, hi, c0, crows);
         __syncthreads();
         if (bactive)
           for (int rb = 0; rb < (crows >> 5); ++rb) row_block(rb, c0 + rb * 32);
       }
     } else {
-      if (has_targets) build_mask(l0, lo, hi, 0, bpad);
+      if (has_targets) build_mask(lo, hi, 0, bpad);
       for (int rb = 0; rb < nrb; ++rb) row_block(rb, rb * 32);
     }
 
@@ -267,10 +269,10 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
 }
 
 template <bool BF16, int MODE>
-static hipError_t launch_bwd(int grid, size_t shm, hipStream_t st, float* W2, float* b2, int L, int F,
+static hipError_t launch_bwd(int grid, size_t shm, hipStream_t st, float* W2, float* b2, int L,
                              const void* H1, const void* H1T, int ld_t, int B, const float* lse,
-                             const float* rw, const int32_t* skeys, const int32_t* svals, int n_keys,
-                             int label_base, const int32_t* lrow, float lr, float invB) {
+                             const float* rw, const int32_t* lbeg, const int32_t* lpair, float lr,
+                             float invB) {
   using E = typename Mma<BF16>::elem;
   const float log2_invB = (float)log2((double)invB);
   static bool attr_done = false;
@@ -280,16 +282,15 @@ static hipError_t launch_bwd(int grid, size_t shm, hipStream_t st, float* W2, fl
     if (e != hipSuccess) return e;
     attr_done = true;
   }
-  hipLaunchKernelGGL((k_out_bwd<BF16, MODE>), dim3(grid), dim3(BWD_THREADS), shm, st, W2, b2, L, F,
-                     (const E*)H1, (const E*)H1T, ld_t, B, lse, rw, skeys, svals, n_keys, label_base,
-                     lrow, lr, invB, log2_invB);
+  hipLaunchKernelGGL((k_out_bwd<BF16, MODE>), dim3(grid), dim3(BWD_THREADS), shm, st, W2, b2, L,
+                     (const E*)H1, (const E*)H1T, ld_t, B, lse, rw, lbeg, lpair, lr, invB, log2_invB);
   return hipGetLastError();
 }
 
-hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, int F, const void* H1,
+hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, const void* H1,
                           const void* H1T, int ld_t, int B, const float* lse, const float* rw,
-                          const int32_t* skeys, const int32_t* svals, int n_keys, int label_base,
-                          const int32_t* lrow, float lr, int n_cu, hipStream_t st) {
+                          const int32_t* lbeg, const int32_t* lpair, float lr, int n_cu,
+                          hipStream_t st) {
   const int nrb = (B + 31) / 32;
   const int mode = !use_bf16 ? BWD_GLOBAL : (B <= BWD_CHUNK ? BWD_STAGED : BWD_CHUNKED);
   const int span = mode == BWD_CHUNKED ? BWD_CHUNK : nrb * 32;
@@ -301,13 +302,13 @@ hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, int F, con
   if (grid > cap) grid = cap;
   const float invB = 1.0f / (float)B;
   if (mode == BWD_STAGED)
-    return launch_bwd<true, BWD_STAGED>(grid, shm, st, W2, b2, L, F, H1, H1T, ld_t, B, lse, rw, skeys,
-                                        svals, n_keys, label_base, lrow, lr, invB);
+    return launch_bwd<true, BWD_STAGED>(grid, shm, st, W2, b2, L, H1, H1T, ld_t, B, lse, rw, lbeg,
+                                        lpair, lr, invB);
   if (mode == BWD_CHUNKED)
-    return launch_bwd<true, BWD_CHUNKED>(grid, shm, st, W2, b2, L, F, H1, H1T, ld_t, B, lse, rw, skeys,
-                                         svals, n_keys, label_base, lrow, lr, invB);
-  return launch_bwd<false, BWD_GLOBAL>(grid, shm, st, W2, b2, L, F, H1, H1T, ld_t, B, lse, rw, skeys,
-                                       svals, n_keys, label_base, lrow, lr, invB);
+    return launch_bwd<true, BWD_CHUNKED>(grid, shm, st, W2, b2, L, H1, H1T, ld_t, B, lse, rw, lbeg,
+                                         lpair, lr, invB);
+  return launch_bwd<false, BWD_GLOBAL>(grid, shm, st, W2, b2, L, H1, H1T, ld_t, B, lse, rw, lbeg,
+                                       lpair, lr, invB);
 }
 
 }  // namespace asgd

@@ -46,20 +46,56 @@ struct TileRegs {
   float bias;
 };
 
-__device__ __forceinline__ void tile_load(const float* __restrict__ W2, const float* __restrict__ b2,
-                                          int L, int tile, TileRegs& r) {
-  // Out-of-range labels read the last row (always valid); their values are
-  // zeroed only when the tile is stored to LDS, so nothing consumes the loaded
-  // registers before the prefetch distance has elapsed.
+// W2 and b2 as raw buffer resources: a load past the end returns zeros (no
+// clamping or masking), and the uniform tile offset rides in a scalar register
+// while the per-thread offset is fixed for the whole kernel.
+struct W2Src {
+  __amdgpu_buffer_rsrc_t w, b;
+  int voff_w;  // bytes: row 2a, hidden 4q
+  int voff_b;  // bytes: label slot t % 32
+};
+
+constexpr int BUF_RSRC_WORD3 = 0x00020000;  // raw (unformatted) 32-bit buffer, gfx9 family
+
+__device__ __forceinline__ W2Src w2_src(const float* W2, const float* b2, int L) {
+  W2Src s;
+  s.w = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(W2), (short)0, L * HID * 4, BUF_RSRC_WORD3);
+  s.b = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(b2), (short)0, L * 4, BUF_RSRC_WORD3);
   const int tid = threadIdx.x, a = tid >> 5, q = tid & 31;
-#pragma unroll
-  for (int it = 0; it < 2; ++it) {
-    const int lab = tile * OUT_TILE + 2 * a + it;
-    r.v[it] = *reinterpret_cast<const float4*>(W2 + (size_t)min(lab, L - 1) * HID + 4 * q);
-  }
-  r.bias = b2[min(tile * OUT_TILE + (tid & (OUT_TILE - 1)), L - 1)];
+  s.voff_w = (2 * a * HID + 4 * q) * 4;
+  s.voff_b = (tid & (OUT_TILE - 1)) * 4;
+  return s;
 }
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// max(v[l], v[l ^ 32]) on every lane, without a trip through LDS: the swap
+// exchanges the upper half of one copy with the lower half of the other, so
+// the two results hold, on each lane, the lane's value and its partner's.
+__device__ __forceinline__ float half_swap_max(float v) {
+  const unsigned u = __builtin_bit_cast(unsigned, v);
+  const auto sw = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__builtin_bit_cast(float, sw[0]), __builtin_bit_cast(float, sw[1]));
+}
+
+__device__ __forceinline__ void tile_load(const W2Src& src, int tile, TileRegs& r) {
+  const int base = (int)((unsigned)tile * (unsigned)(OUT_TILE * HID * 4));
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    // (reinterpret the whole vector: bit casts of single elements of the
+    // builtin's result are folded into one narrowed load by this compiler)
+    const f32x4 v = __builtin_bit_cast(
+        f32x4, __builtin_amdgcn_raw_buffer_load_b128(src.w, src.voff_w + it * HID * 4, base, 0));
+    r.v[it] = make_float4(v.x, v.y, v.z, v.w);
+  }
+  r.bias = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(src.b, src.voff_b,
+                                                                          tile * OUT_TILE * 4, 0));
+}
+
+// Store a loaded tile into LDS as operands: row-major [label][hidden] and, if
+// TRANSPOSED, [hidden][label]; biases of labels past L become -inf (their
+// weights loaded as zeros, so those labels get probability 0).
 template <bool BF16, bool TRANSPOSED>
 __device__ __forceinline__ void tile_store(const TileRegs& r, int L, int tile,
                                            typename Mma<BF16>::elem* wr,
@@ -67,14 +103,9 @@ __device__ __forceinline__ void tile_store(const TileRegs& r, int L, int tile,
   using E = typename Mma<BF16>::elem;
   constexpr int WR = FwdShape<BF16>::WR, WT = FwdShape<BF16>::WT;
   const int tid = threadIdx.x, a = tid >> 5, q = tid & 31;
-  float x[2][4];
+  const float x[2][4] = {{r.v[0].x, r.v[0].y, r.v[0].z, r.v[0].w}, {r.v[1].x, r.v[1].y, r.v[1].z, r.v[1].w}};
 #pragma unroll
   for (int it = 0; it < 2; ++it) {
-    const bool ok = tile * OUT_TILE + 2 * a + it < L;
-    x[it][0] = ok ? r.v[it].x : 0.0f;
-    x[it][1] = ok ? r.v[it].y : 0.0f;
-    x[it][2] = ok ? r.v[it].z : 0.0f;
-    x[it][3] = ok ? r.v[it].w : 0.0f;
     E* d = wr + (2 * a + it) * WR + 4 * q;
     if constexpr (BF16) {
       bf16x4 p;
@@ -98,12 +129,17 @@ __device__ __forceinline__ void tile_store(const TileRegs& r, int L, int tile,
       }
     }
   }
-  if (threadIdx.x < OUT_TILE) bt[threadIdx.x] = tile * OUT_TILE + (int)threadIdx.x < L ? r.bias : -INFINITY;
+  // every thread writes its label slot's bias (threads sharing a slot write the
+  // same value), so the store needs no branch
+  const int sl = threadIdx.x & (OUT_TILE - 1);
+  bt[sl] = tile * OUT_TILE + sl < L ? r.bias : -INFINITY;
 }
 
 // ---------------------------------------------------------------------------
 // Forward, training: per (split, row) partial max, sum of exponentials and O.
 // ---------------------------------------------------------------------------
+constexpr int FWD_NBUF = 3;  // LDS ring of W2 tiles
+
 template <bool BF16>
 __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
     const float* __restrict__ W2, const float* __restrict__ b2, int L,
@@ -113,165 +149,185 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
   using M = Mma<BF16>;
   using E = typename M::elem;
   using Fr = typename M::frag;
-  constexpr int NB = FwdShape<BF16>::NB, WR = FwdShape<BF16>::WR, WT = FwdShape<BF16>::WT;
+  constexpr int WR = FwdShape<BF16>::WR, WT = FwdShape<BF16>::WT;
   constexpr int RB = FwdShape<BF16>::RB;
   constexpr int NCH = 32 / M::KC;
-  __shared__ __attribute__((aligned(16))) E wr[2][OUT_TILE * WR];
-  __shared__ __attribute__((aligned(16))) E wt[2][HID * WT];
-  __shared__ __attribute__((aligned(16))) float bt[2][OUT_TILE];
+  static_assert(FwdShape<BF16>::NB == 1, "one 32-row block per wave");
+  __shared__ __attribute__((aligned(16))) E wr[FWD_NBUF][OUT_TILE * WR];
+  __shared__ __attribute__((aligned(16))) E wt[FWD_NBUF][HID * WT];
+  __shared__ __attribute__((aligned(16))) float bt[FWD_NBUF][OUT_TILE];
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, g = lane >> 5, n = lane & 31;
+  const int lane = threadIdx.x & 63, g = lane >> 5, n = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int split = blockIdx.x;
   const int t_begin = split * tiles_per_split;
   const int t_end = min(n_tiles, t_begin + tiles_per_split);
-  const int row0 = blockIdx.y * RB + wave * 32 * NB;
-  const bool active = row0 < B;
+  const int t_last = t_end - 1;
+  // Rows past B (up to the 256-row padding, zero in H1) are computed like the
+  // others and never written out, so the loop has no row-dependent branch.
+  const int row0 = blockIdx.y * RB + wave * 32;
+  const W2Src src = w2_src(W2, b2, L);
 
   // H1^T as the B operand (K = hidden, N = rows), resident for the whole split.
-  Fr hf[NB][4][NCH];
+  Fr hf[4][NCH];
+  const E* hrow = H1 + (size_t)(row0 + n) * HID;
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const E* hrow = H1 + (size_t)(row0 + nb * 32 + n) * HID;
+  for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-      for (int c = 0; c < NCH; ++c) hf[nb][kb][c] = frag_row<BF16>(hrow + 32 * kb, c, g);
-  }
+    for (int c = 0; c < NCH; ++c) hf[kb][c] = frag_row<BF16>(hrow + 32 * kb, c, g);
   // Redefine the fragments once they have arrived (empty asm), so the loop below
   // never waits on these loads again and its wait counters track only the W2
   // prefetch.
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
+  for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) asm volatile("" : "+v"(hf[kb][c]));
+
+  // Z^T tile from LDS buffer `buf`: A = W2 rows (M = labels, K = hidden),
+  // B = H1^T; the accumulator starts at the labels' biases (-inf past L).
+  auto z_tile = [&](int buf) {
+    const float4* bq = reinterpret_cast<const float4*>(bt[buf]);
+    f32x16 z;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 b = bq[2 * q + g];
+      z[4 * q + 0] = b.x; z[4 * q + 1] = b.y; z[4 * q + 2] = b.z; z[4 * q + 3] = b.w;
+    }
+    const E* wrb = wr[buf] + n * WR;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) asm volatile("" : "+v"(hf[nb][kb][c]));
+      for (int c = 0; c < NCH; ++c) z = M::mma(frag_row<BF16>(wrb + 32 * kb, c, g), hf[kb][c], z);
+    return z;
+  };
 
-  float m_run[NB], s_run[NB];
-  f32x16 acc_o[NB][4];
+  float m_run = -INFINITY, s_run = 0.0f;
+  f32x16 acc_o[4];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    m_run[nb] = -INFINITY;
-    s_run[nb] = 0.0f;
+  for (int hb = 0; hb < 4; ++hb)
 #pragma unroll
-    for (int hb = 0; hb < 4; ++hb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc_o[nb][hb][r] = 0.0f;
-  }
+    for (int r = 0; r < 16; ++r) acc_o[hb][r] = 0.0f;
 
-  // Two tiles in flight: tile i+2 is loaded into registers while tile i is
-  // computed from LDS and tile i+1 (loaded one iteration earlier) is stored.
-  // The loop is unrolled by two so the register buffers are static.
-  TileRegs tr0, tr1;
-  // every split has at least one tile (the host sizes splits that way)
-  tile_load(W2, b2, L, t_begin, tr0);
-  tile_store<BF16, true>(tr0, L, t_begin, wr[0], wt[0], bt[0]);
-  tile_load(W2, b2, L, min(t_begin + 1, t_end - 1), tr1);
+  // Software pipeline over a ring of three LDS tiles.  In the iteration of
+  // tile t: the logits of tile t+1 go to the matrix cores while the softmax
+  // numerators of tile t are formed; then O^T += W2_t^T P_t^T while tile t+2
+  // (loaded into registers one iteration earlier) is converted into the ring
+  // and tile t+3 is loaded.  Tile indices are clamped to the split's last
+  // tile, so every load, store and product is unconditional (a clamped copy is
+  // never consumed).  Every split has at least one tile.
+  TileRegs tr;
+  tile_load(src, t_begin, tr);
+  tile_store<BF16, true>(tr, L, t_begin, wr[0], wt[0], bt[0]);
+  tile_load(src, min(t_begin + 1, t_last), tr);
+  tile_store<BF16, true>(tr, L, min(t_begin + 1, t_last), wr[1], wt[1], bt[1]);
+  tile_load(src, min(t_begin + 2, t_last), tr);
   __syncthreads();
+  f32x16 z = z_tile(0);
 
   // Online softmax in base 2 with lazy rescaling: p = 2^(z log2e - m2) where m2
   // is a per-row reference that is raised only when a tile's maximum exceeds it
   // by more than LAZY (so p <= 2^LAZY); the final normalisation uses the same
   // reference, so the result is exact up to rounding.
   constexpr float LAZY = 8.0f;
-  auto compute = [&](int t, int buf) {
-    const E* wrb = wr[buf];
-    const E* wtb = wt[buf];
-    // Z^T tile: A = W2 rows (M = labels, K = hidden), B = H1^T; the accumulator
-    // starts at the labels' biases (-inf for labels past L).
-    const float4* bq = reinterpret_cast<const float4*>(bt[buf]);
-    f32x16 z[NB];
+  int b0 = 0;
+  for (int t = t_begin; t < t_end; ++t) {
+    const int b1 = b0 == FWD_NBUF - 1 ? 0 : b0 + 1;
+    const int b2i = b1 == FWD_NBUF - 1 ? 0 : b1 + 1;
+    // Operands of this iteration's two products, read from LDS first so that
+    // their latency is covered by the max / rescale work below: A of the next
+    // tile's logits (W2 rows, with the biases as the accumulator's start) and
+    // A of this tile's O (W2^T rows).
+    // (fp32 operands take 16 chunks per 32-wide block: those are read at use,
+    // as holding them all would not fit the register file.)
+    constexpr int PRE = BF16 ? NCH : 1;
+    Fr za[4][PRE], oa[4][PRE];
+    const E* wrb = wr[b1] + n * WR;
+    const E* wtb = wt[b0];
+    if constexpr (BF16) {
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) za[kb][c] = frag_row<BF16>(wrb + 32 * kb, c, g);
+    }
+    f32x16 zn;
+    {
+      const float4* bq = reinterpret_cast<const float4*>(bt[b1]);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const float4 b = bq[2 * q + g];
-        z[nb][4 * q + 0] = b.x; z[nb][4 * q + 1] = b.y; z[nb][4 * q + 2] = b.z; z[nb][4 * q + 3] = b.w;
+        zn[4 * q + 0] = b.x; zn[4 * q + 1] = b.y; zn[4 * q + 2] = b.z; zn[4 * q + 3] = b.w;
       }
+    }
+    if constexpr (BF16) {
+#pragma unroll
+      for (int hb = 0; hb < 4; ++hb)
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) oa[hb][c] = frag_row<BF16>(wtb + (32 * hb + n) * WT, c, g);
+    }
+
+    // running maximum of this tile (rows are lanes: one max per lane pair)
+    float tmax = z[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) tmax = fmaxf(tmax, z[r]);
+    tmax = half_swap_max(tmax);
+    const float m2c = tmax * LOG2E;
+    if (__any(m2c > m_run + LAZY)) {
+      const float m2n = m2c > m_run + LAZY ? m2c : m_run;
+      const float scale = __builtin_amdgcn_exp2f(m_run - m2n);
+      s_run *= scale;
+#pragma unroll
+      for (int hb = 0; hb < 4; ++hb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc_o[hb][r] *= scale;
+      m_run = m2n;
+    }
+    // next tile's logits (matrix cores) ...
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) {
-        const Fr a = frag_row<BF16>(wrb + n * WR + 32 * kb, c, g);
+      for (int c = 0; c < NCH; ++c)
+        zn = M::mma(BF16 ? za[kb][c % PRE] : frag_row<BF16>(wrb + 32 * kb, c, g), hf[kb][c], zn);
+    // ... while this tile's numerators are formed (vector units)
+    float p[16];
+    float ps = 0.0f;
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) z[nb] = M::mma(a, hf[nb][kb][c], z[nb]);
-      }
-    Fr pf[NB][NCH];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      float tmax = z[nb][0];
-#pragma unroll
-      for (int r = 1; r < 16; ++r) tmax = fmaxf(tmax, z[nb][r]);
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-      const float m2c = tmax * LOG2E;
-      if (__any(m2c > m_run[nb] + LAZY)) {
-        const float m2n = m2c > m_run[nb] + LAZY ? m2c : m_run[nb];
-        const float scale = __builtin_amdgcn_exp2f(m_run[nb] - m2n);
-        s_run[nb] *= scale;
-#pragma unroll
-        for (int hb = 0; hb < 4; ++hb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) acc_o[nb][hb][r] *= scale;
-        m_run[nb] = m2n;
-      }
-      float p[16];
-      float ps = 0.0f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        p[r] = __builtin_amdgcn_exp2f(fmaf(z[nb][r], LOG2E, -m_run[nb]));
-        ps += p[r];
-      }
-      s_run[nb] += ps;
-#pragma unroll
-      for (int c = 0; c < NCH; ++c) pf[nb][c] = frag_acc<BF16>(p, c);
+    for (int r = 0; r < 16; ++r) {
+      p[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, -m_run));
+      ps += p[r];
     }
-    // O^T += W2_tile^T P^T : A = W2^T rows (M = hidden, K = labels).
+    s_run += ps;
+    Fr pf[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) pf[c] = frag_acc<BF16>(p, c);
+    // O^T += W2_t^T P^T : A = W2^T rows (M = hidden, K = labels).
 #pragma unroll
     for (int hb = 0; hb < 4; ++hb)
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) {
-        const Fr a = frag_row<BF16>(wtb + (32 * hb + n) * WT, c, g);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc_o[nb][hb] = M::mma(a, pf[nb][c], acc_o[nb][hb]);
-      }
-  };
-
-  // Loads and stores are unconditional (tile index clamped to the last tile; a
-  // redundant copy lands in the buffer nobody reads next), so no branch sits
-  // between a prefetch and its use.
-  const int t_last = t_end - 1;
-  for (int t = t_begin; t < t_end; t += 2) {
-    tile_load(W2, b2, L, min(t + 2, t_last), tr0);
-    if (active) compute(t, 0);
-    tile_store<BF16, true>(tr1, L, min(t + 1, t_last), wr[1], wt[1], bt[1]);
+      for (int c = 0; c < NCH; ++c)
+        acc_o[hb] = M::mma(BF16 ? oa[hb][c % PRE] : frag_row<BF16>(wtb + (32 * hb + n) * WT, c, g),
+                           pf[c], acc_o[hb]);
+    tile_store<BF16, true>(tr, L, min(t + 2, t_last), wr[b2i], wt[b2i], bt[b2i]);
+    tile_load(src, min(t + 3, t_last), tr);
     __syncthreads();
-    if (t + 1 >= t_end) break;
-    tile_load(W2, b2, L, min(t + 3, t_last), tr1);
-    if (active) compute(t + 1, 1);
-    tile_store<BF16, true>(tr0, L, min(t + 2, t_last), wr[0], wt[0], bt[0]);
-    __syncthreads();
+    z = zn;
+    b0 = b1;
   }
 
-  if (active) {
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int row = row0 + nb * 32 + n;
-      const float stot = s_run[nb] + __shfl_xor(s_run[nb], 32);
-      if (row < B) {
-        if (g == 0) {
-          m_part[(size_t)split * ld_part + row] = m_run[nb] * LN2;
-          s_part[(size_t)split * ld_part + row] = stot;
-        }
-        float* o = o_part + ((size_t)split * ld_part + row) * HID;
-#pragma unroll
-        for (int hb = 0; hb < 4; ++hb)
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-            *reinterpret_cast<float4*>(o + 32 * hb + 8 * q + 4 * g) =
-                make_float4(acc_o[nb][hb][4 * q], acc_o[nb][hb][4 * q + 1], acc_o[nb][hb][4 * q + 2],
-                            acc_o[nb][hb][4 * q + 3]);
-      }
+  const int row = row0 + n;
+  const float stot = s_run + __shfl_xor(s_run, 32);
+  if (row < B) {
+    if (g == 0) {
+      m_part[(size_t)split * ld_part + row] = m_run * LN2;
+      s_part[(size_t)split * ld_part + row] = stot;
     }
+    float* o = o_part + ((size_t)split * ld_part + row) * HID;
+#pragma unroll
+    for (int hb = 0; hb < 4; ++hb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<float4*>(o + 32 * hb + 8 * q + 4 * g) =
+            make_float4(acc_o[hb][4 * q], acc_o[hb][4 * q + 1], acc_o[hb][4 * q + 2],
+                        acc_o[hb][4 * q + 3]);
   }
 }
 
@@ -482,6 +538,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_topk(
   const int t_end = min(n_tiles, t_begin + tiles_per_split);
   const int row0 = blockIdx.y * RB + wave * WROWS;
   const bool active = row0 < B;
+  const W2Src src = w2_src(W2, b2, L);
 
   for (int e = lane; e < WROWS * TOPK_MAX; e += 64) {
     ls[wave][e / TOPK_MAX][e % TOPK_MAX] = -INFINITY;
@@ -498,14 +555,14 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_topk(
   }
   TileRegs tr;
   if (t_begin < t_end) {
-    tile_load(W2, b2, L, t_begin, tr);
+    tile_load(src, t_begin, tr);
     tile_store<BF16, false>(tr, L, t_begin, wr[0], nullptr, bt[0]);
   }
   __syncthreads();
   for (int t = t_begin; t < t_end; ++t) {
     const int buf = (t - t_begin) & 1;
     const bool has_next = t + 1 < t_end;
-    if (has_next) tile_load(W2, b2, L, t + 1, tr);
+    if (has_next) tile_load(src, t + 1, tr);
     if (active) {
       const E* wrb = wr[buf];
       f32x16 z[NB];
