@@ -100,6 +100,15 @@ __device__ __forceinline__ typename Mma<BF16>::frag frag_acc(const float* v, int
     return v[c];
 }
 
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+// ds_read_b64_tr_b16: a 64-bit LDS read whose 4 x 16-bit results are
+// transposed inside each group of 16 lanes.  Element i of result lane
+// 16G + 4a + b is element b of the 8 bytes that lane 16G + 4i + a addressed.
+__device__ __forceinline__ bf16x4 lds_read_tr16(const bf16* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
+}
+
 __device__ __forceinline__ int lower_bound_dev(const int32_t* __restrict__ a, int n, int key) {
   int lo = 0, hi = n;
   while (lo < hi) {

@@ -93,46 +93,116 @@ __device__ __forceinline__ void tile_load(const W2Src& src, int tile, TileRegs& 
                                                                           tile * OUT_TILE * 4, 0));
 }
 
-// Store a loaded tile into LDS as operands: row-major [label][hidden] and, if
-// TRANSPOSED, [hidden][label]; biases of labels past L become -inf (their
-// weights loaded as zeros, so those labels get probability 0).
+// ---- W2 tile in LDS, bf16 ---------------------------------------------------
+// [32 labels x 128 hidden], row stride 144 elements (consecutive rows 8 banks
+// apart), 16-byte chunks XOR-permuted by bit 2 of the row:
+//   (label, h) -> label * 144 + 8 * ((h / 8) ^ ((label / 4) % 2)) + h % 8.
+// Three access patterns are free of bank conflicts: the row fragments of the
+// logits (lane = label, 8 consecutive hidden units: one 16-byte read), the
+// transposed reads of the W2^T operand (16 lanes over 4 labels x 4 chunks of 4
+// hidden units) and the tile stores (16 lanes over one label row).  Every
+// fragment address is a per-lane base plus a compile-time offset.
+constexpr int TW_LD = 144;
+
+__device__ __forceinline__ int tw_off(int row, int col) {
+  return row * TW_LD + 8 * ((col >> 3) ^ ((row >> 2) & 1)) + (col & 7);
+}
+// Base of the row fragments of label row n for lane group g: hidden units
+// k + 8g .. k + 8g + 7 are at base + k for k a multiple of 16.
+__device__ __forceinline__ int tw_row_base(int n, int g) { return n * TW_LD + 8 * (g ^ ((n >> 2) & 1)); }
+// Base of the transposed reads: lane (n, g) of the result receives hidden unit
+// m0 + n at labels k + 4g + 0..3 (lo, at base + k * TW_LD + m0) and
+// k + 8 + 4g + 0..3 (hi, 8 rows further), k and m0 multiples of 16.  Source
+// lane (G, i, a) = (lane / 16, lane / 4 % 4, lane % 4) addresses label
+// 4 (G / 2) + i, hidden units 16 (G % 2) + 4a .. + 3.
+__device__ __forceinline__ int tw_col_base(int lane) {
+  const int G = lane >> 4, i = (lane >> 2) & 3, a = lane & 3;
+  return (4 * (G >> 1) + i) * TW_LD + 8 * (2 * (G & 1) + ((a >> 1) ^ (G >> 1))) + 4 * (a & 1);
+}
+
+// Store a loaded tile into LDS as operands.  bf16: the layout above, which
+// also serves the transposed operand.  fp32: row-major [label][hidden] (leading
+// dim WR) and, if TRANSPOSED, [hidden][label] (leading dim WT).  Biases of
+// labels past L become -inf (their weights loaded as zeros, so those labels
+// get probability 0).
+template <bool BF16>
+constexpr int tile_elems() {
+  return BF16 ? OUT_TILE * TW_LD : OUT_TILE * FwdShape<BF16>::WR;
+}
+template <bool BF16>
+constexpr int tileT_elems() {
+  return BF16 ? 1 : HID * FwdShape<BF16>::WT;
+}
+
 template <bool BF16, bool TRANSPOSED>
 __device__ __forceinline__ void tile_store(const TileRegs& r, int L, int tile,
                                            typename Mma<BF16>::elem* wr,
                                            typename Mma<BF16>::elem* wt, float* bt) {
-  using E = typename Mma<BF16>::elem;
   constexpr int WR = FwdShape<BF16>::WR, WT = FwdShape<BF16>::WT;
   const int tid = threadIdx.x, a = tid >> 5, q = tid & 31;
   const float x[2][4] = {{r.v[0].x, r.v[0].y, r.v[0].z, r.v[0].w}, {r.v[1].x, r.v[1].y, r.v[1].z, r.v[1].w}};
+  if constexpr (BF16) {
 #pragma unroll
-  for (int it = 0; it < 2; ++it) {
-    E* d = wr + (2 * a + it) * WR + 4 * q;
-    if constexpr (BF16) {
+    for (int it = 0; it < 2; ++it) {
       bf16x4 p;
       p[0] = (bf16)x[it][0]; p[1] = (bf16)x[it][1]; p[2] = (bf16)x[it][2]; p[3] = (bf16)x[it][3];
-      *reinterpret_cast<bf16x4*>(d) = p;
-    } else {
-      *reinterpret_cast<float4*>(d) = make_float4(x[it][0], x[it][1], x[it][2], x[it][3]);
+      *reinterpret_cast<bf16x4*>(wr + tw_off(2 * a + it, 4 * q)) = p;
     }
-  }
-  if constexpr (TRANSPOSED) {
+  } else {
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      E* d = wt + (4 * q + k) * WT + 2 * a;
-      if constexpr (BF16) {
-        bf16x2 p;
-        p[0] = (bf16)x[0][k];
-        p[1] = (bf16)x[1][k];
-        *reinterpret_cast<bf16x2*>(d) = p;
-      } else {
-        *reinterpret_cast<float2*>(d) = make_float2(x[0][k], x[1][k]);
-      }
+    for (int it = 0; it < 2; ++it)
+      *reinterpret_cast<float4*>(wr + (2 * a + it) * WR + 4 * q) =
+          make_float4(x[it][0], x[it][1], x[it][2], x[it][3]);
+    if constexpr (TRANSPOSED) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        *reinterpret_cast<float2*>(wt + (4 * q + k) * WT + 2 * a) = make_float2(x[0][k], x[1][k]);
     }
   }
   // every thread writes its label slot's bias (threads sharing a slot write the
   // same value), so the store needs no branch
   const int sl = threadIdx.x & (OUT_TILE - 1);
   bt[sl] = tile * OUT_TILE + sl < L ? r.bias : -INFINITY;
+}
+
+// Operand fragments of the logits Z^T = W2_tile H1^T (K = hidden).  With bf16
+// operands a lane's 8 values of chunk c of hidden block kb are the consecutive
+// units 32 kb + 16 c + 8 g .. + 7 on both sides (one 16-byte read each); fp32
+// uses the accumulator-compatible order of frag_row.
+template <bool BF16>
+__device__ __forceinline__ typename Mma<BF16>::frag h1_frag(const typename Mma<BF16>::elem* hrow, int kb, int c,
+                                                            int g) {
+  if constexpr (BF16)
+    return *reinterpret_cast<const bf16x8*>(hrow + 32 * kb + 16 * c + 8 * g);
+  else
+    return frag_row<false>(hrow + 32 * kb, c, g);
+}
+// A fragments of a stored tile: W2 rows (M = labels, K = hidden block kb) and
+// W2^T rows (M = hidden block hb, K = labels in the accumulator-compatible
+// order, to meet the probabilities taken from the logits' accumulators).
+// rbase / cbase: the lane's tw_row_base(n, g) / tw_col_base(lane).
+template <bool BF16>
+__device__ __forceinline__ typename Mma<BF16>::frag tile_frag_w(const typename Mma<BF16>::elem* wr, int rbase,
+                                                                int n, int kb, int c, int g) {
+  if constexpr (BF16)
+    return *reinterpret_cast<const bf16x8*>(wr + rbase + 32 * kb + 16 * c);
+  else
+    return frag_row<false>(wr + n * FwdShape<false>::WR + 32 * kb, c, g);
+}
+template <bool BF16>
+__device__ __forceinline__ typename Mma<BF16>::frag tile_frag_wt(const typename Mma<BF16>::elem* wr,
+                                                                 const typename Mma<BF16>::elem* wt, int cbase,
+                                                                 int hb, int c, int lane) {
+  if constexpr (BF16) {
+    const bf16* o = wr + cbase + 16 * c * TW_LD + 32 * hb;
+    const bf16x4 lo = lds_read_tr16(o), hi = lds_read_tr16(o + 8 * TW_LD);
+    bf16x8 f;
+    f[0] = lo[0]; f[1] = lo[1]; f[2] = lo[2]; f[3] = lo[3];
+    f[4] = hi[0]; f[5] = hi[1]; f[6] = hi[2]; f[7] = hi[3];
+    return f;
+  } else {
+    return frag_row<false>(wt + (32 * hb + (lane & 31)) * FwdShape<false>::WT, c, lane >> 5);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -149,12 +219,11 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
   using M = Mma<BF16>;
   using E = typename M::elem;
   using Fr = typename M::frag;
-  constexpr int WR = FwdShape<BF16>::WR, WT = FwdShape<BF16>::WT;
   constexpr int RB = FwdShape<BF16>::RB;
   constexpr int NCH = 32 / M::KC;
   static_assert(FwdShape<BF16>::NB == 1, "one 32-row block per wave");
-  __shared__ __attribute__((aligned(16))) E wr[FWD_NBUF][OUT_TILE * WR];
-  __shared__ __attribute__((aligned(16))) E wt[FWD_NBUF][HID * WT];
+  __shared__ __attribute__((aligned(16))) E wr[FWD_NBUF][tile_elems<BF16>()];
+  __shared__ __attribute__((aligned(16))) E wt[FWD_NBUF][tileT_elems<BF16>()];
   __shared__ __attribute__((aligned(16))) float bt[FWD_NBUF][OUT_TILE];
 
   const int lane = threadIdx.x & 63, g = lane >> 5, n = lane & 31;
@@ -167,6 +236,8 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
   // others and never written out, so the loop has no row-dependent branch.
   const int row0 = blockIdx.y * RB + wave * 32;
   const W2Src src = w2_src(W2, b2, L);
+  const int rbase = tw_row_base(n, g);
+  const int cbase = tw_col_base(lane);
 
   // H1^T as the B operand (K = hidden, N = rows), resident for the whole split.
   Fr hf[4][NCH];
@@ -174,7 +245,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) hf[kb][c] = frag_row<BF16>(hrow + 32 * kb, c, g);
+    for (int c = 0; c < NCH; ++c) hf[kb][c] = h1_frag<BF16>(hrow, kb, c, g);
   // Redefine the fragments once they have arrived (empty asm), so the loop below
   // never waits on these loads again and its wait counters track only the W2
   // prefetch.
@@ -193,11 +264,10 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
       const float4 b = bq[2 * q + g];
       z[4 * q + 0] = b.x; z[4 * q + 1] = b.y; z[4 * q + 2] = b.z; z[4 * q + 3] = b.w;
     }
-    const E* wrb = wr[buf] + n * WR;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) z = M::mma(frag_row<BF16>(wrb + 32 * kb, c, g), hf[kb][c], z);
+      for (int c = 0; c < NCH; ++c) z = M::mma(tile_frag_w<BF16>(wr[buf], rbase, n, kb, c, g), hf[kb][c], z);
     return z;
   };
 
@@ -208,19 +278,21 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc_o[hb][r] = 0.0f;
 
-  // Software pipeline over a ring of three LDS tiles.  In the iteration of
-  // tile t: the logits of tile t+1 go to the matrix cores while the softmax
-  // numerators of tile t are formed; then O^T += W2_t^T P_t^T while tile t+2
-  // (loaded into registers one iteration earlier) is converted into the ring
-  // and tile t+3 is loaded.  Tile indices are clamped to the split's last
-  // tile, so every load, store and product is unconditional (a clamped copy is
-  // never consumed).  Every split has at least one tile.
-  TileRegs tr;
-  tile_load(src, t_begin, tr);
-  tile_store<BF16, true>(tr, L, t_begin, wr[0], wt[0], bt[0]);
-  tile_load(src, min(t_begin + 1, t_last), tr);
-  tile_store<BF16, true>(tr, L, min(t_begin + 1, t_last), wr[1], wt[1], bt[1]);
-  tile_load(src, min(t_begin + 2, t_last), tr);
+  // Software pipeline over a ring of three LDS tiles and two register tiles.
+  // In the iteration of tile t: the logits of tile t+1 go to the matrix cores
+  // while the softmax numerators of tile t are formed; then O^T += W2_t^T P_t^T
+  // while tile t+2 (loaded into registers two iterations earlier) is converted
+  // into the ring and tile t+4 is loaded in its place.  Tile indices are
+  // clamped to the split's last tile, so every load, store and product is
+  // unconditional (a clamped copy is never consumed).  Every split has at
+  // least one tile.
+  TileRegs tr0, tr1;
+  tile_load(src, t_begin, tr0);
+  tile_store<BF16, true>(tr0, L, t_begin, wr[0], wt[0], bt[0]);
+  tile_load(src, min(t_begin + 1, t_last), tr1);
+  tile_store<BF16, true>(tr1, L, min(t_begin + 1, t_last), wr[1], wt[1], bt[1]);
+  tile_load(src, min(t_begin + 2, t_last), tr0);
+  tile_load(src, min(t_begin + 3, t_last), tr1);
   __syncthreads();
   f32x16 z = z_tile(0);
 
@@ -230,7 +302,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
   // reference, so the result is exact up to rounding.
   constexpr float LAZY = 8.0f;
   int b0 = 0;
-  for (int t = t_begin; t < t_end; ++t) {
+  auto iteration = [&](int t, TileRegs& tr) {
     const int b1 = b0 == FWD_NBUF - 1 ? 0 : b0 + 1;
     const int b2i = b1 == FWD_NBUF - 1 ? 0 : b1 + 1;
     // Operands of this iteration's two products, read from LDS first so that
@@ -241,13 +313,11 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
     // as holding them all would not fit the register file.)
     constexpr int PRE = BF16 ? NCH : 1;
     Fr za[4][PRE], oa[4][PRE];
-    const E* wrb = wr[b1] + n * WR;
-    const E* wtb = wt[b0];
     if constexpr (BF16) {
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) za[kb][c] = frag_row<BF16>(wrb + 32 * kb, c, g);
+        for (int c = 0; c < NCH; ++c) za[kb][c] = tile_frag_w<BF16>(wr[b1], rbase, n, kb, c, g);
     }
     f32x16 zn;
     {
@@ -262,7 +332,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
 #pragma unroll
       for (int hb = 0; hb < 4; ++hb)
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) oa[hb][c] = frag_row<BF16>(wtb + (32 * hb + n) * WT, c, g);
+        for (int c = 0; c < NCH; ++c) oa[hb][c] = tile_frag_wt<BF16>(wr[b0], wt[b0], cbase, hb, c, lane);
     }
 
     // running maximum of this tile (rows are lanes: one max per lane pair)
@@ -286,7 +356,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
       for (int c = 0; c < NCH; ++c)
-        zn = M::mma(BF16 ? za[kb][c % PRE] : frag_row<BF16>(wrb + 32 * kb, c, g), hf[kb][c], zn);
+        zn = M::mma(BF16 ? za[kb][c % PRE] : tile_frag_w<BF16>(wr[b1], rbase, n, kb, c, g), hf[kb][c], zn);
     // ... while this tile's numerators are formed (vector units)
     float p[16];
     float ps = 0.0f;
@@ -304,13 +374,18 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
     for (int hb = 0; hb < 4; ++hb)
 #pragma unroll
       for (int c = 0; c < NCH; ++c)
-        acc_o[hb] = M::mma(BF16 ? oa[hb][c % PRE] : frag_row<BF16>(wtb + (32 * hb + n) * WT, c, g),
+        acc_o[hb] = M::mma(BF16 ? oa[hb][c % PRE] : tile_frag_wt<BF16>(wr[b0], wt[b0], cbase, hb, c, lane),
                            pf[c], acc_o[hb]);
     tile_store<BF16, true>(tr, L, min(t + 2, t_last), wr[b2i], wt[b2i], bt[b2i]);
-    tile_load(src, min(t + 3, t_last), tr);
+    tile_load(src, min(t + 4, t_last), tr);
     __syncthreads();
     z = zn;
     b0 = b1;
+  };
+  for (int t = t_begin; t < t_end; t += 2) {
+    iteration(t, tr0);
+    if (t + 1 >= t_end) break;
+    iteration(t + 1, tr1);
   }
 
   const int row = row0 + n;
@@ -523,11 +598,11 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_topk(
   using M = Mma<BF16>;
   using E = typename M::elem;
   using Fr = typename M::frag;
-  constexpr int NB = FwdShape<BF16>::NB, WR = FwdShape<BF16>::WR;
+  constexpr int NB = FwdShape<BF16>::NB;
   constexpr int RB = FwdShape<BF16>::RB;
   constexpr int NCH = 32 / M::KC;
   constexpr int WROWS = 32 * NB;
-  __shared__ __attribute__((aligned(16))) E wr[2][OUT_TILE * WR];
+  __shared__ __attribute__((aligned(16))) E wr[2][tile_elems<BF16>()];
   __shared__ float bt[2][OUT_TILE];
   __shared__ float ls[FwdShape<BF16>::WAVES][WROWS][TOPK_MAX];
   __shared__ int li[FwdShape<BF16>::WAVES][WROWS][TOPK_MAX];
@@ -539,6 +614,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_topk(
   const int row0 = blockIdx.y * RB + wave * WROWS;
   const bool active = row0 < B;
   const W2Src src = w2_src(W2, b2, L);
+  const int rbase = tw_row_base(n, g);
 
   for (int e = lane; e < WROWS * TOPK_MAX; e += 64) {
     ls[wave][e / TOPK_MAX][e % TOPK_MAX] = -INFINITY;
@@ -551,7 +627,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_topk(
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) hf[nb][kb][c] = frag_row<BF16>(hrow + 32 * kb, c, g);
+      for (int c = 0; c < NCH; ++c) hf[nb][kb][c] = h1_frag<BF16>(hrow, kb, c, g);
   }
   TileRegs tr;
   if (t_begin < t_end) {
@@ -564,7 +640,6 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_topk(
     const bool has_next = t + 1 < t_end;
     if (has_next) tile_load(src, t + 1, tr);
     if (active) {
-      const E* wrb = wr[buf];
       f32x16 z[NB];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
@@ -574,7 +649,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_topk(
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
-          const Fr a = frag_row<BF16>(wrb + n * WR + 32 * kb, c, g);
+          const Fr a = tile_frag_w<BF16>(wr[buf], rbase, n, kb, c, g);
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) z[nb] = M::mma(a, hf[nb][kb][c], z[nb]);
         }

@@ -183,7 +183,7 @@ hipError_t launch_sort(const int32_t* keys_in, int n, int key_bits, int32_t* key
 // of the pairs inside a block is not fixed; the backward only ORs them into a
 // bit mask, whose value does not depend on it.
 // ---------------------------------------------------------------------------
-constexpr int LB_THREADS = 1024;
+constexpr int LB_THREADS = 256;  // one wave per SIMD: fits beside the output-layer forward
 constexpr int LB_LDS_MAX = 32768;  // blocks whose counters fit in LDS (128 KB)
 
 template <bool LDS>
