@@ -305,7 +305,7 @@ enum {
   ASGD_K_OUT_COMBINE = 3, /* per-row merge of label splits, loss, dA1 */
   ASGD_K_HIDDEN = 4,      /* b1 gradient / update and mean loss */
   ASGD_K_OUT_BWD = 5,     /* output-layer backward + W2/b2 update */
-  ASGD_K_W1_UPDATE = 6,   /* sparse W1 gradient + update */
+  ASGD_K_W1_UPDATE = 6,   /* sparse W1 gradient + update (internal stream) */
   ASGD_K_MERGE = 7,       /* normalized merge (timed on the global model) */
   ASGD_K_LABELS = 8,      /* (label, row) pairs grouped by label block (internal stream) */
   ASGD_K_COUNT = 9

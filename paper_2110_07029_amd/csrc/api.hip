@@ -39,7 +39,10 @@ asgd_status fail_hip(hipError_t e, const char* what) {
 
 constexpr int64_t kAlign = 64;  // floats
 constexpr int kMaxBatch = 2048;
-constexpr int kFwdWgs = 256;    // forward workgroups per launch (one per CU)
+// The output-layer forward runs one persistent workgroup per CU except
+// kAuxCus, which stay free for the label grouping and the sort on the internal
+// stream.
+constexpr int kAuxCus = 16;
 
 int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 
@@ -67,7 +70,7 @@ struct asgd_model {
   int n_cu = 256;
   // internal stream: the label grouping and the feature sort overlap the output layer
   hipStream_t aux = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_labels = nullptr, ev_join = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_labels = nullptr, ev_dA1 = nullptr, ev_join = nullptr;
   hipEvent_t ev = nullptr;
 
   // parameters
@@ -137,10 +140,10 @@ int64_t layout_workspace(asgd_model* m, char* base) {
   const int64_t n_lblocks = (m->L + 31) / 32;
   const int nrb = rp / RB;
   const int n_tiles = (m->L + OUT_TILE - 1) / OUT_TILE;
-  // (split, row) pairs: splits <= min(n_tiles, ceil(kFwdWgs / nRB)) for every nRB <= nrb
+  // (split, row) pairs: splits <= min(n_tiles, ceil(n_cu / nRB)) for every nRB <= nrb
   int64_t part_rows = 0;
   for (int r = 1; r <= nrb; ++r) {
-    int s = std::min(n_tiles, (kFwdWgs + r - 1) / r);
+    int s = std::min(n_tiles, (m->n_cu + r - 1) / r);
     part_rows = std::max<int64_t>(part_rows, (int64_t)s * r * RB);
   }
   int64_t tk_rows = 0;
@@ -219,7 +222,8 @@ int fwd_splits(asgd_model* m, int B) {
   const int RB = out_rows_per_block(m->bf16);
   const int nrb = (B + RB - 1) / RB;
   const int n_tiles = (m->L + OUT_TILE - 1) / OUT_TILE;
-  return std::max(1, std::min(n_tiles, (kFwdWgs + nrb - 1) / nrb));
+  const int wgs = std::max(1, m->n_cu - kAuxCus);
+  return std::max(1, std::min(n_tiles, (wgs + nrb - 1) / nrb));
 }
 
 // Start event of the next timed launch of group k (nullptr when not timing).
@@ -362,6 +366,7 @@ asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t s
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_fork, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_labels, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_dA1, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_join, hipEventDisableTiming);
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&m->aux, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipMalloc((void**)&m->params, m->n_pad * sizeof(float));
@@ -403,6 +408,7 @@ asgd_status asgd_model_free(asgd_model* m) {
   if (m->ev) (void)hipEventDestroy(m->ev);
   if (m->ev_fork) (void)hipEventDestroy(m->ev_fork);
   if (m->ev_labels) (void)hipEventDestroy(m->ev_labels);
+  if (m->ev_dA1) (void)hipEventDestroy(m->ev_dA1);
   if (m->ev_join) (void)hipEventDestroy(m->ev_join);
   if (m->aux) (void)hipStreamDestroy(m->aux);
   for (auto& v : m->tev)
@@ -490,7 +496,9 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   if (s) return s;
   // The label grouping and the feature sort depend only on what the gather
   // wrote: they run on the internal stream, overlapped with the output-layer
-  // forward; the backward waits for the label groups, the W1 update for the sort.
+  // forward.  The W1 update follows them there once dA1 exists, overlapped with
+  // the output-layer backward (the two touch disjoint data); the step ends when
+  // both streams have finished.
   const int32_t *sk = nullptr, *sv = nullptr;
   HIP_TRY(hipEventRecord(m->ev_fork, m->stream));
   HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_fork, 0));
@@ -499,16 +507,19 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   HIP_TRY(hipEventRecord(m->ev_labels, m->aux));
   s = run_sort(m, m->aux, x->nnz, &sk, &sv);
   if (s) return s;
-  HIP_TRY(hipEventRecord(m->ev_join, m->aux));
   s = run_forward(m, x, y, rows_pad);
   if (s) return s;
   TIMED(m, ASGD_K_HIDDEN, launch_hidden_bias(B, m->dA1, m->b1(), lr, m->loss_rows, m->loss, m->stream));
+  HIP_TRY(hipEventRecord(m->ev_dA1, m->stream));
+  HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_dA1, 0));
+  CsrDev xd = dev(x);
+  TIMED_ON(m, ASGD_K_W1_UPDATE, m->aux,
+           launch_w1_update(m->W1(), m->F, sk, sv, x->nnz, m->row_of, xd, m->dA1, lr, m->aux));
+  HIP_TRY(hipEventRecord(m->ev_join, m->aux));
   HIP_TRY(hipStreamWaitEvent(m->stream, m->ev_labels, 0));
   TIMED(m, ASGD_K_OUT_BWD, launch_out_bwd(m->bf16, m->W2(), m->b2(), m->L, m->H1, m->H1T, m->rows_pad_max, B,
                          m->lse, m->rw, m->lbeg, m->lpair, lr, m->n_cu, m->stream));
   HIP_TRY(hipStreamWaitEvent(m->stream, m->ev_join, 0));
-  CsrDev xd = dev(x);
-  TIMED(m, ASGD_K_W1_UPDATE, launch_w1_update(m->W1(), m->F, sk, sv, x->nnz, m->row_of, xd, m->dA1, lr, m->stream));
   if (loss_out) return asgd_model_last_loss(m, loss_out);
   return ASGD_OK;
 }

@@ -5,8 +5,10 @@
 // tile can find its true labels with a binary search.
 //
 // One pass over a digit of up to 11 bits = three launches:
-//   hist    : per-workgroup digit counts of a 1024-key chunk (LDS counters)
-//   scan    : exclusive scan over (digit, workgroup) -> global scatter offsets
+//   hist    : per-workgroup digit counts of a 1024-key chunk (LDS counters),
+//             stored block-major: hist[block][digit]
+//   scan    : exclusive scan over (digit, workgroup) -> global scatter offsets,
+//             every read and write coalesced across the digits
 //   scatter : stable ranks inside the chunk from 64-lane ballots (lanes with the
 //             same digit in one wave), per-wave running counts, then a prefix
 //             over the four waves; keys land at offset + rank.
@@ -35,12 +37,13 @@ __global__ __launch_bounds__(SORT_THREADS) void k_sort_hist(const int32_t* __res
     if (p < n) atomicAdd(&cnt[(keys[p] >> shift) & (nd - 1)], 1);
   }
   __syncthreads();
-  for (int d = threadIdx.x; d < nd; d += SORT_THREADS) hist[d * nblk + blockIdx.x] = cnt[d];
+  for (int d = threadIdx.x; d < nd; d += SORT_THREADS) hist[blockIdx.x * nd + d] = cnt[d];
 }
 
-// Scatter offsets offs[d * nblk + b] = (keys with a smaller digit) + (keys with
-// digit d in earlier chunks), by one workgroup: thread t owns digits 2t, 2t+1
-// and their nblk chunk counts; one block-wide exclusive scan of the per-thread
+// Scatter offsets offs[b * ndig + d] = (keys with a smaller digit) + (keys with
+// digit d in earlier chunks), by one workgroup: thread t owns digits t and
+// t + SCAN_THREADS; per chunk b, the threads read consecutive digits (one
+// coalesced row of hist), and one block-wide exclusive scan of the per-digit
 // totals gives every digit's base.
 constexpr int SCAN_THREADS = 1024;
 constexpr int SCAN_DPT = (1 << SORT_MAX_BITS) / SCAN_THREADS;  // digits per thread
@@ -50,42 +53,55 @@ __global__ __launch_bounds__(SCAN_THREADS) void k_sort_scan(const int32_t* __res
                                                             int32_t* __restrict__ offs) {
   __shared__ int wsum[SCAN_THREADS / 64];
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  int local = 0;
+  int tot[SCAN_DPT];
 #pragma unroll
-  for (int k = 0; k < SCAN_DPT; ++k) {
-    const int d = SCAN_DPT * t + k;
-    if (d < ndig)
-      for (int b = 0; b < nblk; ++b) local += hist[d * nblk + b];
-  }
-  int x = local;
+  for (int k = 0; k < SCAN_DPT; ++k) tot[k] = 0;
+#pragma unroll 8
+  for (int b = 0; b < nblk; ++b)
 #pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) wsum[w] = x;
-  __syncthreads();
-  if (w == 0) {
-    int s = lane < SCAN_THREADS / 64 ? wsum[lane] : 0;
-#pragma unroll
-    for (int o = 1; o < SCAN_THREADS / 64; o <<= 1) {
-      const int y = __shfl_up(s, o);
-      if (lane >= o) s += y;
+    for (int k = 0; k < SCAN_DPT; ++k) {
+      const int d = t + k * SCAN_THREADS;
+      if (d < ndig) tot[k] += hist[(size_t)b * ndig + d];
     }
-    if (lane < SCAN_THREADS / 64) wsum[lane] = s;
-  }
-  __syncthreads();
-  int run = (w > 0 ? wsum[w - 1] : 0) + x - local;
+  // digits in order d = t + k * SCAN_THREADS: scan the block once per k
+  int carry = 0;
 #pragma unroll
   for (int k = 0; k < SCAN_DPT; ++k) {
-    const int d = SCAN_DPT * t + k;
-    if (d < ndig)
-      for (int b = 0; b < nblk; ++b) {
-        const int c = hist[d * nblk + b];
-        offs[d * nblk + b] = run;
-        run += c;
+    int x = tot[k];
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) wsum[w] = x;
+    __syncthreads();
+    if (w == 0) {
+      int v = lane < SCAN_THREADS / 64 ? wsum[lane] : 0;
+#pragma unroll
+      for (int o = 1; o < SCAN_THREADS / 64; o <<= 1) {
+        const int y = __shfl_up(v, o);
+        if (lane >= o) v += y;
       }
+      if (lane < SCAN_THREADS / 64) wsum[lane] = v;
+    }
+    __syncthreads();
+    const int base = carry + (w > 0 ? wsum[w - 1] : 0) + x - tot[k];
+    carry += wsum[SCAN_THREADS / 64 - 1];
+    __syncthreads();
+    tot[k] = base;  // becomes the running offset of digit t + k * SCAN_THREADS
   }
+#pragma unroll 8
+  for (int b = 0; b < nblk; ++b)
+#pragma unroll
+    for (int k = 0; k < SCAN_DPT; ++k) {
+      const int d = t + k * SCAN_THREADS;
+      if (d < ndig) {
+        const size_t i = (size_t)b * ndig + d;
+        const int c = hist[i];
+        offs[i] = tot[k];
+        tot[k] += c;
+      }
+    }
 }
 
 __global__ __launch_bounds__(SORT_THREADS) void k_sort_scatter(
@@ -135,7 +151,7 @@ __global__ __launch_bounds__(SORT_THREADS) void k_sort_scatter(
     const int p = p0 + it * 64 + lane;
     if (p < n) {
       const int d = (key[it] >> shift) & (nd - 1);
-      const int pos = offs[d * nblk + blockIdx.x] + wcnt[w][d] + rank[it];
+      const int pos = offs[blockIdx.x * nd + d] + wcnt[w][d] + rank[it];
       keys_out[pos] = key[it];
       vals_out[pos] = val[it];
     }
