@@ -30,6 +30,34 @@ MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}
 H = 128
 OVERLAPPED = ("sort", "labels", "w1_update")  # kernels on the library's second stream
 
+# HBM traffic of a kernel from `rocprofv3 --pmc FETCH_SIZE` and `--pmc WRITE_SIZE` runs of this bench
+# (KiB per dispatch, averaged; profiles/wide_label_hbm_counters.md), scaled by what the same counters
+# read for a plain device copy of 256 MiB: fetched bytes = 2.0 x FETCH_SIZE, written = 1.0 x WRITE_SIZE.
+# A figure holds only for the kernel sources it was measured on (their sha256); otherwise it is null.
+FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
+PMC_TRAFFIC = {
+    ("wide-label", 256, "out_bwd"): dict(
+        sources=("csrc/k_out_bwd.hip", "csrc/asgd_dev.h", "csrc/asgd_kernels.h"),
+        sha256="a1f8a4345dce6da0593333bb60c2b8ba81008d998c6505b57487a7d732f7b7d5",
+        fetch_kib=170315.7, write_kib=374700.7),
+}
+
+
+def measured_traffic(workload: str, batch: int, kernel: str):
+    """HBM bytes per launch from the counters, or None if none were taken on these sources."""
+    import hashlib
+    rec = PMC_TRAFFIC.get((workload, batch, kernel))
+    if rec is None:
+        return None
+    pkg = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2110_07029_amd")
+    h = hashlib.sha256()
+    for rel in rec["sources"]:
+        with open(os.path.join(pkg, rel), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != rec["sha256"]:
+        return None
+    return (rec["fetch_kib"] * FETCH_SCALE + rec["write_kib"] * WRITE_SCALE) * 1024.0
+
 
 def log(msg: str):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
@@ -50,7 +78,7 @@ def parse():
     return ap.parse_args()
 
 
-def kernel_model(w, B, nnz, lnnz, uniq):
+def kernel_model(w, B, nnz, lnnz, uniq, splits):
     """Algorithmic bytes and flops of one launch of each kernel group."""
     F, L = w.n_features, w.n_labels
     op = 2 if w.gemm_bf16 else 4
@@ -63,7 +91,8 @@ def kernel_model(w, B, nnz, lnnz, uniq):
         "labels": dict(bytes=lnnz * 12 + (L // 32 + 1) * 4, flops=0.0),
         # reads W2 and b2 once; Z = H1 W2^T and O = P W2 (the dense part of dH1)
         "out_fwd": dict(bytes=4.0 * L * (H + 1), flops=4.0 * B * H * L),
-        "out_combine": dict(bytes=B * H * 4 * 2 + lnnz * H * 4, flops=2.0 * lnnz * H),
+        # reads the forward's per-(split, row) partials (max, sum, O), A1 and the target rows of W2
+        "out_combine": dict(bytes=splits * B * (H + 2) * 4 + B * H * 4 * 2 + lnnz * H * 4, flops=2.0 * lnnz * H),
         "hidden": dict(bytes=B * H * 4, flops=B * H),
         # reads and writes W2 and b2 once; dW2 = dZ^T H1 (the Z recompute is not counted)
         "out_bwd": dict(bytes=8.0 * L * (H + 1), flops=2.0 * B * H * L),
@@ -281,7 +310,10 @@ def main():
     mean_lnnz = float(np.mean([lnnz[j] for j in used]))
     uniq = float(np.mean([len(np.unique(ds.x.indices[ipx[bounds[j][0]]:ipx[bounds[j][1]]]))
                           for j in used[:32]]))
-    model = kernel_model(w, B, mean_nnz, mean_lnnz, uniq)
+    # label splits of the forward: one persistent workgroup per CU but 16, shared by the 256-row blocks
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    splits = min((w.n_labels + 31) // 32, -(-(n_cu - 16) // -(-B // 256)))
+    model = kernel_model(w, B, mean_nnz, mean_lnnz, uniq, splits)
     dtype = "bf16" if w.gemm_bf16 else "fp32"
     kernels = {}
     for name, (tot, n) in kt.items():
@@ -304,8 +336,12 @@ def main():
         # the merge of the elastic configuration: 4 replicas of this model
         kernels["merge"] = measure_merge(w, 4, 10, stream)
     d = kernels[dom]
+    traffic = measured_traffic(w.name, B, dom)
     roofline = {"kernel": dom, "bound": "hbm", "achieved": d["GB/s"], "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": d["hbm_frac"], "traffic": None}
+                "unit": "GB/s", "frac": d["hbm_frac"],
+                "traffic": None if traffic is None else round(traffic / 1e9, 4)}
+    if traffic is not None:
+        roofline["traffic_unit"] = "GB per launch"
     cpu = None
     if args.cpu_seconds > 0:
         log(f"oracle CPU baseline, ~{args.cpu_seconds:.0f} s budget")
