@@ -100,6 +100,41 @@ __device__ __forceinline__ typename Mma<BF16>::frag frag_acc(const float* v, int
     return v[c];
 }
 
+// Word 3 of a raw (unformatted, 32-bit) buffer resource on the gfx9 family; with
+// stride 0 a load at or past num_records bytes returns zeros.
+constexpr int BUF_RSRC_WORD3 = 0x00020000;
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ---- W2 tile in LDS, bf16 (output-layer forward and backward) ---------------
+// [32 labels x 128 hidden], row stride 160 elements, 16-byte chunks XOR-permuted
+// by bits 2-3 of the row:
+//   (label, h) -> label * 160 + 8 * ((h / 8) ^ ((label / 4) % 4)) + h % 8.
+// gfx950's LDS serves 16-byte reads 16 lanes at a time and transposed 8-byte
+// reads 32 lanes at a time over 64 banks; this layout keeps both reads of the
+// tile (and its 8-byte stores) free of bank conflicts, and the permutation
+// touches only the two low chunk bits, so a fragment's address is one of two
+// per-lane bases plus a compile-time offset.
+constexpr int TW_LD = 160;
+
+__device__ __forceinline__ int tw_off(int row, int col) {
+  return row * TW_LD + 8 * ((col >> 3) ^ ((row >> 2) & 3)) + (col & 7);
+}
+// Row fragments of label row n for lane group g: hidden units 32kb + 16c + 8g
+// .. + 7 are at tw_row_base(n, g, c) + 32kb.
+__device__ __forceinline__ int tw_row_base(int n, int g, int c) {
+  return n * TW_LD + 8 * ((2 * c + g) ^ ((n >> 2) & 3));
+}
+// Transposed reads: result lane (n, g) receives hidden unit 32hb + n at labels
+// 16c + 8hi + 4g + 0..3 from tw_col_base(lane, hi) + 16c * TW_LD + 32hb.  Source
+// lane (G, i, a) = (lane / 16, lane / 4 % 4, lane % 4) addresses label
+// 8hi + 4(G / 2) + i, hidden units 16(G % 2) + 4a .. + 3 (relative).
+__device__ __forceinline__ int tw_col_base(int lane, int hi) {
+  const int G = lane >> 4, i = (lane >> 2) & 3, a = lane & 3;
+  return (8 * hi + 4 * (G >> 1) + i) * TW_LD + 8 * ((2 * (G & 1) + (a >> 1)) ^ ((2 * hi + (G >> 1)) & 3)) +
+         4 * (a & 1);
+}
+
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 // ds_read_b64_tr_b16: a 64-bit LDS read whose 4 x 16-bit results are

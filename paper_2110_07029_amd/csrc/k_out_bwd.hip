@@ -10,9 +10,11 @@
 // lane itself loaded (the accumulator-compatible K order makes the lane that
 // loads a weight the lane that owns its gradient).
 //
-// Workgroups are persistent, 8 wavefronts (2 per SIMD).  H1 is read by every
-// label block, so with bf16 operands it is staged in LDS in both layouts
-// (padded rows: conflict-free 8-byte fragment reads):
+// Workgroups are persistent, 8 wavefronts (2 per SIMD).  With bf16 operands
+// H1 is staged in LDS once, in the conflict-free tile layout of the forward
+// (row stride 160, 16-byte chunks permuted by the row): the logits read H1
+// rows with 16-byte reads, the dW2 product reads H1^T with transposed reads
+// (ds_read_b64_tr_b16) from the same copy.
 //   staged  (B <= 256): the whole batch once per workgroup; each wave then
 //           walks its own sequence of label blocks with no barrier inside
 //           the loop, so loads of one wave overlap the matrix work of another;
@@ -30,30 +32,17 @@ namespace asgd {
 constexpr int BWD_WAVES = 8;
 constexpr int BWD_THREADS = 64 * BWD_WAVES;
 constexpr int BWD_CHUNK = 256;  // rows staged in LDS at a time
-// LDS row strides of 66 and 130 dwords (2 mod 4, odd half): the 8-byte fragment
-// reads of 16 consecutive lanes cover all 32 banks.
-constexpr int H1S_LD = HID + 4;        // row-major H1 in LDS (elements)
-constexpr int H1TS_LD = BWD_CHUNK + 4; // transposed H1 in LDS (elements)
 
 enum BwdMode { BWD_GLOBAL = 0, BWD_STAGED = 1, BWD_CHUNKED = 2 };
 
-// Copy rows [r0, r0 + nrows) of H1 (row-major, ld HID) and the same columns of
-// H1^T (ld ld_t) into LDS; nrows is a multiple of 32 and inside the padded
-// batch (rows past B are zero in both copies).
-__device__ __forceinline__ void stage_h1(bf16* h1s, bf16* h1ts, const bf16* __restrict__ H1,
-                                         const bf16* __restrict__ H1T, int ld_t, int r0, int nrows) {
+// Copy rows [r0, r0 + nrows) of H1 (row-major, ld HID) into the LDS tile (row
+// r of the chunk at tw_off(r, .)); nrows is a multiple of 32 and inside the
+// padded batch (rows past B are zero).  16 lanes store one row: conflict-free.
+__device__ __forceinline__ void stage_h1(bf16* h1s, const bf16* __restrict__ H1, int r0, int nrows) {
   for (int e = threadIdx.x; e < nrows * 16; e += BWD_THREADS) {
     const int r = e >> 4, c = e & 15;
     const uint4 v = *reinterpret_cast<const uint4*>(H1 + (size_t)(r0 + r) * HID + c * 8);
-    *reinterpret_cast<uint2*>(h1s + r * H1S_LD + c * 8) = make_uint2(v.x, v.y);
-    *reinterpret_cast<uint2*>(h1s + r * H1S_LD + c * 8 + 4) = make_uint2(v.z, v.w);
-  }
-  const int cpr = nrows >> 3;
-  for (int e = threadIdx.x; e < HID * cpr; e += BWD_THREADS) {
-    const int h = e / cpr, c = e - h * cpr;
-    const uint4 v = *reinterpret_cast<const uint4*>(H1T + (size_t)h * ld_t + r0 + c * 8);
-    *reinterpret_cast<uint2*>(h1ts + h * H1TS_LD + c * 8) = make_uint2(v.x, v.y);
-    *reinterpret_cast<uint2*>(h1ts + h * H1TS_LD + c * 8 + 4) = make_uint2(v.z, v.w);
+    *reinterpret_cast<uint4*>(h1s + r * TW_LD + 8 * (c ^ ((r >> 2) & 3))) = v;
   }
 }
 
@@ -80,12 +69,9 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
 
   char* sp = smem_raw;
   E* h1s = nullptr;
-  E* h1ts = nullptr;
   if constexpr (LDS_H1) {
     h1s = reinterpret_cast<E*>(sp);
-    sp += BWD_CHUNK * H1S_LD * sizeof(E);
-    h1ts = reinterpret_cast<E*>(sp);
-    sp += HID * H1TS_LD * sizeof(E);
+    sp += BWD_CHUNK * TW_LD * sizeof(E);
   }
   // per row: crow = log2(1/B) - lse*log2(e) (-inf for rows past B) so that
   // dZ = 2^(z*log2(e) + bias*log2(e) + crow) = softmax/B; tw = (1/|Y_i|)/B
@@ -118,17 +104,18 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
   };
 
   if constexpr (MODE == BWD_STAGED) {
-    stage_h1(h1s, h1ts, H1, H1T, ld_t, 0, bpad);
+    if constexpr (LDS_H1) stage_h1(h1s, H1, 0, bpad);
     stage_rows(0, bpad);
     __syncthreads();
   } else if constexpr (MODE == BWD_GLOBAL) {
     stage_rows(0, bpad);
     __syncthreads();
   }
-  const E* h1 = LDS_H1 ? h1s : H1;
-  const int ldh = LDS_H1 ? H1S_LD : HID;
-  const E* h1t = LDS_H1 ? h1ts : H1T;
-  const int ldht = LDS_H1 ? H1TS_LD : ld_t;
+  // the lane's bases in the LDS tile: H1 row fragments (rows 32 rb + n) and
+  // transposed H1^T fragments (hidden 32 hb + n); every offset below is rb, kb,
+  // hb, c or hi times a constant
+  const int rbase[2] = {tw_row_base(n, g, 0), tw_row_base(n, g, 1)};
+  const int cbase[2] = {tw_col_base(lane, 0), tw_col_base(lane, 1)};
 
   const int n_blocks = (L + 31) >> 5;
   // staged / global: each wave walks its own blocks; chunked: the workgroup
@@ -153,17 +140,27 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
         wreg[kb][q] = *reinterpret_cast<const float4*>(wrow + 32 * kb + 8 * q + 4 * g);
     const float bias = b2[min(label, L - 1)];
     const float bb = lvalid ? bias * LOG2E : -INFINITY;
-    // operand fragments of W2 (K = hidden), converted once per block
+    // operand fragments of W2 (K = hidden), converted once per block.  bf16:
+    // the logits take 8 consecutive hidden units per lane (32kb + 16c + 8g ..
+    // + 7, matching the 16-byte H1 reads); the lane holds units 8q + 4g + 0..3,
+    // so the two lane halves trade one float4 per pair with v_permlane32_swap
+    // (its two results are exactly the pair's lo and hi halves on both halves).
     Fr wf[4][NCH];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
       for (int c = 0; c < NCH; ++c) {
         if constexpr (BF16) {
-          const float4 lo4 = wreg[kb][2 * c], hi4 = wreg[kb][2 * c + 1];
+          const float4 a4 = wreg[kb][2 * c], b4 = wreg[kb][2 * c + 1];
+          const float av[4] = {a4.x, a4.y, a4.z, a4.w}, bv[4] = {b4.x, b4.y, b4.z, b4.w};
           Fr f;
-          f[0] = (bf16)lo4.x; f[1] = (bf16)lo4.y; f[2] = (bf16)lo4.z; f[3] = (bf16)lo4.w;
-          f[4] = (bf16)hi4.x; f[5] = (bf16)hi4.y; f[6] = (bf16)hi4.z; f[7] = (bf16)hi4.w;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const auto sw = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, av[j]),
+                                                             __builtin_bit_cast(unsigned, bv[j]), false, false);
+            f[j] = (bf16)__builtin_bit_cast(float, sw[0]);
+            f[4 + j] = (bf16)__builtin_bit_cast(float, sw[1]);
+          }
           wf[kb][c] = f;
         } else {
           const float4 v = wreg[kb][c >> 2];
@@ -192,11 +189,20 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
       f32x16 z;
 #pragma unroll
       for (int r = 0; r < 16; ++r) z[r] = 0.0f;
-      const E* hrow = h1 + (size_t)((LDS_H1 ? rb * 32 : grow0) + n) * ldh;
+      if constexpr (LDS_H1) {
+        const E* t = h1s + rb * 32 * TW_LD;
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
+        for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) z = M::mma(frag_row<BF16>(hrow + 32 * kb, c, g), wf[kb][c], z);
+          for (int c = 0; c < NCH; ++c)
+            z = M::mma(*reinterpret_cast<const bf16x8*>(t + rbase[c] + 32 * kb), wf[kb][c], z);
+      } else {
+        const E* hrow = H1 + (size_t)(grow0 + n) * HID;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int c = 0; c < NCH; ++c) z = M::mma(frag_row<BF16>(hrow + 32 * kb, c, g), wf[kb][c], z);
+      }
       // rows 8*q + 4*g + (0..3) of this block: one float4 of row constants each
       float cr[16];
 #pragma unroll
@@ -225,9 +231,21 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
       for (int c = 0; c < NCH; ++c) df[c] = frag_acc<BF16>(dz, c);
 #pragma unroll
       for (int hb = 0; hb < 4; ++hb) {
-        const E* trow = h1t + (size_t)(32 * hb + n) * ldht + (LDS_H1 ? rb * 32 : grow0);
+        if constexpr (LDS_H1) {
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) accw[hb] = M::mma(frag_row<BF16>(trow, c, g), df[c], accw[hb]);
+          for (int c = 0; c < NCH; ++c) {
+            const E* o = h1s + (rb * 32 + 16 * c) * TW_LD + 32 * hb;
+            const bf16x4 lo4 = lds_read_tr16(o + cbase[0]), hi4 = lds_read_tr16(o + cbase[1]);
+            bf16x8 af;
+            af[0] = lo4[0]; af[1] = lo4[1]; af[2] = lo4[2]; af[3] = lo4[3];
+            af[4] = hi4[0]; af[5] = hi4[1]; af[6] = hi4[2]; af[7] = hi4[3];
+            accw[hb] = M::mma(af, df[c], accw[hb]);
+          }
+        } else {
+          const E* trow = H1T + (size_t)(32 * hb + n) * ld_t + grow0;
+#pragma unroll
+          for (int c = 0; c < NCH; ++c) accw[hb] = M::mma(frag_row<BF16>(trow, c, g), df[c], accw[hb]);
+        }
       }
     };
 
@@ -235,7 +253,7 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
       for (int c0 = 0; c0 < bpad; c0 += BWD_CHUNK) {
         const int crows = min(BWD_CHUNK, bpad - c0);
         __syncthreads();  // every wave is done with the previous chunk
-        stage_h1(h1s, h1ts, H1, H1T, ld_t, c0, crows);
+        if constexpr (LDS_H1) stage_h1(h1s, H1, c0, crows);
         stage_rows(c0, crows);
         if (has_targets) build_mask(lo, hi, c0, crows);
         __syncthreads();
@@ -295,7 +313,7 @@ hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, const void
   const int mode = !use_bf16 ? BWD_GLOBAL : (B <= BWD_CHUNK ? BWD_STAGED : BWD_CHUNKED);
   const int span = mode == BWD_CHUNKED ? BWD_CHUNK : nrb * 32;
   size_t shm = (size_t)2 * span * sizeof(float) + (size_t)BWD_WAVES * 32 * (span / 32) * sizeof(uint32_t);
-  if (mode != BWD_GLOBAL) shm += (size_t)BWD_CHUNK * H1S_LD * 2 + (size_t)HID * H1TS_LD * 2;
+  if (mode != BWD_GLOBAL) shm += (size_t)BWD_CHUNK * TW_LD * 2;
   const int n_blocks = (L + 31) / 32;
   int grid = (n_blocks + BWD_WAVES - 1) / BWD_WAVES;
   const int cap = mode == BWD_GLOBAL ? 2 * n_cu : n_cu;

@@ -55,7 +55,6 @@ struct W2Src {
   int voff_b;  // bytes: label slot t % 32
 };
 
-constexpr int BUF_RSRC_WORD3 = 0x00020000;  // raw (unformatted) 32-bit buffer, gfx9 family
 
 __device__ __forceinline__ W2Src w2_src(const float* W2, const float* b2, int L) {
   W2Src s;
@@ -68,7 +67,6 @@ __device__ __forceinline__ W2Src w2_src(const float* W2, const float* b2, int L)
 }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // max(v[l], v[l ^ 32]) on every lane, without a trip through LDS: the swap
 // exchanges the upper half of one copy with the lower half of the other, so
@@ -91,33 +89,6 @@ __device__ __forceinline__ void tile_load(const W2Src& src, int tile, TileRegs& 
   }
   r.bias = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(src.b, src.voff_b,
                                                                           tile * OUT_TILE * 4, 0));
-}
-
-// ---- W2 tile in LDS, bf16 ---------------------------------------------------
-// [32 labels x 128 hidden], row stride 144 elements (consecutive rows 8 banks
-// apart), 16-byte chunks XOR-permuted by bit 2 of the row:
-//   (label, h) -> label * 144 + 8 * ((h / 8) ^ ((label / 4) % 2)) + h % 8.
-// Three access patterns are free of bank conflicts: the row fragments of the
-// logits (lane = label, 8 consecutive hidden units: one 16-byte read), the
-// transposed reads of the W2^T operand (16 lanes over 4 labels x 4 chunks of 4
-// hidden units) and the tile stores (16 lanes over one label row).  Every
-// fragment address is a per-lane base plus a compile-time offset.
-constexpr int TW_LD = 144;
-
-__device__ __forceinline__ int tw_off(int row, int col) {
-  return row * TW_LD + 8 * ((col >> 3) ^ ((row >> 2) & 1)) + (col & 7);
-}
-// Base of the row fragments of label row n for lane group g: hidden units
-// k + 8g .. k + 8g + 7 are at base + k for k a multiple of 16.
-__device__ __forceinline__ int tw_row_base(int n, int g) { return n * TW_LD + 8 * (g ^ ((n >> 2) & 1)); }
-// Base of the transposed reads: lane (n, g) of the result receives hidden unit
-// m0 + n at labels k + 4g + 0..3 (lo, at base + k * TW_LD + m0) and
-// k + 8 + 4g + 0..3 (hi, 8 rows further), k and m0 multiples of 16.  Source
-// lane (G, i, a) = (lane / 16, lane / 4 % 4, lane % 4) addresses label
-// 4 (G / 2) + i, hidden units 16 (G % 2) + 4a .. + 3.
-__device__ __forceinline__ int tw_col_base(int lane) {
-  const int G = lane >> 4, i = (lane >> 2) & 3, a = lane & 3;
-  return (4 * (G >> 1) + i) * TW_LD + 8 * (2 * (G & 1) + ((a >> 1) ^ (G >> 1))) + 4 * (a & 1);
 }
 
 // Store a loaded tile into LDS as operands.  bf16: the layout above, which
@@ -180,22 +151,22 @@ __device__ __forceinline__ typename Mma<BF16>::frag h1_frag(const typename Mma<B
 // A fragments of a stored tile: W2 rows (M = labels, K = hidden block kb) and
 // W2^T rows (M = hidden block hb, K = labels in the accumulator-compatible
 // order, to meet the probabilities taken from the logits' accumulators).
-// rbase / cbase: the lane's tw_row_base(n, g) / tw_col_base(lane).
+// rb[c] = tw_row_base(n, g, c), cb[hi] = tw_col_base(lane, hi): the lane's bases.
 template <bool BF16>
-__device__ __forceinline__ typename Mma<BF16>::frag tile_frag_w(const typename Mma<BF16>::elem* wr, int rbase,
-                                                                int n, int kb, int c, int g) {
+__device__ __forceinline__ typename Mma<BF16>::frag tile_frag_w(const typename Mma<BF16>::elem* wr,
+                                                                const int (&rb)[2], int n, int kb, int c, int g) {
   if constexpr (BF16)
-    return *reinterpret_cast<const bf16x8*>(wr + rbase + 32 * kb + 16 * c);
+    return *reinterpret_cast<const bf16x8*>(wr + rb[c] + 32 * kb);
   else
     return frag_row<false>(wr + n * FwdShape<false>::WR + 32 * kb, c, g);
 }
 template <bool BF16>
 __device__ __forceinline__ typename Mma<BF16>::frag tile_frag_wt(const typename Mma<BF16>::elem* wr,
-                                                                 const typename Mma<BF16>::elem* wt, int cbase,
-                                                                 int hb, int c, int lane) {
+                                                                 const typename Mma<BF16>::elem* wt,
+                                                                 const int (&cb)[2], int hb, int c, int lane) {
   if constexpr (BF16) {
-    const bf16* o = wr + cbase + 16 * c * TW_LD + 32 * hb;
-    const bf16x4 lo = lds_read_tr16(o), hi = lds_read_tr16(o + 8 * TW_LD);
+    const bf16* o = wr + 16 * c * TW_LD + 32 * hb;
+    const bf16x4 lo = lds_read_tr16(o + cb[0]), hi = lds_read_tr16(o + cb[1]);
     bf16x8 f;
     f[0] = lo[0]; f[1] = lo[1]; f[2] = lo[2]; f[3] = lo[3];
     f[4] = hi[0]; f[5] = hi[1]; f[6] = hi[2]; f[7] = hi[3];
@@ -236,8 +207,8 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
   // others and never written out, so the loop has no row-dependent branch.
   const int row0 = blockIdx.y * RB + wave * 32;
   const W2Src src = w2_src(W2, b2, L);
-  const int rbase = tw_row_base(n, g);
-  const int cbase = tw_col_base(lane);
+  const int rbase[2] = {tw_row_base(n, g, 0), tw_row_base(n, g, 1)};
+  const int cbase[2] = {tw_col_base(lane, 0), tw_col_base(lane, 1)};
 
   // H1^T as the B operand (K = hidden, N = rows), resident for the whole split.
   Fr hf[4][NCH];
@@ -614,7 +585,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_topk(
   const int row0 = blockIdx.y * RB + wave * WROWS;
   const bool active = row0 < B;
   const W2Src src = w2_src(W2, b2, L);
-  const int rbase = tw_row_base(n, g);
+  const int rbase[2] = {tw_row_base(n, g, 0), tw_row_base(n, g, 1)};
 
   for (int e = lane; e < WROWS * TOPK_MAX; e += 64) {
     ls[wave][e / TOPK_MAX][e % TOPK_MAX] = -INFINITY;

@@ -9,7 +9,8 @@ import paper_2110_07029_amd as asgd
 from oracle import model as om
 from paper_2110_07029_amd import synth
 
-from gpu_util import (RTOL_BF16, RTOL_FP32, Setup, a1_bound, assert_rel_close, assert_update_close,
+from gpu_util import (RTOL_BF16, RTOL_EMU_ELEM, RTOL_EMU_NORM, RTOL_FP32, Setup, a1_bound, assert_rel_close,
+                      assert_update_close,
                       flush, read_params, step_magnitudes)
 
 pytestmark = pytest.mark.gpu
@@ -150,8 +151,10 @@ def test_step_parity_bf16(rows, B):
         xh, yh = s.host_batch(*rows)
         ref_emu, _, g, fw = om.train_step(before, xh, yh, 0.05, "bf16")
         mag = step_magnitudes(before, xh, yh, g, fw, 0.05)
-        assert_update_close("W2(bf16 operands)", before["W2"], after["W2"], ref_emu["W2"], 2e-3, mag["W2"])
-        assert_update_close("b2(bf16 operands)", before["b2"], after["b2"], ref_emu["b2"], 2e-3, mag["b2"])
+        assert_update_close("W2(bf16 operands)", before["W2"], after["W2"], ref_emu["W2"], RTOL_EMU_ELEM,
+                            mag["W2"], norm_rtol=RTOL_EMU_NORM)
+        assert_update_close("b2(bf16 operands)", before["b2"], after["b2"], ref_emu["b2"], RTOL_EMU_ELEM,
+                            mag["b2"], norm_rtol=RTOL_EMU_NORM)
     finally:
         s.free()
 
