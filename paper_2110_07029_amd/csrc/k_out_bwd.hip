@@ -286,6 +286,199 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Staged batches (B <= 256, bf16) with the next label block's W2 in flight:
+// 4 wavefronts, one per SIMD, each with the full register file.  A wave keeps
+// two blocks' fp32 W2 rows in registers with fixed roles (the block loop is
+// unrolled by two): while it works on one block the other set is loading the
+// block two steps ahead.  Inside a block the logits of row block rb+1 go to
+// the matrix cores while the exponentials of row block rb are formed.
+// ---------------------------------------------------------------------------
+constexpr int BWP_WAVES = 4;
+constexpr int BWP_THREADS = 64 * BWP_WAVES;
+
+__global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
+    float* __restrict__ W2, float* __restrict__ b2, int L, const bf16* __restrict__ H1, int B,
+    const float* __restrict__ lse, const float* __restrict__ rw, const int32_t* __restrict__ lbeg,
+    const int32_t* __restrict__ lpair, float lr, float invB, float log2_invB) {
+  using M = Mma<true>;
+  using Fr = M::frag;
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  const int nrb = (B + 31) >> 5;
+  const int bpad = nrb * 32;
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, n = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  char* sp = smem_raw;
+  bf16* h1s = reinterpret_cast<bf16*>(sp);
+  sp += BWD_CHUNK * TW_LD * sizeof(bf16);
+  float* crow_s = reinterpret_cast<float*>(sp);
+  sp += bpad * sizeof(float);
+  float* tw_s = reinterpret_cast<float*>(sp);
+  sp += bpad * sizeof(float);
+  uint32_t* mask = reinterpret_cast<uint32_t*>(sp) + wave * 32 * nrb;
+
+  for (int e = tid; e < bpad * 16; e += BWP_THREADS) {
+    const int r = e >> 4, c = e & 15;
+    const uint4 v = *reinterpret_cast<const uint4*>(H1 + (size_t)r * HID + c * 8);
+    *reinterpret_cast<uint4*>(h1s + r * TW_LD + 8 * (c ^ ((r >> 2) & 3))) = v;
+  }
+  for (int i = tid; i < bpad; i += BWP_THREADS) {
+    crow_s[i] = i < B ? log2_invB - lse[i] * LOG2E : -INFINITY;
+    tw_s[i] = i < B ? rw[i] * invB : 0.0f;
+  }
+  __syncthreads();
+  const int rbase[2] = {tw_row_base(n, g, 0), tw_row_base(n, g, 1)};
+  const int cbase[2] = {tw_col_base(lane, 0), tw_col_base(lane, 1)};
+
+  const int n_blocks = (L + 31) >> 5;
+  const int step = gridDim.x * BWP_WAVES;
+  // a block's W2 rows (fp32 master, hidden 32kb + 8q + 4g + 0..3 per lane; labels
+  // past L read the last row and are never stored), its bias and pair range
+  struct Blk {
+    float4 w[4][4];
+    float bias;
+    int lo, hi;
+  };
+  auto load_blk = [&](int b, Blk& o) {
+    b = min(b, n_blocks - 1);
+    const int label = min(b * 32 + n, L - 1);
+    const float* wrow = W2 + (size_t)label * HID;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o.w[kb][q] = *reinterpret_cast<const float4*>(wrow + 32 * kb + 8 * q + 4 * g);
+    o.bias = b2[label];
+    o.lo = lbeg[b];
+    o.hi = lbeg[b + 1];
+  };
+
+  auto process = [&](int blk, Blk& cur) {
+    const int l0 = blk * 32;
+    const int label = l0 + n;
+    const bool lvalid = label < L;
+    const float bb = lvalid ? cur.bias * LOG2E : -INFINITY;
+    // bf16 fragments of the logits' W2 operand: 8 consecutive hidden units per
+    // lane, from the two lane halves' float4s traded by v_permlane32_swap
+    Fr wf[4][2];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const float4 a4 = cur.w[kb][2 * c], b4 = cur.w[kb][2 * c + 1];
+        const float av[4] = {a4.x, a4.y, a4.z, a4.w}, bv[4] = {b4.x, b4.y, b4.z, b4.w};
+        Fr f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const auto sw = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, av[j]),
+                                                           __builtin_bit_cast(unsigned, bv[j]), false, false);
+          f[j] = (bf16)__builtin_bit_cast(float, sw[0]);
+          f[4 + j] = (bf16)__builtin_bit_cast(float, sw[1]);
+        }
+        wf[kb][c] = f;
+      }
+    const bool has_targets = cur.hi > cur.lo;
+    if (has_targets) {
+      for (int k = lane; k < 32 * nrb; k += 64) mask[k] = 0u;
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      for (int q = cur.lo + lane; q < cur.hi; q += 64) {
+        const int pr = lpair[q];
+        const int row = pr >> 5;
+        atomicOr(&mask[(pr & 31) * nrb + (row >> 5)], 1u << (row & 31));
+      }
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    }
+    f32x16 accw[4];
+#pragma unroll
+    for (int hb = 0; hb < 4; ++hb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) accw[hb][r] = 0.0f;
+    float db2p = 0.0f;
+
+    auto logits = [&](int rb) {
+      f32x16 z;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) z[r] = 0.0f;
+      const bf16* t = h1s + rb * 32 * TW_LD;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) z = M::mma(*reinterpret_cast<const bf16x8*>(t + rbase[c] + 32 * kb), wf[kb][c], z);
+      return z;
+    };
+    f32x16 z = logits(0);
+    for (int rb = 0; rb < nrb; ++rb) {
+      // next row block's logits (the last iteration recomputes a block and drops it)
+      const f32x16 zn = logits(min(rb + 1, nrb - 1));
+      float cr[16];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 c4 = *reinterpret_cast<const float4*>(crow_s + rb * 32 + 8 * q + 4 * g);
+        cr[4 * q + 0] = c4.x; cr[4 * q + 1] = c4.y; cr[4 * q + 2] = c4.z; cr[4 * q + 3] = c4.w;
+      }
+      float dz[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dz[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, bb) + cr[r]);
+      if (has_targets) {
+        const uint32_t mw = mask[n * nrb + rb];
+        if (__any(mw != 0u)) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int rl = 8 * (r >> 2) + 4 * g + (r & 3);
+            if ((mw >> rl) & 1u) dz[r] -= tw_s[rb * 32 + rl];
+          }
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) db2p += dz[r];
+      Fr df[2];
+#pragma unroll
+      for (int c = 0; c < 2; ++c) df[c] = frag_acc<true>(dz, c);
+#pragma unroll
+      for (int hb = 0; hb < 4; ++hb)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const bf16* o = h1s + (rb * 32 + 16 * c) * TW_LD + 32 * hb;
+          const bf16x4 lo4 = lds_read_tr16(o + cbase[0]), hi4 = lds_read_tr16(o + cbase[1]);
+          bf16x8 af;
+          af[0] = lo4[0]; af[1] = lo4[1]; af[2] = lo4[2]; af[3] = lo4[3];
+          af[4] = hi4[0]; af[5] = hi4[1]; af[6] = hi4[2]; af[7] = hi4[3];
+          accw[hb] = M::mma(af, df[c], accw[hb]);
+        }
+      z = zn;
+    }
+    const float db2 = db2p + __shfl_xor(db2p, 32);
+    if (lvalid) {
+      float* wout = W2 + (size_t)label * HID;
+#pragma unroll
+      for (int hb = 0; hb < 4; ++hb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 w = cur.w[hb][q];
+          float4 o;
+          o.x = fmaf(-lr, accw[hb][4 * q + 0], w.x);
+          o.y = fmaf(-lr, accw[hb][4 * q + 1], w.y);
+          o.z = fmaf(-lr, accw[hb][4 * q + 2], w.z);
+          o.w = fmaf(-lr, accw[hb][4 * q + 3], w.w);
+          *reinterpret_cast<float4*>(wout + 32 * hb + 8 * q + 4 * g) = o;
+        }
+      if (g == 0) b2[label] = fmaf(-lr, db2, cur.bias);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    load_blk(blk + 2 * step, cur);  // this set now carries the block two steps ahead
+  };
+
+  const int first = blockIdx.x * BWP_WAVES + wave;
+  Blk s0, s1;
+  load_blk(first, s0);
+  load_blk(first + step, s1);
+  for (int blk = first; blk < n_blocks; blk += 2 * step) {
+    process(blk, s0);
+    if (blk + step >= n_blocks) break;
+    process(blk + step, s1);
+  }
+}
+
 template <bool BF16, int MODE>
 static hipError_t launch_bwd(int grid, size_t shm, hipStream_t st, float* W2, float* b2, int L,
                              const void* H1, const void* H1T, int ld_t, int B, const float* lse,
@@ -319,9 +512,22 @@ hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, const void
   const int cap = mode == BWD_GLOBAL ? 2 * n_cu : n_cu;
   if (grid > cap) grid = cap;
   const float invB = 1.0f / (float)B;
-  if (mode == BWD_STAGED)
-    return launch_bwd<true, BWD_STAGED>(grid, shm, st, W2, b2, L, H1, H1T, ld_t, B, lse, rw, lbeg,
-                                        lpair, lr, invB);
+  if (mode == BWD_STAGED) {
+    static bool attr_done = false;
+    if (!attr_done) {
+      hipError_t e = hipFuncSetAttribute((const void*)k_out_bwd_prefetch,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+      if (e != hipSuccess) return e;
+      attr_done = true;
+    }
+    const size_t shp = (size_t)BWD_CHUNK * TW_LD * 2 + (size_t)2 * nrb * 32 * sizeof(float) +
+                       (size_t)BWP_WAVES * 32 * nrb * sizeof(uint32_t);
+    int gp = (n_blocks + BWP_WAVES - 1) / BWP_WAVES;
+    if (gp > n_cu) gp = n_cu;
+    hipLaunchKernelGGL(k_out_bwd_prefetch, dim3(gp), dim3(BWP_THREADS), shp, st, W2, b2, L,
+                       (const bf16*)H1, B, lse, rw, lbeg, lpair, lr, invB, (float)log2((double)invB));
+    return hipGetLastError();
+  }
   if (mode == BWD_CHUNKED)
     return launch_bwd<true, BWD_CHUNKED>(grid, shm, st, W2, b2, L, H1, H1T, ld_t, B, lse, rw, lbeg,
                                          lpair, lr, invB);
