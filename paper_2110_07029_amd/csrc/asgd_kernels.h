@@ -24,8 +24,8 @@ hipError_t launch_fill_int(int32_t* p, int32_t v, int64_t n, hipStream_t st);
 
 // ---- first layer forward + sort keys ---------------------------------------
 // A1 = X W1 + b1 (fp32), H1 = ReLU(A1) as the output layer's operand type in
-// row-major [rows_pad x 128] and transposed [128 x ld_t]; rows in [B, rows_pad)
-// are zero.  Feature entry p (0 <= p < x.nnz): keys[p] = feature id (F if
+// row-major [rows_pad x 128] and, for fp32 operands only, transposed
+// [128 x ld_t]; rows in [B, rows_pad) are zero.  Feature entry p (0 <= p < x.nnz): keys[p] = feature id (F if
 // invalid), row_of[p] = its row.  With y != NULL, label entry q: lkeys[q] =
 // label id (L if invalid), lrow[q] = its row, and rw[i] = 1/|Y_i|.
 hipError_t launch_gather_fwd(bool use_bf16, const CsrDev& x, const CsrDev* y, const float* W1,

@@ -73,8 +73,10 @@ __global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
     if (wave == 0) {
       H1[(size_t)i * HID + h0] = (E)0.0f;
       H1[(size_t)i * HID + h0 + 1] = (E)0.0f;
-      H1T[(size_t)h0 * ld_t + i] = (E)0.0f;
-      H1T[(size_t)(h0 + 1) * ld_t + i] = (E)0.0f;
+      if constexpr (!BF16) {  // the transposed copy is read only by the fp32 backward
+        H1T[(size_t)h0 * ld_t + i] = (E)0.0f;
+        H1T[(size_t)(h0 + 1) * ld_t + i] = (E)0.0f;
+      }
     }
     return;
   }
@@ -183,8 +185,10 @@ __global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
     const float r0 = fmaxf(a.x, 0.0f), r1 = fmaxf(a.y, 0.0f);
     H1[(size_t)i * HID + h0] = (E)r0;
     H1[(size_t)i * HID + h0 + 1] = (E)r1;
-    H1T[(size_t)h0 * ld_t + i] = (E)r0;
-    H1T[(size_t)(h0 + 1) * ld_t + i] = (E)r1;
+    if constexpr (!BF16) {
+      H1T[(size_t)h0 * ld_t + i] = (E)r0;
+      H1T[(size_t)(h0 + 1) * ld_t + i] = (E)r1;
+    }
   }
 }
 

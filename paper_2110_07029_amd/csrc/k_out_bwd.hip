@@ -323,8 +323,10 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
     const uint4 v = *reinterpret_cast<const uint4*>(H1 + (size_t)r * HID + c * 8);
     *reinterpret_cast<uint4*>(h1s + r * TW_LD + 8 * (c ^ ((r >> 2) & 3))) = v;
   }
+  // per row: the logits' accumulator starts at crow = (log2(1/B) - lse*log2(e)) / log2(e)
+  // (-inf past B), so that dZ = 2^(z*log2(e) + bias*log2(e)) = softmax/B with one fma
   for (int i = tid; i < bpad; i += BWP_THREADS) {
-    crow_s[i] = i < B ? log2_invB - lse[i] * LOG2E : -INFINITY;
+    crow_s[i] = i < B ? (log2_invB - lse[i] * LOG2E) * LN2 : -INFINITY;
     tw_s[i] = i < B ? rw[i] * invB : 0.0f;
   }
   __syncthreads();
@@ -395,10 +397,14 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
       for (int r = 0; r < 16; ++r) accw[hb][r] = 0.0f;
     float db2p = 0.0f;
 
+    // logits of row block rb plus the rows' constants (rows 8q + 4g + 0..3: one float4 each)
     auto logits = [&](int rb) {
       f32x16 z;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) z[r] = 0.0f;
+      for (int q = 0; q < 4; ++q) {
+        const float4 c4 = *reinterpret_cast<const float4*>(crow_s + rb * 32 + 8 * q + 4 * g);
+        z[4 * q + 0] = c4.x; z[4 * q + 1] = c4.y; z[4 * q + 2] = c4.z; z[4 * q + 3] = c4.w;
+      }
       const bf16* t = h1s + rb * 32 * TW_LD;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
@@ -410,15 +416,9 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
     for (int rb = 0; rb < nrb; ++rb) {
       // next row block's logits (the last iteration recomputes a block and drops it)
       const f32x16 zn = logits(min(rb + 1, nrb - 1));
-      float cr[16];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float4 c4 = *reinterpret_cast<const float4*>(crow_s + rb * 32 + 8 * q + 4 * g);
-        cr[4 * q + 0] = c4.x; cr[4 * q + 1] = c4.y; cr[4 * q + 2] = c4.z; cr[4 * q + 3] = c4.w;
-      }
       float dz[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) dz[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, bb) + cr[r]);
+      for (int r = 0; r < 16; ++r) dz[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, bb));
       if (has_targets) {
         const uint32_t mw = mask[n * nrb + rb];
         if (__any(mw != 0u)) {
