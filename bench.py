@@ -28,7 +28,7 @@ METRIC = "training samples/sec at 1 GPU + % of HBM/MFMA roofline per kernel"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}
 H = 128
-OVERLAPPED = ("sort", "labels", "w1_update")  # kernels on the library's second stream
+OVERLAPPED = ("sort", "labels", "hidden", "w1_update")  # kernels on the library's second stream
 
 # HBM traffic of a kernel from `rocprofv3 --pmc FETCH_SIZE` and `--pmc WRITE_SIZE` runs of this bench
 # (KiB per dispatch, averaged; profiles/wide_label_hbm_counters.md), scaled by what the same counters

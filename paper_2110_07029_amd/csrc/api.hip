@@ -496,9 +496,9 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   if (s) return s;
   // The label grouping and the feature sort depend only on what the gather
   // wrote: they run on the internal stream, overlapped with the output-layer
-  // forward.  The W1 update follows them there once dA1 exists, overlapped with
-  // the output-layer backward (the two touch disjoint data); the step ends when
-  // both streams have finished.
+  // forward.  The b1 update, the mean loss and the W1 update follow them there
+  // once dA1 exists, overlapped with the output-layer backward (they touch
+  // disjoint data); the step ends when both streams have finished.
   const int32_t *sk = nullptr, *sv = nullptr;
   HIP_TRY(hipEventRecord(m->ev_fork, m->stream));
   HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_fork, 0));
@@ -509,9 +509,10 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   if (s) return s;
   s = run_forward(m, x, y, rows_pad);
   if (s) return s;
-  TIMED(m, ASGD_K_HIDDEN, launch_hidden_bias(B, m->dA1, m->b1(), lr, m->loss_rows, m->loss, m->stream));
   HIP_TRY(hipEventRecord(m->ev_dA1, m->stream));
   HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_dA1, 0));
+  TIMED_ON(m, ASGD_K_HIDDEN, m->aux,
+           launch_hidden_bias(B, m->dA1, m->b1(), lr, m->loss_rows, m->loss, m->aux));
   CsrDev xd = dev(x);
   TIMED_ON(m, ASGD_K_W1_UPDATE, m->aux,
            launch_w1_update(m->W1(), m->F, sk, sv, x->nnz, m->row_of, xd, m->dA1, lr, m->aux));

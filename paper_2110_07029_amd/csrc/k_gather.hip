@@ -46,15 +46,19 @@ hipError_t launch_fill_int(int32_t* p, int32_t v, int64_t n, hipStream_t st) {
 
 // ---------------------------------------------------------------------------
 // A1[i] = b1 + sum_{(f, v) in row i} v * W1[f];  H1 = max(A1, 0).
-// One workgroup (4 wavefronts) per sample row.  Lane l owns hidden units 2l
+// One workgroup (8 wavefronts) per sample row.  Lane l owns hidden units 2l
 // and 2l+1, so every W1 row is one coalesced 512-byte access.  The row's
-// entries are split into 4 contiguous ranges, one per wavefront; a wavefront
+// entries are split into 8 contiguous ranges, one per wavefront; a wavefront
 // loads up to 64 (id, value) pairs at once (one per lane, also writing their
-// sort keys), broadcasts them with readlane and keeps 8 W1 rows in flight.
-// The 4 partial sums are added in wavefront order, then b1.
+// sort keys), broadcasts them with readlane and issues 16 W1 row loads before
+// the first is used.  Lanes past the range carry id -1, so a partial group of
+// 16 costs one round trip like a full one (the step time follows the longest
+// row of the batch, and nnz per row is heavy-tailed).  The 8 partial sums are
+// added in wavefront order, then b1.
 // ---------------------------------------------------------------------------
-constexpr int GATHER_WAVES = 4;
-constexpr int GATHER_UNROLL = 8;
+constexpr int GATHER_WAVES = 8;
+constexpr int GATHER_UNROLL = 16;
+static_assert(64 % GATHER_UNROLL == 0, "readlane indices stay below 64");
 
 template <bool BF16>
 __global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
@@ -111,8 +115,7 @@ __global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
       row_of[p - base] = i;
     }
     const int cnt = min(64, we - p0);
-    int j = 0;
-    for (; j + GATHER_UNROLL <= cnt; j += GATHER_UNROLL) {
+    for (int j = 0; j < cnt; j += GATHER_UNROLL) {
       int fj[GATHER_UNROLL];
       float vj[GATHER_UNROLL];
       float2 wv[GATHER_UNROLL];
@@ -122,24 +125,14 @@ __global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
         vj[u] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), j + u));
       }
 #pragma unroll
-      for (int u = 0; u < GATHER_UNROLL; ++u)
-        wv[u] = fj[u] >= 0 ? *reinterpret_cast<const float2*>(W1 + (size_t)fj[u] * HID + h0)
-                           : make_float2(0.0f, 0.0f);
+      for (int u = 0; u < GATHER_UNROLL; ++u)  // id -1 (padding, invalid) reads row 0, discarded below
+        wv[u] = *reinterpret_cast<const float2*>(W1 + (size_t)max(fj[u], 0) * HID + h0);
 #pragma unroll
       for (int u = 0; u < GATHER_UNROLL; ++u) {
         if (fj[u] >= 0) {
           acc.x = fmaf(vj[u], wv[u].x, acc.x);
           acc.y = fmaf(vj[u], wv[u].y, acc.y);
         }
-      }
-    }
-    for (; j < cnt; ++j) {
-      const int fj = __builtin_amdgcn_readlane(f, j);
-      const float vj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), j));
-      if (fj >= 0) {
-        const float2 wv = *reinterpret_cast<const float2*>(W1 + (size_t)fj * HID + h0);
-        acc.x = fmaf(vj, wv.x, acc.x);
-        acc.y = fmaf(vj, wv.y, acc.y);
       }
     }
   }

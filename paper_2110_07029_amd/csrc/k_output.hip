@@ -395,14 +395,15 @@ hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2,
 }
 
 // ---------------------------------------------------------------------------
-// Per row: merge the splits, log-sum-exp, loss, dA1.  512 threads = 4 split
-// groups x 128 hidden units for the softmax-weighted sums, 8 wavefronts x
-// the row's labels for the target terms; every partial is combined in a fixed
-// order, so the result does not depend on scheduling.
+// Per row: merge the splits, log-sum-exp, loss, dA1.  512 threads = 16 split
+// groups x 32 threads x 4 hidden units (16-byte loads) for the
+// softmax-weighted sums, 8 wavefronts x the row's labels for the target terms;
+// every partial is combined in a fixed order, so the result does not depend
+// on scheduling.
 // ---------------------------------------------------------------------------
 constexpr int CMB_THREADS = 512;
-constexpr int CMB_GROUPS = CMB_THREADS / HID;  // 4
-constexpr int CMB_WAVES = CMB_THREADS / 64;    // 8
+constexpr int CMB_GROUPS = CMB_THREADS / 32;  // 16
+constexpr int CMB_WAVES = CMB_THREADS / 64;   // 8
 
 template <bool BF16>
 __global__ __launch_bounds__(CMB_THREADS) void k_out_combine(
@@ -417,7 +418,7 @@ __global__ __launch_bounds__(CMB_THREADS) void k_out_combine(
   __shared__ float red_t[CMB_WAVES][HID];
   __shared__ float red_z[CMB_WAVES];
   const int i = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int h = t & (HID - 1), grp = t >> 7;
+  const int grp = t >> 5, h4 = (t & 31) * 4;
 
   float mloc = -INFINITY;
   for (int s = t; s < splits; s += CMB_THREADS) mloc = fmaxf(mloc, m_part[(size_t)s * ld_part + i]);
@@ -428,16 +429,21 @@ __global__ __launch_bounds__(CMB_THREADS) void k_out_combine(
 #pragma unroll
   for (int k = 1; k < CMB_WAVES; ++k) M = fmaxf(M, red_m[k]);
 
-  float St = 0.0f, O = 0.0f;
-#pragma unroll 4
+  float St = 0.0f;
+  float4 O = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll 8
   for (int s = grp; s < splits; s += CMB_GROUPS) {
     const size_t r = (size_t)s * ld_part + i;
     const float e = exp_fast(m_part[r] - M);
     St = fmaf(e, s_part[r], St);
-    O = fmaf(e, o_part[r * HID + h], O);
+    const float4 o = *reinterpret_cast<const float4*>(o_part + r * HID + h4);
+    O.x = fmaf(e, o.x, O.x);
+    O.y = fmaf(e, o.y, O.y);
+    O.z = fmaf(e, o.z, O.z);
+    O.w = fmaf(e, o.w, O.w);
   }
-  red_o[grp][h] = O;
-  if (h == 0) red_s[grp] = St;
+  *reinterpret_cast<float4*>(&red_o[grp][h4]) = O;
+  if ((t & 31) == 0) red_s[grp] = St;
 
   // target terms: wave w takes labels q = w, w + 8, ... of row i; lane owns hidden 2l, 2l+1
   float tw0 = 0.0f, tw1 = 0.0f, zw = 0.0f;
@@ -512,10 +518,13 @@ hipError_t launch_out_combine(bool use_bf16, int B, int splits, const float* m_p
   return hipGetLastError();
 }
 
-// db1 = sum_i dA1[i, :] and the mean loss, 8 row groups x 128 hidden units,
-// groups combined in a fixed order; then b1 -= lr db1.
-constexpr int HB_THREADS = 1024;
-constexpr int HB_GROUPS = HB_THREADS / HID;  // 8
+// db1 = sum_i dA1[i, :] and the mean loss: 256 threads = 8 row groups x 32
+// threads x 4 hidden units (16-byte loads), groups combined in a fixed order;
+// then b1 -= lr db1.  It runs beside the output-layer backward, whose waves
+// hold most of each SIMD's registers: one wave per SIMD and few registers let
+// it find room there.
+constexpr int HB_THREADS = 256;
+constexpr int HB_GROUPS = HB_THREADS / 32;  // 8
 
 __global__ __launch_bounds__(HB_THREADS) void k_hidden_bias(int B, const float* __restrict__ dA1,
                                                             float* __restrict__ b1, float lr,
@@ -523,11 +532,17 @@ __global__ __launch_bounds__(HB_THREADS) void k_hidden_bias(int B, const float* 
                                                             float* __restrict__ loss) {
   __shared__ float red[HB_GROUPS][HID];
   __shared__ float red_l[HB_THREADS / 64];
-  const int t = threadIdx.x, h = t & (HID - 1), grp = t >> 7;
-  float s = 0.0f;
+  const int t = threadIdx.x, grp = t >> 5, h4 = (t & 31) * 4;
+  float4 s = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
 #pragma unroll 4
-  for (int i = grp; i < B; i += HB_GROUPS) s += dA1[(size_t)i * HID + h];
-  red[grp][h] = s;
+  for (int i = grp; i < B; i += HB_GROUPS) {
+    const float4 v = *reinterpret_cast<const float4*>(dA1 + (size_t)i * HID + h4);
+    s.x += v.x;
+    s.y += v.y;
+    s.z += v.z;
+    s.w += v.w;
+  }
+  *reinterpret_cast<float4*>(&red[grp][h4]) = s;
   float ls = 0.0f;
   for (int i = t; i < B; i += HB_THREADS) ls += loss_rows[i];
   ls = wave_sum(ls);

@@ -159,7 +159,9 @@ def step_magnitudes(p, x, y, g, fw, lr):
 
 
 def a1_bound(p, x):
-    """Rigorous bound of a float32 fma chain for A1 = b1 + X W1: n u (|b1| + |X| |W1|)."""
+    """Rigorous bound for A1 = b1 + X W1 summed in float32 in any order, products
+    exact inside fma: row i has n_i + 1 terms, so |err| <= gamma_{n_i} (|b1| + |X| |W1|)
+    <= (n_i + 2) u (|b1| + |X| |W1|) per row."""
     from oracle.model import row_ids
     s0, e0 = int(x.indptr[0]), int(x.indptr[-1])
     ind = np.asarray(x.indices[s0:e0], np.int64)
@@ -168,5 +170,27 @@ def a1_bound(p, x):
     B = len(x.indptr) - 1
     mag = np.tile(np.abs(p["b1"]).astype(np.float64), (B, 1))
     np.add.at(mag, rows, val[:, None] * np.abs(p["W1"][ind]).astype(np.float64))
-    n = np.diff(np.asarray(x.indptr, np.int64)).max() + 1
-    return (n + 1) * 2.0 ** -24 * mag
+    n = np.diff(np.asarray(x.indptr, np.int64)).astype(np.float64)
+    return ((n + 2.0) * 2.0 ** -24)[:, None] * mag
+
+
+def h1_flip_logit_bound(p, x, fw, labels=None):
+    """Largest change of a logit that rounding H1 to bf16 can make between the
+    kernel and the oracle.  The kernel's float32 A1 lies within a1_bound of the
+    exact A1, and ReLU, float32 and bf16 rounding are monotonic, so its bf16 H1
+    lies between the roundings of the interval's ends; d = the larger distance
+    from the oracle's bf16 H1 (zero unless the interval straddles a rounding
+    boundary).  Returns d |W2_bf16|^T, (B, L) or (B, len(labels))."""
+    from oracle.model import round_bf16
+    A1 = np.asarray(fw["A1"], np.float64)
+    e = a1_bound(p, x)
+    rb = lambda a: round_bf16(np.maximum(a, 0.0).astype(np.float32)).astype(np.float64)
+    h = rb(A1)
+    d = np.maximum(np.abs(rb(A1 + e) - h), np.abs(rb(A1 - e) - h))
+    W2 = p["W2"] if labels is None else p["W2"][labels]
+    aw = np.abs(round_bf16(np.asarray(W2, np.float32)).astype(np.float64))
+    out = np.zeros((A1.shape[0], aw.shape[0]))
+    rows = np.flatnonzero(d.any(axis=1))
+    if rows.size:
+        out[rows] = d[rows] @ aw.T
+    return out

@@ -11,8 +11,8 @@ from oracle import elastic as oe
 from oracle import model as om
 from paper_2110_07029_amd import synth
 
-from gpu_util import (RTOL_BF16, Setup, assert_update_close, flush, read_params, step_magnitudes,
-                      write_params)
+from gpu_util import (RTOL_BF16, Setup, assert_update_close, flush, h1_flip_logit_bound, read_params,
+                      step_magnitudes, write_params)
 
 pytestmark = pytest.mark.gpu
 
@@ -69,13 +69,19 @@ def test_full_size_top1():
         asgd.asgd_predict_topk(s.m, s.xb(0, 256), 1, ids, sc)
         torch.cuda.synchronize()
         xh, _ = s.host_batch(0, 256)
-        Z = om.forward(s.params(), xh, None, "bf16")["Z"]
+        p = s.params()
+        fw = om.forward(p, xh, None, "bf16")
+        Z = fw["Z"]
         gi, gs = ids.cpu().numpy()[:, 0], sc.cpu().numpy()[:, 0]
+        # a float32 A1 next to a bf16 rounding boundary may round the other way
+        # in the kernel; fb bounds what that does to each logit
+        fb = h1_flip_logit_bound(p, xh, fw)
         top2 = -np.sort(-Z, axis=1)[:, :2]
-        clear = (top2[:, 0] - top2[:, 1]) > 1e-3 * np.maximum(1.0, np.abs(top2[:, 0]))
+        clear = (top2[:, 0] - top2[:, 1]) > 1e-3 * np.maximum(1.0, np.abs(top2[:, 0])) + 2.0 * fb.max(axis=1)
         assert clear.sum() > 200
         assert np.array_equal(gi[clear], np.argmax(Z[clear], axis=1))
-        assert np.allclose(gs, Z[np.arange(256), gi], rtol=1e-5, atol=1e-5)
+        zi = Z[np.arange(256), gi]
+        assert np.all(np.abs(gs - zi) <= 1e-5 * (1.0 + np.abs(zi)) + fb[np.arange(256), gi])
     finally:
         s.free()
 

@@ -8,7 +8,7 @@ from oracle import elastic as oe
 from oracle import model as om
 from paper_2110_07029_amd import synth
 
-from gpu_util import Setup, flush, read_params, write_params
+from gpu_util import Setup, flush, h1_flip_logit_bound, read_params, write_params
 
 pytestmark = pytest.mark.gpu
 
@@ -127,19 +127,24 @@ def test_topk_ids_bit_exact_on_tie_free_rows(w, bf16, k):
         xh, _ = s.host_batch(0, B)
         p = s.params()
         ops = "bf16" if bf16 else "fp32"
-        Z = om.forward(p, xh, None, ops)["Z"]
+        fw = om.forward(p, xh, None, ops)
+        Z = fw["Z"]
         rid, rsc = om.predict_topk(p, xh, k, ops)
         gi, gs = ids.cpu().numpy(), sc.cpu().numpy()
         tol = 1e-5
+        # bf16 operands: a float32 A1 next to a bf16 rounding boundary may round
+        # the other way in the kernel; fb bounds what that does to each logit
+        fb = h1_flip_logit_bound(p, xh, fw) if bf16 else np.zeros_like(Z)
         checked = 0
         for i in range(B):
             row = np.sort(Z[i])[::-1]
             gaps = -np.diff(row[:k + 1])
-            if np.all(gaps > 50 * tol * max(1.0, abs(row[0]))):
+            if np.all(gaps > 50 * tol * max(1.0, abs(row[0])) + 2.0 * fb[i].max()):
                 assert np.array_equal(gi[i], rid[i]), i
                 checked += 1
             # every returned id is a valid label with its own logit
-            assert np.allclose(gs[i], Z[i, gi[i]], rtol=tol, atol=tol)
+            zi = Z[i, gi[i]]
+            assert np.all(np.abs(gs[i] - zi) <= tol * (1.0 + np.abs(zi)) + fb[i, gi[i]]), i
             assert np.all(np.diff(gs[i]) <= 0)
         assert checked > B // 2
     finally:
