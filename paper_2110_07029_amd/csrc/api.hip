@@ -43,6 +43,10 @@ constexpr int kMaxBatch = 2048;
 // kAuxCus, which stay free for the label grouping and the sort on the internal
 // stream.
 constexpr int kAuxCus = 16;
+// Events that only order work between streams of this device: a device-scope
+// release when recorded (a system-scope one writes the caches back for the
+// host, which costs several microseconds on the recording stream).
+constexpr unsigned kSyncEventFlags = hipEventDisableTiming | hipEventReleaseToDevice;
 
 int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 
@@ -363,11 +367,11 @@ asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t s
   hipError_t e = hipGetDevice(&m->device);
   if (e == hipSuccess)
     e = hipDeviceGetAttribute(&m->n_cu, hipDeviceAttributeMultiprocessorCount, m->device);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_fork, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_labels, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_dA1, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_join, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev, kSyncEventFlags);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_fork, kSyncEventFlags);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_labels, kSyncEventFlags);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_dA1, kSyncEventFlags);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_join, kSyncEventFlags);
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&m->aux, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipMalloc((void**)&m->params, m->n_pad * sizeof(float));
   if (e != hipSuccess) {

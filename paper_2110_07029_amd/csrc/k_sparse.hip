@@ -10,6 +10,7 @@
 namespace asgd {
 
 constexpr int W1_UNROLL = 16;  // dA1 rows in flight per wavefront
+static_assert(64 % W1_UNROLL == 0, "readlane indices stay below 64");
 
 __global__ __launch_bounds__(256) void k_w1_update(float* __restrict__ W1, int F,
                                                    const int32_t* __restrict__ skeys,
@@ -23,6 +24,8 @@ __global__ __launch_bounds__(256) void k_w1_update(float* __restrict__ W1, int F
   if (f >= F) return;                      // label keys and invalid ids
   if (j > 0 && skeys[j - 1] == f) return;  // not the head of its segment
   const int xbase = x.indptr[0];
+  float2* wp = reinterpret_cast<float2*>(W1 + (size_t)f * HID + 2 * lane);
+  float2 w = *wp;  // in flight while the segment is summed
   float2 acc = make_float2(0.0f, 0.0f);
   for (int q0 = j;; q0 += 64) {
     const int q = q0 + lane;
@@ -35,8 +38,9 @@ __global__ __launch_bounds__(256) void k_w1_update(float* __restrict__ W1, int F
       xv = x.values[xbase + p];
     }
     const int cnt = __popcll(__ballot(in));  // a segment is contiguous: lanes 0..cnt-1
-    int u = 0;
-    for (; u + W1_UNROLL <= cnt; u += W1_UNROLL) {
+    // Lanes past the segment read dA1 row 0 and are discarded, so a partial
+    // group of 16 costs one round trip like a full one (most segments are short).
+    for (int u = 0; u < cnt; u += W1_UNROLL) {
       int ru[W1_UNROLL];
       float xu[W1_UNROLL];
       float2 d[W1_UNROLL];
@@ -50,21 +54,14 @@ __global__ __launch_bounds__(256) void k_w1_update(float* __restrict__ W1, int F
         d[k] = *reinterpret_cast<const float2*>(dA1 + (size_t)ru[k] * HID + 2 * lane);
 #pragma unroll
       for (int k = 0; k < W1_UNROLL; ++k) {
-        acc.x = fmaf(xu[k], d[k].x, acc.x);
-        acc.y = fmaf(xu[k], d[k].y, acc.y);
+        if (u + k < cnt) {
+          acc.x = fmaf(xu[k], d[k].x, acc.x);
+          acc.y = fmaf(xu[k], d[k].y, acc.y);
+        }
       }
-    }
-    for (; u < cnt; ++u) {
-      const int ru = __builtin_amdgcn_readlane(row, u);
-      const float xu = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, xv), u));
-      const float2 d = *reinterpret_cast<const float2*>(dA1 + (size_t)ru * HID + 2 * lane);
-      acc.x = fmaf(xu, d.x, acc.x);
-      acc.y = fmaf(xu, d.y, acc.y);
     }
     if (cnt < 64) break;
   }
-  float2* wp = reinterpret_cast<float2*>(W1 + (size_t)f * HID + 2 * lane);
-  float2 w = *wp;
   w.x = fmaf(-lr, acc.x, w.x);
   w.y = fmaf(-lr, acc.y, w.y);
   *wp = w;
