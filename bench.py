@@ -38,8 +38,8 @@ FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 PMC_TRAFFIC = {
     ("wide-label", 256, "out_bwd"): dict(
         sources=("csrc/k_out_bwd.hip", "csrc/asgd_dev.h", "csrc/asgd_kernels.h"),
-        sha256="a1f8a4345dce6da0593333bb60c2b8ba81008d998c6505b57487a7d732f7b7d5",
-        fetch_kib=170315.7, write_kib=374700.7),
+        sha256="0c9448bee78548966a17fa2ce9aef85e774a0bf5722fa3c92fce72c2680b0b94",
+        fetch_kib=169705.7, write_kib=337741.3),
 }
 
 
