@@ -96,8 +96,10 @@ enum {
 
 /* Merge-weight modes (Alg. 2). */
 enum {
-  ASGD_WEIGHTS_ALG2 = 0,   /* by batch size if all u_i are equal, else by update count */
-  ASGD_WEIGHTS_SAMPLES = 1 /* by samples processed (the alternative named in Sec. 3.3) */
+  ASGD_WEIGHTS_ALG2 = 0,    /* by batch size if all u_i are equal, else by update count */
+  ASGD_WEIGHTS_SAMPLES = 1, /* by samples processed (the alternative named in Sec. 3.3) */
+  ASGD_WEIGHTS_UNIFORM = 2  /* 1/n: the plain average of elastic model averaging and of
+                               gradient aggregation (Sec. 2.2), the paper's baselines */
 };
 
 /* ------------------------------------------------------------------------ */
@@ -181,7 +183,8 @@ asgd_status asgd_model_l2_per_param(asgd_model* m, double* out);
 
 /* Alg. 2 weight computation (host only).  u: updates per replica since the
  * last merge; b: batch sizes; samples: samples processed (used by
- * ASGD_WEIGHTS_SAMPLES, may be NULL otherwise).  l2_per_param: per-replica
+ * ASGD_WEIGHTS_SAMPLES, may be NULL otherwise); ASGD_WEIGHTS_UNIFORM gives
+ * every replica 1/n.  l2_per_param: per-replica
  * ||w_i||_2/|w| or NULL to disable the perturbation; when every value is
  * < pert_thr and n > 1, alpha_r *= 1 + delta and alpha_s *= 1 - delta for the
  * replica r with the most updates (then largest batch, then lowest index)
@@ -214,6 +217,15 @@ asgd_status asgd_scale_batches(int32_t n, const int32_t* u, int32_t* b, float* l
  * and learning rate from its update count. */
 typedef struct asgd_elastic asgd_elastic; /* opaque */
 
+/* Who takes the next batch of a round. */
+enum {
+  ASGD_DISPATCH_DYNAMIC = 0, /* the first free replica (Adaptive SGD, Sec. 3.1) */
+  ASGD_DISPATCH_STATIC = 1   /* batch k of the round goes to replica k mod n, whatever its speed:
+                                the fixed schedule of elastic model averaging and, with a
+                                mega-batch of one batch per replica, of gradient aggregation
+                                (Sec. 2.2); a round then waits for its slowest replica */
+};
+
 enum {
   ASGD_CLOCK_TIMED = 0,  /* a replica is free when its last step's HIP event completed */
   ASGD_CLOCK_VIRTUAL = 1 /* deterministic: replica i's clock advances by
@@ -228,10 +240,11 @@ typedef struct asgd_elastic_config {
   double beta;             /* Alg. 1 scaling parameter */
   float lr;                /* learning rate at b_max (linear scaling below) */
   float gamma;             /* momentum of the merge (Alg. 2) */
-  int32_t weight_mode;     /* ASGD_WEIGHTS_ALG2 or ASGD_WEIGHTS_SAMPLES */
+  int32_t weight_mode;     /* ASGD_WEIGHTS_ALG2, _SAMPLES or _UNIFORM */
   int32_t perturb;         /* 1: Alg. 2 perturbation with the L2-per-parameter gate */
   double pert_thr, delta;  /* perturbation threshold and factor */
   int64_t megabatch;       /* samples per round */
+  int32_t dispatch;        /* ASGD_DISPATCH_DYNAMIC or ASGD_DISPATCH_STATIC */
   int32_t clock;           /* ASGD_CLOCK_TIMED or ASGD_CLOCK_VIRTUAL */
   double c0, c1, c2;       /* virtual clock cost model */
   double slow[16];         /* virtual clock per-replica multipliers (0 -> 1) */

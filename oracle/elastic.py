@@ -16,7 +16,12 @@
 * ``dispatch_round`` - dynamic scheduling of one mega-batch (Sec. 3.1): batches
                        go one by one to whichever worker is free first, until
                        the fixed sample budget is spent; worker speed comes
-                       from a deterministic virtual clock.
+                       from a deterministic virtual clock.  With ``static``
+                       the k-th batch goes to worker k mod n instead: the
+                       fixed schedule of the paper's baselines (elastic model
+                       averaging; gradient aggregation when the budget is one
+                       batch per worker, Sec. 2.2), whose uniform weights are
+                       ``MODE_UNIFORM``.
 
 Readings where the paper is silent: the scaled batch size is rounded to the
 nearest integer (halves away from zero) after the bound test on the exact
@@ -35,6 +40,7 @@ import numpy as np
 
 MODE_ALG2 = 0      # Alg. 2: by batch size if all update counts are equal, else by update count
 MODE_SAMPLES = 1   # by samples processed (the alternative named in Sec. 3.3)
+MODE_UNIFORM = 2   # 1/n: the plain model average of the baselines (Sec. 2.2)
 
 
 def _round_half_away(v: float) -> int:
@@ -76,6 +82,8 @@ def merge_weights(u: Sequence[int], b: Sequence[int], samples: Sequence[int], mo
     elif mode == MODE_SAMPLES:
         tot = float(sum(samples))
         alpha = [float(v) / tot for v in samples]
+    elif mode == MODE_UNIFORM:
+        alpha = [1.0 / n] * n
     else:
         raise ValueError(mode)
     if l2_per_param is not None and n > 1 and all(v < pert_thr for v in l2_per_param):
@@ -103,7 +111,7 @@ def step_cost(c0: float, c1: float, c2: float, slow: float, rows: int, nnz: int)
 
 
 def dispatch_round(indptr: np.ndarray, cursor: int, b: Sequence[int], budget: int,
-                   clock: Sequence[float], cost=(0.0, 0.0, 0.0), slow=None):
+                   clock: Sequence[float], cost=(0.0, 0.0, 0.0), slow=None, static: bool = False):
     """Dynamic dispatch of one mega-batch of ``budget`` samples over n workers.
 
     Each batch goes to the worker whose clock is smallest (lowest index on ties);
@@ -119,7 +127,7 @@ def dispatch_round(indptr: np.ndarray, cursor: int, b: Sequence[int], budget: in
     sched, u, samples = [], [0] * n, [0] * n
     left = int(budget)
     while left > 0:
-        w = min(range(n), key=lambda i: (clock[i], i))
+        w = len(sched) % n if static else min(range(n), key=lambda i: (clock[i], i))
         take = min(int(b[w]), left, n_rows - cursor)
         r0, r1 = cursor, cursor + take
         sched.append((w, r0, r1))

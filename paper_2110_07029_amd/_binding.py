@@ -19,7 +19,8 @@ LIB_PATH = os.path.join(_PKG, "libasgd.so")
 ASGD_OK, ASGD_EINVAL, ASGD_ERANGE, ASGD_ENOMEM, ASGD_EHIP, ASGD_ESTATE = 0, -1, -2, -3, -4, -5
 ASGD_VALIDATE = 0x1
 ASGD_PARAM_W1, ASGD_PARAM_B1, ASGD_PARAM_W2, ASGD_PARAM_B2 = 0, 1, 2, 3
-ASGD_WEIGHTS_ALG2, ASGD_WEIGHTS_SAMPLES = 0, 1
+ASGD_WEIGHTS_ALG2, ASGD_WEIGHTS_SAMPLES, ASGD_WEIGHTS_UNIFORM = 0, 1, 2
+ASGD_DISPATCH_DYNAMIC, ASGD_DISPATCH_STATIC = 0, 1
 HIDDEN = 128
 
 # Every symbol include/asgd.h declares (checked by the CPU tests).
@@ -58,7 +59,8 @@ class asgd_csr(ctypes.Structure):
 class asgd_elastic_config(ctypes.Structure):
     _fields_ = [("n_replicas", c_int32), ("b_min", c_int32), ("b_max", c_int32), ("beta", c_double),
                 ("lr", c_float), ("gamma", c_float), ("weight_mode", c_int32), ("perturb", c_int32),
-                ("pert_thr", c_double), ("delta", c_double), ("megabatch", c_int64), ("clock", c_int32),
+                ("pert_thr", c_double), ("delta", c_double), ("megabatch", c_int64), ("dispatch", c_int32),
+                ("clock", c_int32),
                 ("c0", c_double), ("c1", c_double), ("c2", c_double), ("slow", c_double * 16)]
 
 

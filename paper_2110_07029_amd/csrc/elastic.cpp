@@ -3,7 +3,10 @@
 // scheduler (Sec. 4, "Architecture and Workflow").  Per round: dynamic
 // dispatch of a fixed sample budget (Sec. 3.1), normalized merge weights and
 // the momentum merge (Alg. 2, Sec. 3.3), batch-size scaling (Alg. 1,
-// Sec. 3.2).  Built only on the public C ABI plus HIP events.
+// Sec. 3.2).  The same loop runs the paper's baselines (Sec. 2.2, Sec. 5):
+// a static schedule with uniform weights, no momentum and fixed batches is
+// elastic model averaging, and with one batch per replica per round it is
+// gradient aggregation.  Built only on the public C ABI plus HIP events.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -58,8 +61,11 @@ asgd_status asgd_elastic_create(asgd_elastic** out, const asgd_elastic_config* c
   if (cfg->megabatch < 1) return efail(ASGD_EINVAL, "megabatch must be >= 1");
   if (cfg->clock != ASGD_CLOCK_TIMED && cfg->clock != ASGD_CLOCK_VIRTUAL)
     return efail(ASGD_EINVAL, "unknown clock mode");
-  if (cfg->weight_mode != ASGD_WEIGHTS_ALG2 && cfg->weight_mode != ASGD_WEIGHTS_SAMPLES)
+  if (cfg->weight_mode != ASGD_WEIGHTS_ALG2 && cfg->weight_mode != ASGD_WEIGHTS_SAMPLES &&
+      cfg->weight_mode != ASGD_WEIGHTS_UNIFORM)
     return efail(ASGD_EINVAL, "unknown weight mode");
+  if (cfg->dispatch != ASGD_DISPATCH_DYNAMIC && cfg->dispatch != ASGD_DISPATCH_STATIC)
+    return efail(ASGD_EINVAL, "unknown dispatch mode");
   if (!(cfg->lr == cfg->lr) || !(cfg->beta == cfg->beta)) return efail(ASGD_EINVAL, "NaN parameter");
 
   asgd_elastic* e = new (std::nothrow) asgd_elastic();
@@ -128,7 +134,9 @@ asgd_status asgd_elastic_round(asgd_elastic* e, const asgd_csr* x_all, const asg
   }
   while (left > 0) {
     int w = 0;
-    if (c.clock == ASGD_CLOCK_VIRTUAL) {
+    if (c.dispatch == ASGD_DISPATCH_STATIC) {
+      w = nd % n;  // fixed schedule: enqueue on the replica's stream whether or not it is busy
+    } else if (c.clock == ASGD_CLOCK_VIRTUAL) {
       for (int i = 1; i < n; ++i)
         if (clock[i] < clock[w]) w = i;
     } else {

@@ -29,6 +29,8 @@ asgd_status asgd_merge_weights(int32_t n, const int32_t* u, const int32_t* b,
     for (int i = 0; i < n; ++i) tot += equal ? (double)b[i] : (double)u[i];
     if (!(tot > 0.0)) return alg_fail(ASGD_EINVAL, "weights sum to zero");
     for (int i = 0; i < n; ++i) alpha[i] = (equal ? (double)b[i] : (double)u[i]) / tot;
+  } else if (mode == ASGD_WEIGHTS_UNIFORM) {
+    for (int i = 0; i < n; ++i) alpha[i] = 1.0 / (double)n;
   } else if (mode == ASGD_WEIGHTS_SAMPLES) {
     if (!samples) return alg_fail(ASGD_EINVAL, "samples is NULL");
     double tot = 0.0;

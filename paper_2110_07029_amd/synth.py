@@ -229,3 +229,70 @@ def batches(ds: Dataset, batch: int):
     n = ds.x.n_rows
     for r0 in range(0, n, batch):
         yield r0, min(n, r0 + batch)
+
+
+# ---------------------------------------------------------------------------
+# Planted label structure, for time-to-accuracy runs: the draws above have no
+# relation between features and labels, so no model can learn them.  Here
+# every label owns a signature of `sig` feature ids (drawn from the feature
+# Zipf law); a row's labels are drawn as above, its features are each of its
+# labels' signature features kept with probability `keep`, plus `noise`
+# features from the Zipf law; values U(0,1), L2-normalised.  Top-1 accuracy
+# (the best-scoring label is one of the row's labels) is then learnable.
+# ---------------------------------------------------------------------------
+@dataclasses.dataclass(frozen=True)
+class Planted:
+    name: str
+    n_features: int
+    n_labels: int
+    feat_zipf: float
+    label_zipf: float
+    label_lam: float     # labels per row: 1 + Poisson(label_lam)
+    sig: int             # signature features per label
+    keep: float          # probability a signature feature appears in a row
+    noise: int           # noise features per row: Poisson(noise)
+    seed: int
+
+
+PLANTED_SMALL = Planted("planted-small", 20_000, 2_000, 1.05, 1.1, 1.0, 8, 0.7, 12, 3001)
+PLANTED_WIDE = Planted("planted-wide", 135_909, 670_091, 1.05, 1.2, 4.5, 8, 0.7, 40, 3004)
+
+
+def generate_planted(p: Planted, n_samples: int, seed_offset: int = 0) -> Dataset:
+    """Rows of the planted-structure dataset (``seed_offset`` draws a disjoint
+    sample set, e.g. held-out rows, from the same signatures)."""
+    rng_sig = np.random.default_rng(p.seed)
+    fz = _BoundedZipf(p.n_features, p.feat_zipf, rng_sig)
+    sig = fz.draw(p.n_labels * p.sig, rng_sig).reshape(p.n_labels, p.sig)
+    lz = _BoundedZipf(p.n_labels, p.label_zipf, rng_sig)
+    rng = np.random.default_rng(p.seed + 7919 * (1 + seed_offset))
+    n = int(n_samples)
+    lcounts = np.minimum(1 + rng.poisson(p.label_lam, n), p.n_labels).astype(np.int64)
+    lindptr, lids = _distinct_rows(lcounts, p.n_labels, lambda k: lz.draw(k, rng), rng)
+    row_l = np.repeat(np.arange(n), np.diff(lindptr))
+    cand_f = sig[lids].reshape(-1)
+    cand_r = np.repeat(row_l, p.sig)
+    kept = rng.random(len(cand_f)) < p.keep
+    nz = rng.poisson(p.noise, n)
+    noise_r = np.repeat(np.arange(n), nz)
+    noise_f = fz.draw(int(nz.sum()), rng)
+    r_all = np.concatenate([cand_r[kept], noise_r])
+    f_all = np.concatenate([cand_f[kept], noise_f]).astype(np.int64)
+    # distinct (row, feature), sorted; rows left empty get one noise feature
+    key = np.unique(r_all * p.n_features + f_all)
+    rows, feats = key // p.n_features, key % p.n_features
+    empty = np.setdiff1d(np.arange(n), rows)
+    if len(empty):
+        extra = fz.draw(len(empty), rng)
+        key = np.unique(np.concatenate([key, empty * p.n_features + extra]))
+        rows, feats = key // p.n_features, key % p.n_features
+    indptr = np.zeros(n + 1, np.int64)
+    np.cumsum(np.bincount(rows, minlength=n), out=indptr[1:])
+    vals = rng.random(len(feats))
+    norms = np.sqrt(np.bincount(rows, weights=vals * vals, minlength=n))
+    vals = (vals / norms[rows]).astype(np.float32)
+    x = CSR(indptr, feats.astype(np.int32), vals, p.n_features)
+    y = CSR(lindptr, lids, None, p.n_labels)
+    w = Workload(p.name, p.n_features, p.n_labels, n, 256, 0.01, True, "planted", 0.0, 0.0, 0,
+                 p.feat_zipf, "uniform", "poisson", p.label_lam, p.label_zipf, 0)
+    return Dataset(w, x, y)

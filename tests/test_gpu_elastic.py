@@ -29,7 +29,7 @@ def _cuda():
     torch.cuda.synchronize()
 
 
-def _make(ds, clock, perturb, mode, megabatch):
+def _make(ds, clock, perturb, mode, megabatch, dispatch=asgd.ASGD_DISPATCH_DYNAMIC, beta=BETA, gamma=0.9):
     import torch
     ip = np.asarray(ds.x.indptr, np.int64)
     lp = np.asarray(ds.y.indptr, np.int64)
@@ -37,8 +37,9 @@ def _make(ds, clock, perturb, mode, megabatch):
     max_lnnz = int(max(lp[i + B_MAX] - lp[i] for i in range(len(lp) - B_MAX)))
     mcfg = asgd.asgd_config(W.n_features, W.n_labels, 128, B_MAX, max_nnz, max_lnnz, 0, 0)
     cfg = asgd.asgd_elastic_config()
-    cfg.n_replicas, cfg.b_min, cfg.b_max, cfg.beta = N_REP, B_MIN, B_MAX, BETA
-    cfg.lr, cfg.gamma, cfg.weight_mode, cfg.perturb = 0.05, 0.9, mode, perturb
+    cfg.n_replicas, cfg.b_min, cfg.b_max, cfg.beta = N_REP, B_MIN, B_MAX, beta
+    cfg.lr, cfg.gamma, cfg.weight_mode, cfg.perturb = 0.05, gamma, mode, perturb
+    cfg.dispatch = dispatch
     cfg.pert_thr, cfg.delta, cfg.megabatch, cfg.clock = 0.1, 0.1, megabatch, clock
     cfg.c0, cfg.c1, cfg.c2 = COST
     for i, v in enumerate(SLOW):
@@ -48,13 +49,23 @@ def _make(ds, clock, perturb, mode, megabatch):
     return e, streams
 
 
-@pytest.mark.parametrize("mode,perturb", [(asgd.ASGD_WEIGHTS_SAMPLES, 0), (asgd.ASGD_WEIGHTS_ALG2, 1)])
-def test_virtual_clock_rounds_match_oracle_replay(mode, perturb):
+# (weights, perturbation, dispatch, beta, gamma): Adaptive SGD in both weight modes, and the
+# baselines: elastic model averaging (static schedule, uniform weights, fixed batches, no
+# momentum) and gradient aggregation (the same with one batch per replica per round)
+CASES = [(asgd.ASGD_WEIGHTS_SAMPLES, 0, asgd.ASGD_DISPATCH_DYNAMIC, BETA, 0.9, 8),
+         (asgd.ASGD_WEIGHTS_ALG2, 1, asgd.ASGD_DISPATCH_DYNAMIC, BETA, 0.9, 8),
+         (asgd.ASGD_WEIGHTS_UNIFORM, 0, asgd.ASGD_DISPATCH_STATIC, 0.0, 0.0, 8),
+         (asgd.ASGD_WEIGHTS_UNIFORM, 0, asgd.ASGD_DISPATCH_STATIC, 0.0, 0.0, 1)]
+
+
+@pytest.mark.parametrize("mode,perturb,dispatch,beta,gamma,batches", CASES)
+def test_virtual_clock_rounds_match_oracle_replay(mode, perturb, dispatch, beta, gamma, batches):
     import torch
-    flush(f"elastic virtual clock: mode={mode} perturb={perturb}")
+    flush(f"elastic virtual clock: mode={mode} perturb={perturb} dispatch={dispatch} batches/replica={batches}")
     ds = synth.generate(W, n_samples=2000)
-    megabatch = 8 * N_REP * B_MAX
-    e, _ = _make(ds, asgd.ASGD_CLOCK_VIRTUAL, perturb, mode, megabatch)
+    megabatch = batches * N_REP * B_MAX
+    static = dispatch == asgd.ASGD_DISPATCH_STATIC
+    e, _ = _make(ds, asgd.ASGD_CLOCK_VIRTUAL, perturb, mode, megabatch, dispatch, beta, gamma)
     try:
         dx, dy = asgd.DeviceCSR(ds.x), asgd.DeviceCSR(ds.y)
         xa, ya = dx.batch(0, ds.x.n_rows), dy.batch(0, ds.y.n_rows)
@@ -65,7 +76,7 @@ def test_virtual_clock_rounds_match_oracle_replay(mode, perturb):
             log = asgd.asgd_elastic_round(e, xa, ya, ds.x.indptr, ds.y.indptr)
             torch.cuda.synchronize()
             sched, cursor2, _, u, samples = oe.dispatch_round(ds.x.indptr, cursor, b, megabatch,
-                                                              [0.0] * N_REP, COST, SLOW)
+                                                              [0.0] * N_REP, COST, SLOW, static=static)
             assert log["schedule"] == sched, rnd
             assert log["u"][:N_REP] == u and log["samples"][:N_REP] == samples
             assert log["cursor"] == cursor2
@@ -82,9 +93,9 @@ def test_virtual_clock_rounds_match_oracle_replay(mode, perturb):
                 l2 = log["l2_per_param"][:N_REP]  # the gate's inputs are the library's norms
             alpha = oe.merge_weights(u, b, samples, mode, l2, 0.1, 0.1)
             assert np.array_equal(log["alpha"][:N_REP], alpha)
-            ref_g_new, ref_prev = oe.merge(ref_g, ref_prev, flat, alpha, 0.9)
+            ref_g_new, ref_prev = oe.merge(ref_g, ref_prev, flat, alpha, gamma)
             ref_g = ref_g_new
-            b, lr = oe.scale_batches(u, b, lr, B_MIN, B_MAX, BETA)
+            b, lr = oe.scale_batches(u, b, lr, B_MIN, B_MAX, beta)
             assert log["b_next"][:N_REP] == b
             assert [float(np.float32(v)) for v in log["lr_next"][:N_REP]] == [float(np.float32(v)) for v in lr]
             cursor = cursor2
@@ -99,8 +110,11 @@ def test_virtual_clock_rounds_match_oracle_replay(mode, perturb):
         for i in range(N_REP):
             rep = om.flat_params(read_params(asgd.asgd_elastic_model(e, i), W.n_features, W.n_labels))
             assert np.array_equal(rep.view(np.uint32), got.view(np.uint32))
-        # heterogeneous clocks moved the batch sizes: fastest replica largest
-        assert b[0] >= b[-1]
+        if static:      # the baselines keep equal batches and give every replica its share
+            uu = log["u"][:N_REP]   # (a batch cut at the dataset's end adds one dispatch)
+            assert b == [B_MAX] * N_REP and min(uu) >= batches and max(uu) - min(uu) <= 1
+        else:           # heterogeneous clocks moved the batch sizes: fastest replica largest
+            assert b[0] >= b[-1]
     finally:
         asgd.asgd_elastic_free(e)
 

@@ -151,3 +151,46 @@ def test_dispatch_budget_wrap_and_cut():
     # rows 7..10 cut at the end (3 rows), wrap, 4 rows, then the last batch is cut to 2
     assert [(r0, r1) for _, r0, r1 in sched] == [(7, 10), (0, 4), (4, 6)]
     assert sum(s) == 9 and cur == 6 and sum(u) == 3
+
+
+# --------------------------------------------------------------------------- baselines
+def test_uniform_weights_are_one_over_n_whatever_the_counts():
+    for n in (1, 3, 4, 7):
+        u = list(range(1, n + 1))
+        a = oe.merge_weights(u, [64] * n, [10 * v for v in u], oe.MODE_UNIFORM)
+        assert np.array_equal(a, np.full(n, np.float32(1.0 / n)))
+
+
+def test_static_dispatch_is_round_robin_whatever_the_speeds():
+    # the baselines' fixed schedule: a 3x slower worker still gets every n-th batch,
+    # where dynamic dispatch would give most batches to the fast one
+    indptr = np.arange(0, 1001)
+    kw = dict(cost=(0.0, 1.0, 0.0), slow=[1.0, 3.0])
+    sched, cur, clock, u, s = oe.dispatch_round(indptr, 0, [100, 100], 600, [0.0, 0.0], static=True, **kw)
+    assert [w for w, *_ in sched] == [0, 1, 0, 1, 0, 1] and u == [3, 3] and s == [300, 300]
+    assert clock == [300.0, 900.0]          # the round waits for the slower worker
+    _, _, _, ud, _ = oe.dispatch_round(indptr, 0, [100, 100], 600, [0.0, 0.0], **kw)
+    assert ud == [4, 2]                  # dynamic: the fast worker takes more
+
+
+def test_gradient_aggregation_mode_is_one_step_on_the_whole_mega_batch():
+    # Sec. 2.2 (merging after every batch turns model averaging into gradient
+    # aggregation) through the driver's pieces: static dispatch of a budget of one
+    # batch per worker, uniform weights, no momentum.
+    from oracle import model as om
+    from paper_2110_07029_amd import synth
+    w = synth.TINY
+    ds = synth.generate(w, n_samples=300)
+    p = om.init_params(w.n_features, w.n_labels, 128, w.init_seed)
+    n, b, lr = 3, 40, 0.05
+    sched, cur, _, u, s = oe.dispatch_round(ds.x.indptr, 0, [b] * n, n * b, [0.0] * n, static=True)
+    assert [x[0] for x in sched] == [0, 1, 2] and cur == n * b
+    reps = [om.flat_params(om.train_step(p, ds.x.rows(r0, r1), ds.y.rows(r0, r1), lr)[0])
+            for _, r0, r1 in sched]
+    alpha = oe.merge_weights(u, [b] * n, s, oe.MODE_UNIFORM)
+    g0 = om.flat_params(p)
+    merged, _ = oe.merge(g0, g0, reps, alpha, 0.0)
+    big = om.flat_params(om.train_step(p, ds.x.rows(0, n * b), ds.y.rows(0, n * b), lr)[0])
+    d_m, d_b = merged.astype(np.float64) - g0, big.astype(np.float64) - g0
+    # equal up to the float32 storage of the replicas, of 1/3 and of the merge
+    assert np.linalg.norm(d_m - d_b) <= 1e-6 * np.linalg.norm(d_b) + 4 * np.linalg.norm(np.spacing(np.abs(g0)))
