@@ -307,6 +307,36 @@ asgd_status asgd_debug_touched_rows(asgd_model* m, const asgd_csr* x, int32_t* i
                                     int32_t* count_host);
 
 /* ------------------------------------------------------------------------ */
+/* Dataset files (host)                                                      */
+/* ------------------------------------------------------------------------ */
+
+/* Sparse multi-label datasets in the text format of the Extreme
+ * Classification Repository, where the paper's datasets come from (Sec. 5.1,
+ * Table 1, libSVM files): an optional header line "n_rows n_features
+ * n_labels", then per row "l1,l2,... f1:v1 f2:v2 ..." (labels may be empty;
+ * blank lines and lines starting with '#' are skipped).  Feature ids are
+ * 0-based, or 1-based with one_based = 1 (as in plain libSVM files); they are
+ * shifted to 0-based.  Without a header, n_features / n_labels are one past
+ * the largest id seen. */
+typedef struct asgd_libsvm_info {
+  int64_t n_rows, nnz, label_nnz;
+  int64_t n_features, n_labels;
+  int64_t header_rows; /* the header's row count, or -1 without a header */
+} asgd_libsvm_info;
+
+/* First pass: sizes.  ASGD_EINVAL names the file and line of a syntax
+ * error, or an id beyond the header's counts. */
+asgd_status asgd_libsvm_scan(const char* path, int32_t one_based, asgd_libsvm_info* info);
+
+/* Second pass into caller-owned host arrays sized from info: indptr and
+ * label_indptr [n_rows + 1] (int64, from 0), indices / values [nnz],
+ * label_indices [label_nnz]; every row sorted by id.  A repeated id in a row
+ * is ASGD_EINVAL; a file that changed since the scan is ASGD_ESTATE. */
+asgd_status asgd_libsvm_read(const char* path, int32_t one_based, const asgd_libsvm_info* info,
+                             int64_t* indptr, int32_t* indices, float* values, int64_t* label_indptr,
+                             int32_t* label_indices);
+
+/* ------------------------------------------------------------------------ */
 /* Kernel timing (HIP events on the model's stream)                          */
 /* ------------------------------------------------------------------------ */
 

@@ -14,6 +14,6 @@ from ._binding import (  # noqa: F401
     asgd_merge_weights, asgd_scale_batches, asgd_debug_forward, asgd_debug_touched_rows,
     asgd_model_set_timing, asgd_model_get_timing, KERNELS, ASGD_CLOCK_TIMED, ASGD_CLOCK_VIRTUAL,
     asgd_elastic_config, asgd_elastic_log, asgd_elastic_create, asgd_elastic_free, asgd_elastic_round,
-    asgd_elastic_model,
+    asgd_elastic_model, asgd_libsvm_info, asgd_libsvm_scan, asgd_libsvm_read,
 )
 from .device_data import DeviceCSR  # noqa: F401

@@ -29,7 +29,8 @@ EXPORTS = (
     "asgd_model_num_params", "asgd_model_get_params", "asgd_model_set_params",
     "asgd_train_step", "asgd_model_last_loss", "asgd_predict_topk", "asgd_merge",
     "asgd_model_l2_per_param", "asgd_merge_weights", "asgd_scale_batches",
-    "asgd_debug_forward", "asgd_debug_touched_rows", "asgd_model_set_timing",
+    "asgd_debug_forward", "asgd_debug_touched_rows", "asgd_libsvm_scan", "asgd_libsvm_read",
+    "asgd_model_set_timing",
     "asgd_model_get_timing", "asgd_elastic_create", "asgd_elastic_free", "asgd_elastic_round",
     "asgd_elastic_model", "asgd_last_error",
 )
@@ -64,6 +65,11 @@ class asgd_elastic_config(ctypes.Structure):
                 ("c0", c_double), ("c1", c_double), ("c2", c_double), ("slow", c_double * 16)]
 
 
+class asgd_libsvm_info(ctypes.Structure):
+    _fields_ = [("n_rows", c_int64), ("nnz", c_int64), ("label_nnz", c_int64), ("n_features", c_int64),
+                ("n_labels", c_int64), ("header_rows", c_int64)]
+
+
 class asgd_elastic_log(ctypes.Structure):
     _fields_ = [("n_dispatch", c_int32), ("max_dispatch", c_int32), ("replica", POINTER(c_int32)),
                 ("row0", POINTER(c_int32)), ("row1", POINTER(c_int32)), ("u", c_int32 * 16),
@@ -96,6 +102,8 @@ def _declare(lib):
                                          c_int32, c_int32, c_double]),
         "asgd_debug_forward": (c_int32, [P, POINTER(asgd_csr), POINTER(asgd_csr), P, P, P]),
         "asgd_debug_touched_rows": (c_int32, [P, POINTER(asgd_csr), P, POINTER(c_int32)]),
+        "asgd_libsvm_scan": (c_int32, [ctypes.c_char_p, c_int32, POINTER(asgd_libsvm_info)]),
+        "asgd_libsvm_read": (c_int32, [ctypes.c_char_p, c_int32, POINTER(asgd_libsvm_info), P, P, P, P, P]),
         "asgd_model_set_timing": (c_int32, [P, c_int32]),
         "asgd_model_get_timing": (c_int32, [P, c_int32, POINTER(c_double), POINTER(c_int64)]),
         "asgd_elastic_create": (c_int32, [POINTER(c_void_p), POINTER(asgd_elastic_config),
@@ -269,6 +277,25 @@ def asgd_debug_touched_rows(m: int, x: asgd_csr, ids_dev) -> int:
     c = c_int32()
     _check(load().asgd_debug_touched_rows(m, byref(x), _ptr(ids_dev), byref(c)), "asgd_debug_touched_rows")
     return c.value
+
+
+def asgd_libsvm_scan(path: str, one_based: bool = False) -> asgd_libsvm_info:
+    info = asgd_libsvm_info()
+    _check(load().asgd_libsvm_scan(os.fsencode(path), 1 if one_based else 0, byref(info)), "asgd_libsvm_scan")
+    return info
+
+
+def asgd_libsvm_read(path: str, info: asgd_libsvm_info, one_based: bool = False):
+    """(indptr, indices, values, label_indptr, label_indices) as host numpy arrays."""
+    ip = np.zeros(info.n_rows + 1, np.int64)
+    ix = np.zeros(max(info.nnz, 1), np.int32)
+    va = np.zeros(max(info.nnz, 1), np.float32)
+    lp = np.zeros(info.n_rows + 1, np.int64)
+    lx = np.zeros(max(info.label_nnz, 1), np.int32)
+    _check(load().asgd_libsvm_read(os.fsencode(path), 1 if one_based else 0, byref(info), ip.ctypes.data,
+                                   ix.ctypes.data, va.ctypes.data, lp.ctypes.data, lx.ctypes.data),
+           "asgd_libsvm_read")
+    return ip, ix[:info.nnz], va[:info.nnz], lp, lx[:info.label_nnz]
 
 
 def asgd_model_set_timing(m: int, enable: bool):
