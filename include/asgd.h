@@ -350,7 +350,8 @@ enum {
   ASGD_K_OUT_BWD = 5,     /* output-layer backward + W2/b2 update */
   ASGD_K_W1_UPDATE = 6,   /* sparse W1 gradient + update (internal stream) */
   ASGD_K_MERGE = 7,       /* normalized merge (timed on the global model) */
-  ASGD_K_LABELS = 8,      /* (label, row) pairs grouped by label block (internal stream) */
+  ASGD_K_LABELS = 8,      /* (label, row) pairs grouped by label block: a workgroup of the
+                             OUT_FWD launch, so never recorded on its own */
   ASGD_K_COUNT = 9
 };
 

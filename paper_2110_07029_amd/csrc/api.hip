@@ -40,8 +40,8 @@ asgd_status fail_hip(hipError_t e, const char* what) {
 constexpr int64_t kAlign = 64;  // floats
 constexpr int kMaxBatch = 2048;
 // The output-layer forward runs one persistent workgroup per CU except
-// kAuxCus, which stay free for the label grouping and the sort on the internal
-// stream.
+// kAuxCus, which stay free for the feature sort on the internal stream and
+// the forward launch's own label-grouping workgroup.
 constexpr int kAuxCus = 16;
 // Events that only order work between streams of this device: a device-scope
 // release when recorded (a system-scope one writes the caches back for the
@@ -74,7 +74,8 @@ struct asgd_model {
   int n_cu = 256;
   // internal stream: the label grouping and the feature sort overlap the output layer
   hipStream_t aux = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_labels = nullptr, ev_dA1 = nullptr, ev_join = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_dA1 = nullptr, ev_join = nullptr;
+  LabelJobPlan label_plan{};  // LDS of the forward launch's label-grouping workgroup
   hipEvent_t ev = nullptr;
 
   // parameters
@@ -299,7 +300,8 @@ asgd_status run_sort(asgd_model* m, hipStream_t st, int n_keys, const int32_t** 
   return ASGD_OK;
 }
 
-asgd_status run_forward(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int rows_pad) {
+asgd_status run_forward(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int rows_pad,
+                        const LabelJob* labels) {
   const int B = x->n_rows;
   const int splits = fwd_splits(m, B);
   const int n_tiles = (m->L + OUT_TILE - 1) / OUT_TILE;
@@ -307,7 +309,7 @@ asgd_status run_forward(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int
   const int s_eff = (n_tiles + tps - 1) / tps;
   if ((int64_t)s_eff * rows_pad > m->part_rows) return fail(ASGD_ERANGE, "partial buffer too small");
   TIMED(m, ASGD_K_OUT_FWD, launch_out_fwd_train(m->bf16, m->W2(), m->b2(), m->L, m->H1, B, splits, m->m_part,
-                               m->s_part, m->o_part, rows_pad, m->stream));
+                               m->s_part, m->o_part, rows_pad, labels, &m->label_plan, m->stream));
   CsrDev yd = y ? dev(y) : CsrDev{};
   TIMED(m, ASGD_K_OUT_COMBINE, launch_out_combine(m->bf16, B, s_eff, m->m_part, m->s_part, m->o_part, rows_pad, m->W2(),
                              m->b2(), m->L, m->H1, m->A1, y ? &yd : nullptr, m->lse, m->loss_rows,
@@ -369,10 +371,13 @@ asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t s
     e = hipDeviceGetAttribute(&m->n_cu, hipDeviceAttributeMultiprocessorCount, m->device);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev, kSyncEventFlags);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_fork, kSyncEventFlags);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_labels, kSyncEventFlags);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_dA1, kSyncEventFlags);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_join, kSyncEventFlags);
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&m->aux, hipStreamNonBlocking);
+  if (e == hipSuccess) {
+    m->label_plan = label_job_plan(m->bf16, L);
+    if (!m->label_plan.ok) e = hipErrorInvalidConfiguration;
+  }
   if (e == hipSuccess) e = hipMalloc((void**)&m->params, m->n_pad * sizeof(float));
   if (e != hipSuccess) {
     asgd_model_free(m);
@@ -411,7 +416,6 @@ asgd_status asgd_model_free(asgd_model* m) {
   if (m->ws) (void)hipFree(m->ws);
   if (m->ev) (void)hipEventDestroy(m->ev);
   if (m->ev_fork) (void)hipEventDestroy(m->ev_fork);
-  if (m->ev_labels) (void)hipEventDestroy(m->ev_labels);
   if (m->ev_dA1) (void)hipEventDestroy(m->ev_dA1);
   if (m->ev_join) (void)hipEventDestroy(m->ev_join);
   if (m->aux) (void)hipStreamDestroy(m->aux);
@@ -498,20 +502,19 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   int rows_pad = 0;
   s = run_gather(m, x, y, &rows_pad);
   if (s) return s;
-  // The label grouping and the feature sort depend only on what the gather
-  // wrote: they run on the internal stream, overlapped with the output-layer
-  // forward.  The b1 update, the mean loss and the W1 update follow them there
-  // once dA1 exists, overlapped with the output-layer backward (they touch
-  // disjoint data); the step ends when both streams have finished.
+  // The feature sort depends only on what the gather wrote: it runs on the
+  // internal stream, overlapped with the output-layer forward, whose launch
+  // also groups the labels for the backward (one workgroup of its own).  The
+  // b1 update, the mean loss and the W1 update follow the sort on the internal
+  // stream once dA1 exists, overlapped with the output-layer backward (they
+  // touch disjoint data); the step ends when both streams have finished.
   const int32_t *sk = nullptr, *sv = nullptr;
   HIP_TRY(hipEventRecord(m->ev_fork, m->stream));
   HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_fork, 0));
-  TIMED_ON(m, ASGD_K_LABELS, m->aux,
-           launch_label_blocks(m->lkeys, y->nnz, m->L, m->lrow, m->lbeg, m->lpair, m->lcnt, m->aux));
-  HIP_TRY(hipEventRecord(m->ev_labels, m->aux));
   s = run_sort(m, m->aux, x->nnz, &sk, &sv);
   if (s) return s;
-  s = run_forward(m, x, y, rows_pad);
+  const LabelJob labels{m->lkeys, y->nnz, m->lrow, m->lbeg, m->lpair, m->lcnt, 0};
+  s = run_forward(m, x, y, rows_pad, &labels);
   if (s) return s;
   HIP_TRY(hipEventRecord(m->ev_dA1, m->stream));
   HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_dA1, 0));
@@ -521,7 +524,6 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   TIMED_ON(m, ASGD_K_W1_UPDATE, m->aux,
            launch_w1_update(m->W1(), m->F, sk, sv, x->nnz, m->row_of, xd, m->dA1, lr, m->aux));
   HIP_TRY(hipEventRecord(m->ev_join, m->aux));
-  HIP_TRY(hipStreamWaitEvent(m->stream, m->ev_labels, 0));
   TIMED(m, ASGD_K_OUT_BWD, launch_out_bwd(m->bf16, m->W2(), m->b2(), m->L, m->H1, m->H1T, m->rows_pad_max, B,
                          m->lse, m->rw, m->lbeg, m->lpair, lr, m->n_cu, m->stream));
   HIP_TRY(hipStreamWaitEvent(m->stream, m->ev_join, 0));
@@ -651,7 +653,7 @@ asgd_status asgd_debug_forward(asgd_model* m, const asgd_csr* x, const asgd_csr*
   int rows_pad = 0;
   s = run_gather(m, x, y, &rows_pad);
   if (s) return s;
-  s = run_forward(m, x, y, rows_pad);
+  s = run_forward(m, x, y, rows_pad, nullptr);
   if (s) return s;
   if (a1_dev)
     HIP_TRY(hipMemcpyAsync(a1_dev, m->A1, (size_t)B * HID * 4, hipMemcpyDeviceToDevice, m->stream));

@@ -48,19 +48,31 @@ hipError_t launch_sort(const int32_t* keys_in, int n, int key_bits, int32_t* key
 // ---- (label, row) pairs grouped by 32-label block ---------------------------
 // For the m label entries: lbeg[b] .. lbeg[b+1] (b < ceil(L/32)) is the range
 // of block b's pairs in lpair, each (row << 5) | (label % 32); invalid labels
-// (key L) are dropped.  gcnt: ceil(L/32) ints of scratch, used only when the
-// counters do not fit in LDS.
-hipError_t launch_label_blocks(const int32_t* lkeys, int m, int L, const int32_t* lrow, int32_t* lbeg,
-                               int32_t* lpair, int32_t* gcnt, hipStream_t st);
+// (key L) are dropped.  lcnt: ceil(L/32) ints of scratch, used only when the
+// counters do not fit in LDS.  Runs as one workgroup of the output-layer
+// forward launch.
+struct LabelJob {
+  const int32_t* lkeys;
+  int m;
+  const int32_t* lrow;
+  int32_t *lbeg, *lpair, *lcnt;
+  int in_lds;  // filled in from the plan by the launcher
+};
+struct LabelJobPlan {
+  int ok, lds_bytes, in_lds;
+};
+LabelJobPlan label_job_plan(bool use_bf16, int L);
 
 // ---- output layer -----------------------------------------------------------
 constexpr int OUT_TILE = 32;  // labels per forward tile
 int out_rows_per_block(bool use_bf16);
 // Forward over label splits: per (split, row) running max, sum of exponentials
-// and sum_l exp(Z - m) W2[l] (flash-style); grid = splits x row blocks.
+// and sum_l exp(Z - m) W2[l] (flash-style); one workgroup per (split, row
+// block), plus, with job != NULL, one that groups the labels (plan from
+// label_job_plan).
 hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2, int L, const void* H1,
                                 int B, int splits, float* m_part, float* s_part, float* o_part,
-                                int ld_part, hipStream_t st);
+                                int ld_part, const LabelJob* job, const LabelJobPlan* plan, hipStream_t st);
 // Per row: lse, loss_i, dA1 (see kernel); y may be NULL (lse only).
 hipError_t launch_out_combine(bool use_bf16, int B, int splits, const float* m_part,
                               const float* s_part, const float* o_part, int ld_part,

@@ -17,6 +17,7 @@
 
 #include "asgd_dev.h"
 #include "asgd_kernels.h"
+#include "aux_dev.h"
 
 namespace asgd {
 
@@ -181,12 +182,17 @@ __device__ __forceinline__ typename Mma<BF16>::frag tile_frag_wt(const typename 
 // ---------------------------------------------------------------------------
 constexpr int FWD_NBUF = 3;  // LDS ring of W2 tiles
 
+// With a label job, workgroup n_fwd of the launch (dispatched last, on a CU
+// the forward leaves free) groups the batch's labels for the backward: it
+// depends only on the gather and finishes long before the forward, so the
+// backward needs no event from another stream.  Its counters live in the
+// launch's dynamic LDS (or in global memory when they do not fit).
 template <bool BF16>
 __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
     const float* __restrict__ W2, const float* __restrict__ b2, int L,
     const typename Mma<BF16>::elem* __restrict__ H1, int B, int tiles_per_split, int n_tiles,
     float* __restrict__ m_part, float* __restrict__ s_part, float* __restrict__ o_part,
-    int ld_part) {
+    int ld_part, int s_eff, int n_fwd, LabelJob lj) {
   using M = Mma<BF16>;
   using E = typename M::elem;
   using Fr = typename M::frag;
@@ -197,15 +203,24 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
   __shared__ __attribute__((aligned(16))) E wt[FWD_NBUF][tileT_elems<BF16>()];
   __shared__ __attribute__((aligned(16))) float bt[FWD_NBUF][OUT_TILE];
 
+  if ((int)blockIdx.x >= n_fwd) {
+    extern __shared__ int32_t job_lds[];
+    if (lj.in_lds)
+      wg_label_blocks<FWD_THREADS, true>(lj.lkeys, lj.m, L, lj.lrow, lj.lbeg, lj.lpair, job_lds,
+                                         job_lds + ((L + 31) >> 5));
+    else
+      wg_label_blocks<FWD_THREADS, false>(lj.lkeys, lj.m, L, lj.lrow, lj.lbeg, lj.lpair, lj.lcnt, job_lds);
+    return;
+  }
   const int lane = threadIdx.x & 63, g = lane >> 5, n = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int split = blockIdx.x;
+  const int split = (int)blockIdx.x % s_eff;
   const int t_begin = split * tiles_per_split;
   const int t_end = min(n_tiles, t_begin + tiles_per_split);
   const int t_last = t_end - 1;
   // Rows past B (up to the 256-row padding, zero in H1) are computed like the
   // others and never written out, so the loop has no row-dependent branch.
-  const int row0 = blockIdx.y * RB + wave * 32;
+  const int row0 = ((int)blockIdx.x / s_eff) * RB + wave * 32;
   const W2Src src = w2_src(W2, b2, L);
   const int rbase[2] = {tw_row_base(n, g, 0), tw_row_base(n, g, 1)};
   const int cbase[2] = {tw_col_base(lane, 0), tw_col_base(lane, 1)};
@@ -377,20 +392,48 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
   }
 }
 
+LabelJobPlan label_job_plan(bool use_bf16, int L) {
+  const void* fn = use_bf16 ? (const void*)k_out_fwd_train<true> : (const void*)k_out_fwd_train<false>;
+  LabelJobPlan p{};
+  hipFuncAttributes fa{};
+  int dev = 0, lds_max = 0;
+  if (hipFuncGetAttributes(&fa, fn) != hipSuccess || hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+    return p;
+  // what the forward's own arrays leave of a workgroup's LDS (160 KB on gfx950)
+  const int budget = lds_max - (int)fa.sharedSizeBytes;
+  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, budget) != hipSuccess) return p;
+  const int ints = (L + 31) / 32 + FWD_THREADS / 64;
+  p.in_lds = ints * 4 <= budget;
+  p.lds_bytes = 4 * (p.in_lds ? ints : FWD_THREADS / 64);
+  p.ok = p.lds_bytes <= budget;
+  return p;
+}
+
 hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2, int L, const void* H1,
                                 int B, int splits, float* m_part, float* s_part, float* o_part,
-                                int ld_part, hipStream_t st) {
+                                int ld_part, const LabelJob* job, const LabelJobPlan* plan, hipStream_t st) {
   const int n_tiles = (L + OUT_TILE - 1) / OUT_TILE;
   const int tps = (n_tiles + splits - 1) / splits;
   const int s_eff = (n_tiles + tps - 1) / tps;
   const int RB = out_rows_per_block(use_bf16);
-  const dim3 grid(s_eff, (B + RB - 1) / RB), block(FWD_THREADS);
+  const int n_fwd = s_eff * ((B + RB - 1) / RB);
+  LabelJob lj{};
+  int lds = 0, n_job = 0;
+  if (job) {
+    if (!plan || !plan->ok) return hipErrorInvalidValue;
+    lj = *job;
+    lj.in_lds = plan->in_lds;
+    lds = plan->lds_bytes;
+    n_job = 1;
+  }
+  const dim3 grid(n_fwd + n_job), block(FWD_THREADS);
   if (use_bf16)
-    hipLaunchKernelGGL(k_out_fwd_train<true>, grid, block, 0, st, W2, b2, L, (const bf16*)H1, B,
-                       tps, n_tiles, m_part, s_part, o_part, ld_part);
+    hipLaunchKernelGGL(k_out_fwd_train<true>, grid, block, lds, st, W2, b2, L, (const bf16*)H1, B, tps,
+                       n_tiles, m_part, s_part, o_part, ld_part, s_eff, n_fwd, lj);
   else
-    hipLaunchKernelGGL(k_out_fwd_train<false>, grid, block, 0, st, W2, b2, L, (const float*)H1, B,
-                       tps, n_tiles, m_part, s_part, o_part, ld_part);
+    hipLaunchKernelGGL(k_out_fwd_train<false>, grid, block, lds, st, W2, b2, L, (const float*)H1, B, tps,
+                       n_tiles, m_part, s_part, o_part, ld_part, s_eff, n_fwd, lj);
   return hipGetLastError();
 }
 

@@ -1,8 +1,7 @@
 // Stable LSD radix sort of int32 keys with their original positions as the
-// payload.  It orders the batch's (feature id) and (label id) entries so that
-// the sparse W1 gradient becomes a segmented reduction over equal feature ids
-// (no contended atomics, fixed summation order) and so that each output-layer
-// tile can find its true labels with a binary search.
+// payload.  It orders the batch's feature entries so that the sparse W1
+// gradient becomes a segmented reduction over equal feature ids (no contended
+// atomics, fixed summation order).
 //
 // One pass over a digit of up to 11 bits = three launches:
 //   hist    : per-workgroup digit counts of a 1024-key chunk (LDS counters),
@@ -187,111 +186,6 @@ hipError_t launch_sort(const int32_t* keys_in, int n, int key_bits, int32_t* key
     vin = vout;
     kout = (kout == keys_a) ? keys_b : keys_a;
     vout = (vout == vals_a) ? vals_b : vals_a;
-  }
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------------------
-// (label, row) pairs grouped by 32-label block for the output-layer backward,
-// where a wavefront owns one block and needs the rows that carry its labels.
-// One workgroup: a counter per block (LDS when they fit), an exclusive scan
-// into lbeg, then every valid pair is placed in its block's range.  The order
-// of the pairs inside a block is not fixed; the backward only ORs them into a
-// bit mask, whose value does not depend on it.
-// ---------------------------------------------------------------------------
-constexpr int LB_THREADS = 256;  // one wave per SIMD: fits beside the output-layer forward
-constexpr int LB_LDS_MAX = 32768;  // blocks whose counters fit in LDS (128 KB)
-
-template <bool LDS>
-__device__ __forceinline__ int lb_load(const int32_t* p) {
-  if constexpr (LDS)
-    return *p;
-  else  // counters updated by atomics at L2: read past the L1
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-template <bool LDS>
-__device__ __forceinline__ void lb_sync() {
-  if constexpr (!LDS) __threadfence();
-  __syncthreads();
-}
-
-template <bool LDS>
-__global__ __launch_bounds__(LB_THREADS) void k_label_blocks(const int32_t* __restrict__ lkeys, int m,
-                                                             int L, const int32_t* __restrict__ lrow,
-                                                             int32_t* __restrict__ lbeg,
-                                                             int32_t* __restrict__ lpair,
-                                                             int32_t* gcnt) {
-  extern __shared__ int32_t lds_cnt[];
-  __shared__ int wsum[LB_THREADS / 64];
-  int32_t* cnt = LDS ? lds_cnt : gcnt;
-  const int nb = (L + 31) >> 5;
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  for (int b = t; b < nb; b += LB_THREADS) cnt[b] = 0;
-  lb_sync<LDS>();
-  for (int q = t; q < m; q += LB_THREADS) {
-    const int lab = lkeys[q];
-    if (lab >= 0 && lab < L) atomicAdd(&cnt[lab >> 5], 1);
-  }
-  lb_sync<LDS>();
-  // exclusive scan; thread t owns the contiguous blocks [t*per, t*per + per)
-  const int per = (nb + LB_THREADS - 1) / LB_THREADS;
-  const int b0 = min(nb, t * per), b1 = min(nb, b0 + per);
-  int local = 0;
-  for (int b = b0; b < b1; ++b) local += lb_load<LDS>(cnt + b);
-  int x = local;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) wsum[w] = x;
-  __syncthreads();
-  if (w == 0) {
-    int v = lane < LB_THREADS / 64 ? wsum[lane] : 0;
-#pragma unroll
-    for (int o = 1; o < LB_THREADS / 64; o <<= 1) {
-      const int y = __shfl_up(v, o);
-      if (lane >= o) v += y;
-    }
-    if (lane < LB_THREADS / 64) wsum[lane] = v;
-  }
-  __syncthreads();
-  int run = (w > 0 ? wsum[w - 1] : 0) + x - local;
-  for (int b = b0; b < b1; ++b) {
-    const int c = lb_load<LDS>(cnt + b);
-    lbeg[b] = run;
-    cnt[b] = run;  // becomes the block's fill cursor
-    run += c;
-  }
-  if (t == LB_THREADS - 1) lbeg[nb] = run;  // the last thread ends at the total
-  lb_sync<LDS>();
-  for (int q = t; q < m; q += LB_THREADS) {
-    const int lab = lkeys[q];
-    if (lab >= 0 && lab < L) {
-      const int pos = atomicAdd(&cnt[lab >> 5], 1);
-      lpair[pos] = (lrow[q] << 5) | (lab & 31);
-    }
-  }
-}
-
-hipError_t launch_label_blocks(const int32_t* lkeys, int m, int L, const int32_t* lrow, int32_t* lbeg,
-                               int32_t* lpair, int32_t* gcnt, hipStream_t st) {
-  const int nb = (L + 31) / 32;
-  if (nb <= LB_LDS_MAX) {
-    static bool attr_done = false;
-    if (!attr_done) {
-      hipError_t e = hipFuncSetAttribute((const void*)k_label_blocks<true>,
-                                         hipFuncAttributeMaxDynamicSharedMemorySize,
-                                         LB_LDS_MAX * (int)sizeof(int32_t));
-      if (e != hipSuccess) return e;
-      attr_done = true;
-    }
-    hipLaunchKernelGGL(k_label_blocks<true>, dim3(1), dim3(LB_THREADS), nb * sizeof(int32_t), st, lkeys,
-                       m, L, lrow, lbeg, lpair, gcnt);
-  } else {
-    hipLaunchKernelGGL(k_label_blocks<false>, dim3(1), dim3(LB_THREADS), 0, st, lkeys, m, L, lrow, lbeg,
-                       lpair, gcnt);
   }
   return hipGetLastError();
 }
