@@ -346,9 +346,10 @@ enum {
   ASGD_K_SORT = 1,        /* radix sort of the batch's feature ids (internal stream) */
   ASGD_K_OUT_FWD = 2,     /* output-layer forward over all labels */
   ASGD_K_OUT_COMBINE = 3, /* per-row merge of label splits, loss, dA1 */
-  ASGD_K_HIDDEN = 4,      /* b1 gradient / update and mean loss (internal stream) */
+  ASGD_K_HIDDEN = 4,      /* b1 gradient / update and mean loss: a workgroup of the
+                             W1_UPDATE launch, so never recorded on its own */
   ASGD_K_OUT_BWD = 5,     /* output-layer backward + W2/b2 update */
-  ASGD_K_W1_UPDATE = 6,   /* sparse W1 gradient + update (internal stream) */
+  ASGD_K_W1_UPDATE = 6,   /* sparse W1 gradient + update, b1 update, mean loss (internal stream) */
   ASGD_K_MERGE = 7,       /* normalized merge (timed on the global model) */
   ASGD_K_LABELS = 8,      /* (label, row) pairs grouped by label block: a workgroup of the
                              OUT_FWD launch, so never recorded on its own */

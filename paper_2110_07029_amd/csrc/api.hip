@@ -106,6 +106,7 @@ struct asgd_model {
   int32_t *ka = nullptr, *va = nullptr, *kb = nullptr, *vb = nullptr;
   int32_t* hist = nullptr;
   int32_t* row_of = nullptr;
+  float* w1_part = nullptr;  // partial W1 gradients of segments that cross a window
   int32_t* lrow = nullptr;
   int32_t* lkeys = nullptr;
   int32_t* lpair = nullptr;
@@ -176,6 +177,7 @@ int64_t layout_workspace(asgd_model* m, char* base) {
   m->vb = carve<int32_t>(p, n_keys + 1);
   m->hist = carve<int32_t>(p, 2 * ((int64_t)nblk << SORT_MAX_BITS));
   m->row_of = carve<int32_t>(p, (int64_t)c.max_nnz + 1);
+  m->w1_part = carve<float>(p, 2 * (int64_t)sparse_windows((int)std::max<int64_t>(n_keys, 1)) * HID);
   m->lrow = carve<int32_t>(p, (int64_t)c.max_label_nnz + 1);
   m->lkeys = carve<int32_t>(p, (int64_t)c.max_label_nnz + 1);
   m->lpair = carve<int32_t>(p, (int64_t)c.max_label_nnz + 1);
@@ -371,8 +373,8 @@ asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t s
     e = hipDeviceGetAttribute(&m->n_cu, hipDeviceAttributeMultiprocessorCount, m->device);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev, kSyncEventFlags);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_fork, kSyncEventFlags);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_dA1, kSyncEventFlags);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_join, kSyncEventFlags);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_dA1, kSyncEventFlags);
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&m->aux, hipStreamNonBlocking);
   if (e == hipSuccess) {
     m->label_plan = label_job_plan(m->bf16, L);
@@ -416,8 +418,8 @@ asgd_status asgd_model_free(asgd_model* m) {
   if (m->ws) (void)hipFree(m->ws);
   if (m->ev) (void)hipEventDestroy(m->ev);
   if (m->ev_fork) (void)hipEventDestroy(m->ev_fork);
-  if (m->ev_dA1) (void)hipEventDestroy(m->ev_dA1);
   if (m->ev_join) (void)hipEventDestroy(m->ev_join);
+  if (m->ev_dA1) (void)hipEventDestroy(m->ev_dA1);
   if (m->aux) (void)hipStreamDestroy(m->aux);
   for (auto& v : m->tev)
     for (hipEvent_t e : v) (void)hipEventDestroy(e);
@@ -505,7 +507,7 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   // The feature sort depends only on what the gather wrote: it runs on the
   // internal stream, overlapped with the output-layer forward, whose launch
   // also groups the labels for the backward (one workgroup of its own).  The
-  // b1 update, the mean loss and the W1 update follow the sort on the internal
+  // W1 update, the b1 update and the mean loss follow the sort on the internal
   // stream once dA1 exists, overlapped with the output-layer backward (they
   // touch disjoint data); the step ends when both streams have finished.
   const int32_t *sk = nullptr, *sv = nullptr;
@@ -518,11 +520,10 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   if (s) return s;
   HIP_TRY(hipEventRecord(m->ev_dA1, m->stream));
   HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_dA1, 0));
-  TIMED_ON(m, ASGD_K_HIDDEN, m->aux,
-           launch_hidden_bias(B, m->dA1, m->b1(), lr, m->loss_rows, m->loss, m->aux));
   CsrDev xd = dev(x);
   TIMED_ON(m, ASGD_K_W1_UPDATE, m->aux,
-           launch_w1_update(m->W1(), m->F, sk, sv, x->nnz, m->row_of, xd, m->dA1, lr, m->aux));
+           launch_sparse_update(m->W1(), m->F, sk, sv, x->nnz, m->row_of, xd, m->dA1, lr, B, m->b1(),
+                                m->loss_rows, m->loss, m->w1_part, m->aux));
   HIP_TRY(hipEventRecord(m->ev_join, m->aux));
   TIMED(m, ASGD_K_OUT_BWD, launch_out_bwd(m->bf16, m->W2(), m->b2(), m->L, m->H1, m->H1T, m->rows_pad_max, B,
                          m->lse, m->rw, m->lbeg, m->lpair, lr, m->n_cu, m->stream));

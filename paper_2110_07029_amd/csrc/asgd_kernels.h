@@ -79,18 +79,19 @@ hipError_t launch_out_combine(bool use_bf16, int B, int splits, const float* m_p
                               const float* W2, const float* b2, int L, const void* H1,
                               const float* A1, const CsrDev* y, float* lse, float* loss_rows,
                               float* dA1, hipStream_t st);
-// db1 = sum_i dA1[i]; b1 -= lr db1; loss = mean_i loss_rows[i].
-hipError_t launch_hidden_bias(int B, const float* dA1, float* b1, float lr, const float* loss_rows,
-                              float* loss, hipStream_t st);
 // Recompute Z per label tile, dZ = (softmax - T)/B, dW2 = dZ^T H1, db2; update W2, b2 in place.
 hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, const void* H1,
                           const void* H1T, int ld_t, int B, const float* lse, const float* rw,
                           const int32_t* lbeg, const int32_t* lpair, float lr, int n_cu,
                           hipStream_t st);
-// W1[f] -= lr * sum_{entries of f} x * dA1[row], one segment per distinct f.
-hipError_t launch_w1_update(float* W1, int F, const int32_t* skeys, const int32_t* svals,
-                            int n_feat_keys, const int32_t* row_of, const CsrDev& x,
-                            const float* dA1, float lr, hipStream_t st);
+// W1[f] -= lr * sum_{entries of f} x * dA1[row], one segment per distinct f
+// (keys sorted by feature, invalid ids >= F last); and, in the same launch,
+// db1 = sum_i dA1[i]; b1 -= lr db1; loss = mean_i loss_rows[i].
+// part: 2 * sparse_windows(n_keys) * HID floats of scratch.
+int sparse_windows(int n_keys);
+hipError_t launch_sparse_update(float* W1, int F, const int32_t* skeys, const int32_t* svals, int n_keys,
+                                const int32_t* row_of, const CsrDev& x, const float* dA1, float lr, int B,
+                                float* b1, const float* loss_rows, float* loss, float* part, hipStream_t st);
 // Distinct sorted feature ids (compaction of segment heads); count to *count_dev.
 hipError_t launch_touched(const int32_t* skeys, int n_keys, int F, int32_t* ids, int32_t* count_dev,
                           hipStream_t st);

@@ -24,6 +24,8 @@
 // fp32 operands read H1 from its L2-resident global copies.
 #include <math.h>
 
+#include <type_traits>
+
 #include "asgd_dev.h"
 #include "asgd_kernels.h"
 
@@ -295,6 +297,7 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
 // the matrix cores while the exponentials of row block rb are formed.
 // ---------------------------------------------------------------------------
 constexpr int BWP_WAVES = 4;
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 constexpr int BWP_THREADS = 64 * BWP_WAVES;
 
 __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
@@ -355,11 +358,15 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
     o.hi = lbeg[b + 1];
   };
 
-  auto process = [&](int blk, Blk& cur) {
-    const int l0 = blk * 32;
-    const int label = l0 + n;
+  const int first = blockIdx.x * BWP_WAVES + wave;
+  Blk nxt;
+  load_blk(first, nxt);
+  for (int blk = first; blk < n_blocks; blk += step) {
+    const Blk cur = nxt;
+    const int label = blk * 32 + n;
     const bool lvalid = label < L;
-    const float bb = lvalid ? cur.bias * LOG2E : -INFINITY;
+    const float bias = cur.bias;
+    const float bb = lvalid ? bias * LOG2E : -INFINITY;
     // bf16 fragments of the logits' W2 operand: 8 consecutive hidden units per
     // lane, from the two lane halves' float4s traded by v_permlane32_swap
     Fr wf[4][2];
@@ -377,13 +384,36 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
           f[j] = (bf16)__builtin_bit_cast(float, sw[0]);
           f[4 + j] = (bf16)__builtin_bit_cast(float, sw[1]);
         }
-        wf[kb][c] = f;
+        // kept in accumulation registers too (matrix instructions read their
+        // operands from either half of the register file)
+        i32x4 fi = __builtin_bit_cast(i32x4, f);
+        asm volatile("" : "+a"(fi));
+        wf[kb][c] = __builtin_bit_cast(Fr, fi);
       }
-    const bool has_targets = cur.hi > cur.lo;
+    // The fp32 master values wait for the update in accumulation registers
+    // (the register file's second half, which vector ALU code cannot use
+    // directly), leaving the vector registers to the next block's loads and
+    // to deep LDS read pipelines.
+    float keep[4][4][4];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        keep[kb][q][0] = cur.w[kb][q].x;
+        keep[kb][q][1] = cur.w[kb][q].y;
+        keep[kb][q][2] = cur.w[kb][q].z;
+        keep[kb][q][3] = cur.w[kb][q].w;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) asm volatile("" : "+a"(keep[kb][q][j]));
+      }
+    const int lo = cur.lo, hi = cur.hi;
+    load_blk(blk + step, nxt);  // the next block's rows load during this one
+
+    const bool has_targets = hi > lo;
     if (has_targets) {
       for (int k = lane; k < 32 * nrb; k += 64) mask[k] = 0u;
       __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-      for (int q = cur.lo + lane; q < cur.hi; q += 64) {
+      for (int q = lo + lane; q < hi; q += 64) {
         const int pr = lpair[q];
         const int row = pr >> 5;
         atomicOr(&mask[(pr & 31) * nrb + (row >> 5)], 1u << (row & 31));
@@ -397,56 +427,101 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
       for (int r = 0; r < 16; ++r) accw[hb][r] = 0.0f;
     float db2p = 0.0f;
 
-    // logits of row block rb plus the rows' constants (rows 8q + 4g + 0..3: one float4 each)
-    auto logits = [&](int rb) {
+    // The row-block loop, specialised on whether the block has true labels in
+    // this batch (most blocks of a wide label space have none), so that its
+    // body is straight-line code in three phases: (A) every LDS read of the
+    // iteration (H1^T fragments of row block rb, H1 rows and row constants of
+    // rb+1), (B) the logits of rb+1 on the matrix cores beside the
+    // exponentials of rb, (C) dZ of rb into dW2.  The scheduling barriers keep
+    // the reads ahead of the arithmetic that hides their latency.
+    auto rows = [&](auto targets) {
+      constexpr bool TGT = decltype(targets)::value;
+      auto read_rows = [&](int rb, bf16x8 (&hr)[4][2], f32x16& c) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 c4 = *reinterpret_cast<const float4*>(crow_s + rb * 32 + 8 * q + 4 * g);
+          c[4 * q + 0] = c4.x; c[4 * q + 1] = c4.y; c[4 * q + 2] = c4.z; c[4 * q + 3] = c4.w;
+        }
+        const bf16* t = h1s + rb * 32 * TW_LD;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int c2 = 0; c2 < 2; ++c2) hr[kb][c2] = *reinterpret_cast<const bf16x8*>(t + rbase[c2] + 32 * kb);
+      };
+      // per row: the accumulator starts at the row constant, then Z += H1 W2^T
+      auto logits = [&](const bf16x8 (&hr)[4][2], f32x16 z) {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int c = 0; c < 2; ++c) z = M::mma(hr[kb][c], wf[kb][c], z);
+        return z;
+      };
       f32x16 z;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float4 c4 = *reinterpret_cast<const float4*>(crow_s + rb * 32 + 8 * q + 4 * g);
-        z[4 * q + 0] = c4.x; z[4 * q + 1] = c4.y; z[4 * q + 2] = c4.z; z[4 * q + 3] = c4.w;
+      {
+        bf16x8 hr[4][2];
+        read_rows(0, hr, z);
+        z = logits(hr, z);
       }
-      const bf16* t = h1s + rb * 32 * TW_LD;
+      for (int rb = 0; rb < nrb; ++rb) {
+        // (A)
+        bf16x8 at[4][2];
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
+        for (int hb = 0; hb < 4; ++hb)
 #pragma unroll
-        for (int c = 0; c < 2; ++c) z = M::mma(*reinterpret_cast<const bf16x8*>(t + rbase[c] + 32 * kb), wf[kb][c], z);
-      return z;
-    };
-    f32x16 z = logits(0);
-    for (int rb = 0; rb < nrb; ++rb) {
-      // next row block's logits (the last iteration recomputes a block and drops it)
-      const f32x16 zn = logits(min(rb + 1, nrb - 1));
-      float dz[16];
+          for (int c = 0; c < 2; ++c) {
+            const bf16* o = h1s + (rb * 32 + 16 * c) * TW_LD + 32 * hb;
+            const bf16x4 lo4 = lds_read_tr16(o + cbase[0]), hi4 = lds_read_tr16(o + cbase[1]);
+            bf16x8 af;
+            af[0] = lo4[0]; af[1] = lo4[1]; af[2] = lo4[2]; af[3] = lo4[3];
+            af[4] = hi4[0]; af[5] = hi4[1]; af[6] = hi4[2]; af[7] = hi4[3];
+            at[hb][c] = af;
+          }
+        // next row block (the last iteration recomputes a block and drops it)
+        bf16x8 hr[4][2];
+        f32x16 zn;
+        read_rows(min(rb + 1, nrb - 1), hr, zn);
+        uint32_t mw = 0;
+        float tv[16];
+        if constexpr (TGT) {
+          mw = mask[n * nrb + rb];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) dz[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, bb));
-      if (has_targets) {
-        const uint32_t mw = mask[n * nrb + rb];
-        if (__any(mw != 0u)) {
+          for (int q = 0; q < 4; ++q) {
+            const float4 t4 = *reinterpret_cast<const float4*>(tw_s + rb * 32 + 8 * q + 4 * g);
+            tv[4 * q + 0] = t4.x; tv[4 * q + 1] = t4.y; tv[4 * q + 2] = t4.z; tv[4 * q + 3] = t4.w;
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        // (B)
+        zn = logits(hr, zn);
+        float dz[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dz[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, bb));
+        __builtin_amdgcn_sched_barrier(0);
+        // (C)
+        if constexpr (TGT) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int rl = 8 * (r >> 2) + 4 * g + (r & 3);
-            if ((mw >> rl) & 1u) dz[r] -= tw_s[rb * 32 + rl];
+            dz[r] -= ((mw >> rl) & 1u) ? tv[r] : 0.0f;
           }
         }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) db2p += dz[r];
+        Fr df[2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) df[c] = frag_acc<true>(dz, c);
+#pragma unroll
+        for (int hb = 0; hb < 4; ++hb)
+#pragma unroll
+          for (int c = 0; c < 2; ++c) accw[hb] = M::mma(at[hb][c], df[c], accw[hb]);
+        z = zn;
       }
-#pragma unroll
-      for (int r = 0; r < 16; ++r) db2p += dz[r];
-      Fr df[2];
-#pragma unroll
-      for (int c = 0; c < 2; ++c) df[c] = frag_acc<true>(dz, c);
-#pragma unroll
-      for (int hb = 0; hb < 4; ++hb)
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const bf16* o = h1s + (rb * 32 + 16 * c) * TW_LD + 32 * hb;
-          const bf16x4 lo4 = lds_read_tr16(o + cbase[0]), hi4 = lds_read_tr16(o + cbase[1]);
-          bf16x8 af;
-          af[0] = lo4[0]; af[1] = lo4[1]; af[2] = lo4[2]; af[3] = lo4[3];
-          af[4] = hi4[0]; af[5] = hi4[1]; af[6] = hi4[2]; af[7] = hi4[3];
-          accw[hb] = M::mma(af, df[c], accw[hb]);
-        }
-      z = zn;
-    }
+    };
+    if (has_targets)
+      rows(std::true_type{});
+    else
+      rows(std::false_type{});
+
     const float db2 = db2p + __shfl_xor(db2p, 32);
     if (lvalid) {
       float* wout = W2 + (size_t)label * HID;
@@ -454,28 +529,16 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
       for (int hb = 0; hb < 4; ++hb)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const float4 w = cur.w[hb][q];
           float4 o;
-          o.x = fmaf(-lr, accw[hb][4 * q + 0], w.x);
-          o.y = fmaf(-lr, accw[hb][4 * q + 1], w.y);
-          o.z = fmaf(-lr, accw[hb][4 * q + 2], w.z);
-          o.w = fmaf(-lr, accw[hb][4 * q + 3], w.w);
+          o.x = fmaf(-lr, accw[hb][4 * q + 0], keep[hb][q][0]);
+          o.y = fmaf(-lr, accw[hb][4 * q + 1], keep[hb][q][1]);
+          o.z = fmaf(-lr, accw[hb][4 * q + 2], keep[hb][q][2]);
+          o.w = fmaf(-lr, accw[hb][4 * q + 3], keep[hb][q][3]);
           *reinterpret_cast<float4*>(wout + 32 * hb + 8 * q + 4 * g) = o;
         }
-      if (g == 0) b2[label] = fmaf(-lr, db2, cur.bias);
+      if (g == 0) b2[label] = fmaf(-lr, db2, bias);
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    load_blk(blk + 2 * step, cur);  // this set now carries the block two steps ahead
-  };
-
-  const int first = blockIdx.x * BWP_WAVES + wave;
-  Blk s0, s1;
-  load_blk(first, s0);
-  load_blk(first + step, s1);
-  for (int blk = first; blk < n_blocks; blk += 2 * step) {
-    process(blk, s0);
-    if (blk + step >= n_blocks) break;
-    process(blk + step, s1);
   }
 }
 

@@ -205,7 +205,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
 
   if ((int)blockIdx.x >= n_fwd) {
     extern __shared__ int32_t job_lds[];
-    if (lj.in_lds)
+      if (lj.in_lds)
       wg_label_blocks<FWD_THREADS, true>(lj.lkeys, lj.m, L, lj.lrow, lj.lbeg, lj.lpair, job_lds,
                                          job_lds + ((L + 31) >> 5));
     else
@@ -558,55 +558,6 @@ hipError_t launch_out_combine(bool use_bf16, int B, int splits, const float* m_p
     hipLaunchKernelGGL(k_out_combine<false>, dim3(B), dim3(CMB_THREADS), 0, st, B, splits, m_part,
                        s_part, o_part, ld_part, W2, b2, L, (const float*)H1, A1, yy, y != nullptr,
                        invB, lse, loss_rows, dA1);
-  return hipGetLastError();
-}
-
-// db1 = sum_i dA1[i, :] and the mean loss: 256 threads = 8 row groups x 32
-// threads x 4 hidden units (16-byte loads), groups combined in a fixed order;
-// then b1 -= lr db1.  It runs beside the output-layer backward, whose waves
-// hold most of each SIMD's registers: one wave per SIMD and few registers let
-// it find room there.
-constexpr int HB_THREADS = 256;
-constexpr int HB_GROUPS = HB_THREADS / 32;  // 8
-
-__global__ __launch_bounds__(HB_THREADS) void k_hidden_bias(int B, const float* __restrict__ dA1,
-                                                            float* __restrict__ b1, float lr,
-                                                            const float* __restrict__ loss_rows,
-                                                            float* __restrict__ loss) {
-  __shared__ float red[HB_GROUPS][HID];
-  __shared__ float red_l[HB_THREADS / 64];
-  const int t = threadIdx.x, grp = t >> 5, h4 = (t & 31) * 4;
-  float4 s = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-#pragma unroll 4
-  for (int i = grp; i < B; i += HB_GROUPS) {
-    const float4 v = *reinterpret_cast<const float4*>(dA1 + (size_t)i * HID + h4);
-    s.x += v.x;
-    s.y += v.y;
-    s.z += v.z;
-    s.w += v.w;
-  }
-  *reinterpret_cast<float4*>(&red[grp][h4]) = s;
-  float ls = 0.0f;
-  for (int i = t; i < B; i += HB_THREADS) ls += loss_rows[i];
-  ls = wave_sum(ls);
-  if ((t & 63) == 0) red_l[t >> 6] = ls;
-  __syncthreads();
-  if (t < HID) {
-    float tot = red[0][t];
-#pragma unroll
-    for (int k = 1; k < HB_GROUPS; ++k) tot += red[k][t];
-    b1[t] = fmaf(-lr, tot, b1[t]);
-  }
-  if (t == 0) {
-    float l = red_l[0];
-    for (int k = 1; k < HB_THREADS / 64; ++k) l += red_l[k];
-    *loss = l / (float)B;
-  }
-}
-
-hipError_t launch_hidden_bias(int B, const float* dA1, float* b1, float lr, const float* loss_rows,
-                              float* loss, hipStream_t st) {
-  hipLaunchKernelGGL(k_hidden_bias, dim3(1), dim3(HB_THREADS), 0, st, B, dA1, b1, lr, loss_rows, loss);
   return hipGetLastError();
 }
 

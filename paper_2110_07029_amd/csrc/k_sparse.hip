@@ -1,78 +1,200 @@
 // Sparse first-layer gradient and update: dW1[f] = sum over the batch entries
 // (i, f, x) of x * dA1[i], applied only to the features present in the batch
 // (the update pass of Sec. 2.1 restricted to the rows the sparse input
-// touches).  Entries are grouped by the radix sort, so each distinct feature
-// is one contiguous segment summed by one wavefront in ascending
-// (row, position) order: deterministic, no atomics.
+// touches), plus the hidden-layer bias update and the batch's mean loss.
+// Entries are grouped by the radix sort, so each distinct feature is one
+// contiguous segment, summed in ascending (row, position) order: deterministic,
+// no atomics.
+#include <limits.h>
+
 #include "asgd_dev.h"
 #include "asgd_kernels.h"
 
 namespace asgd {
 
-constexpr int W1_UNROLL = 16;  // dA1 rows in flight per wavefront
-static_assert(64 % W1_UNROLL == 0, "readlane indices stay below 64");
+constexpr int SPU_THREADS = 256;
+constexpr int SPU_WAVES = SPU_THREADS / 64;
 
-__global__ __launch_bounds__(256) void k_w1_update(float* __restrict__ W1, int F,
-                                                   const int32_t* __restrict__ skeys,
-                                                   const int32_t* __restrict__ svals, int n_keys,
-                                                   const int32_t* __restrict__ row_of, CsrDev x,
-                                                   const float* __restrict__ dA1, float lr) {
-  const int lane = threadIdx.x & 63;
-  const int j = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (j >= n_keys) return;
-  const int f = skeys[j];
-  if (f >= F) return;                      // label keys and invalid ids
-  if (j > 0 && skeys[j - 1] == f) return;  // not the head of its segment
-  const int xbase = x.indptr[0];
-  float2* wp = reinterpret_cast<float2*>(W1 + (size_t)f * HID + 2 * lane);
-  float2 w = *wp;  // in flight while the segment is summed
-  float2 acc = make_float2(0.0f, 0.0f);
-  for (int q0 = j;; q0 += 64) {
-    const int q = q0 + lane;
-    const bool in = q < n_keys && skeys[q] == f;
-    int row = 0;
-    float xv = 0.0f;
-    if (in) {
-      const int p = svals[q];
-      row = row_of[p];
-      xv = x.values[xbase + p];
-    }
-    const int cnt = __popcll(__ballot(in));  // a segment is contiguous: lanes 0..cnt-1
-    // Lanes past the segment read dA1 row 0 and are discarded, so a partial
-    // group of 16 costs one round trip like a full one (most segments are short).
-    for (int u = 0; u < cnt; u += W1_UNROLL) {
-      int ru[W1_UNROLL];
-      float xu[W1_UNROLL];
-      float2 d[W1_UNROLL];
-#pragma unroll
-      for (int k = 0; k < W1_UNROLL; ++k) {
-        ru[k] = __builtin_amdgcn_readlane(row, u + k);
-        xu[k] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, xv), u + k));
-      }
-#pragma unroll
-      for (int k = 0; k < W1_UNROLL; ++k)
-        d[k] = *reinterpret_cast<const float2*>(dA1 + (size_t)ru[k] * HID + 2 * lane);
-#pragma unroll
-      for (int k = 0; k < W1_UNROLL; ++k) {
-        if (u + k < cnt) {
-          acc.x = fmaf(xu[k], d[k].x, acc.x);
-          acc.y = fmaf(xu[k], d[k].y, acc.y);
-        }
-      }
-    }
-    if (cnt < 64) break;
+// db1 = sum_i dA1[i]; b1 -= lr db1; loss = mean_i loss_rows[i]: one workgroup,
+// 8 groups of 32 threads x 4 hidden units, rows summed in a fixed order.
+__device__ void hidden_bias_wg(int B, const float* __restrict__ dA1, float* __restrict__ b1, float lr,
+                               const float* __restrict__ loss_rows, float* __restrict__ loss) {
+  constexpr int GROUPS = SPU_THREADS / 32;
+  __shared__ float red[GROUPS][HID];
+  __shared__ float red_l[SPU_WAVES];
+  const int t = threadIdx.x, grp = t >> 5, h4 = (t & 31) * 4;
+  float4 s = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll 8
+  for (int i = grp; i < B; i += GROUPS) {
+    const float4 v = *reinterpret_cast<const float4*>(dA1 + (size_t)i * HID + h4);
+    s.x += v.x;
+    s.y += v.y;
+    s.z += v.z;
+    s.w += v.w;
   }
-  w.x = fmaf(-lr, acc.x, w.x);
-  w.y = fmaf(-lr, acc.y, w.y);
-  *wp = w;
+  *reinterpret_cast<float4*>(&red[grp][h4]) = s;
+  float ls = 0.0f;
+  for (int i = t; i < B; i += SPU_THREADS) ls += loss_rows[i];
+  ls = wave_sum(ls);
+  if ((t & 63) == 0) red_l[t >> 6] = ls;
+  __syncthreads();
+  if (t < HID) {
+    float tot = red[0][t];
+#pragma unroll
+    for (int k = 1; k < GROUPS; ++k) tot += red[k][t];
+    b1[t] = fmaf(-lr, tot, b1[t]);
+  }
+  if (t == 0) {
+    float l = red_l[0];
+    for (int k = 1; k < SPU_WAVES; ++k) l += red_l[k];
+    *loss = l / (float)B;
+  }
 }
 
-hipError_t launch_w1_update(float* W1, int F, const int32_t* skeys, const int32_t* svals,
-                            int n_feat_keys, const int32_t* row_of, const CsrDev& x,
-                            const float* dA1, float lr, hipStream_t st) {
-  if (n_feat_keys <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_w1_update, dim3((n_feat_keys + 3) / 4), dim3(256), 0, st, W1, F, skeys, svals,
-                     n_feat_keys, row_of, x, dA1, lr);
+// Two launches, one wavefront per window of SPU_WIN consecutive sorted
+// entries.  Pieces: the wave sums each run of equal keys inside its window in
+// entry order (lanes hold hidden units 2*lane, 2*lane+1; the dA1 and W1 rows
+// of all the window's entries are loaded together, an entry's W1 row being its
+// feature's).  A segment that lies inside the window is applied to W1 at once;
+// the piece that continues a segment from the previous window goes to
+// part[2w] and the piece that starts a segment running past the window's end
+// to part[2w + 1].  Join: the wave whose window holds the head of such a
+// segment finds how many windows it spans (one lane per window), adds their
+// continuing pieces to its own in window order and applies the sum.  The
+// summation order is fixed (entry order inside a piece, window order across
+// pieces), so results do not depend on scheduling, and a long segment (a
+// feature in most rows) costs every wave at most one window of entries.  The
+// last workgroup of the first launch updates b1 and the loss.
+constexpr int SPU_WIN = 32;
+int sparse_windows(int n_keys) { return (n_keys + SPU_WIN - 1) / SPU_WIN; }
+
+__global__ __launch_bounds__(SPU_THREADS) void k_sparse_pieces(
+    float* __restrict__ W1, int F, const int32_t* __restrict__ skeys, const int32_t* __restrict__ svals,
+    int n_keys, const int32_t* __restrict__ row_of, CsrDev x, const float* __restrict__ dA1, float lr, int B,
+    float* __restrict__ b1, const float* __restrict__ loss_rows, float* __restrict__ loss,
+    float* __restrict__ part, int n_win_blocks) {
+  if ((int)blockIdx.x == n_win_blocks) {
+    hidden_bias_wg(B, dA1, b1, lr, loss_rows, loss);
+    return;
+  }
+  const int lane = threadIdx.x & 63;
+  const int win = blockIdx.x * SPU_WAVES + (threadIdx.x >> 6);
+  const int w0 = win * SPU_WIN;
+  if (w0 >= n_keys) return;
+  // lanes 0..SPU_WIN-1: the window's entries; lane SPU_WIN: the next window's first
+  const int q = w0 + lane;
+  const int key = lane <= SPU_WIN && q < n_keys ? skeys[q] : INT_MAX;  // invalid ids (>= F) sort last
+  if (__builtin_amdgcn_readfirstlane(key) >= F) return;
+  const int before = w0 > 0 ? skeys[w0 - 1] : -1;
+  const int kn = __shfl_down(key, 1);
+  const bool valid = lane < SPU_WIN && key < F;
+  // last entry of a run inside the window (at the window's end a run may go on)
+  const bool last = valid && (kn != key || lane == SPU_WIN - 1);
+  const bool runs_on = __shfl(key, SPU_WIN) == __shfl(key, SPU_WIN - 1);  // for the window's last run
+  const bool first_cont = __shfl(key, 0) == before;  // the window starts inside a segment
+  int row = 0;
+  float xv = 0.0f;
+  if (valid) {
+    const int p = svals[q];
+    row = row_of[p];
+    xv = x.values[x.indptr[0] + p];
+  }
+  const int cnt = __popcll(__ballot(valid));  // valid entries are a prefix of the window
+  const float2* dA = reinterpret_cast<const float2*>(dA1) + lane;  // row r at dA[r * HID / 2]
+  float2* Wl = reinterpret_cast<float2*>(W1) + lane;
+  float2* P = reinterpret_cast<float2*>(part) + lane;
+  int rk[SPU_WIN], fk[SPU_WIN], lk[SPU_WIN];
+  float xk[SPU_WIN];
+  float2 d[SPU_WIN], w[SPU_WIN];
+#pragma unroll
+  for (int k = 0; k < SPU_WIN; ++k) {
+    rk[k] = __builtin_amdgcn_readlane(row, k);
+    fk[k] = __builtin_amdgcn_readlane(valid ? key : 0, k);
+    lk[k] = __builtin_amdgcn_readlane((int)last, k);
+    xk[k] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, xv), k));
+  }
+  // entries past cnt read dA1 row 0 and W1 row 0 and are discarded
+#pragma unroll
+  for (int k = 0; k < SPU_WIN; ++k) {
+    d[k] = dA[(size_t)rk[k] * (HID / 2)];
+    w[k] = Wl[(size_t)fk[k] * (HID / 2)];
+  }
+  float2 acc = make_float2(0.0f, 0.0f);
+  bool in_first = first_cont;  // the current run continues a segment from the previous window
+#pragma unroll
+  for (int k = 0; k < SPU_WIN; ++k) {
+    if (k < cnt) {
+      acc.x = fmaf(xk[k], d[k].x, acc.x);
+      acc.y = fmaf(xk[k], d[k].y, acc.y);
+      if (lk[k]) {
+        if (in_first)
+          P[(size_t)(2 * win) * (HID / 2)] = acc;
+        else if (k == SPU_WIN - 1 && runs_on)
+          P[(size_t)(2 * win + 1) * (HID / 2)] = acc;
+        else
+          Wl[(size_t)fk[k] * (HID / 2)] = make_float2(fmaf(-lr, acc.x, w[k].x), fmaf(-lr, acc.y, w[k].y));
+        acc = make_float2(0.0f, 0.0f);
+        in_first = false;
+      }
+    }
+  }
+}
+
+constexpr int JOIN_BATCH = 16;  // continuing pieces loaded together
+
+__global__ __launch_bounds__(SPU_THREADS) void k_sparse_join(float* __restrict__ W1, int F,
+                                                              const int32_t* __restrict__ skeys, int n_keys,
+                                                              float lr, const float* __restrict__ part) {
+  const int lane = threadIdx.x & 63;
+  const int win = blockIdx.x * SPU_WAVES + (threadIdx.x >> 6);
+  const int w0 = win * SPU_WIN;
+  // this window's last entry starts or continues a segment that runs past it ...
+  if (w0 + SPU_WIN >= n_keys) return;
+  const int f = skeys[w0 + SPU_WIN - 1];
+  if (f >= F || skeys[w0 + SPU_WIN] != f) return;
+  // ... and the segment's head lies in this window (else an earlier wave joins it)
+  if (skeys[w0] == f && w0 > 0 && skeys[w0 - 1] == f) return;
+  // windows win+1 .. win+m hold the rest: window v is followed by another piece
+  // when it is all f and the next window starts with f (one lane per window)
+  int m = 0;
+  for (;;) {
+    const int v1 = (win + 2 + m + lane) * SPU_WIN;  // first entry after window win+1+m+lane
+    const bool more = v1 < n_keys && skeys[v1] == f && skeys[v1 - 1] == f;
+    const uint64_t stop = __ballot(!more);
+    if (stop) {
+      m += __builtin_ctzll(stop) + 1;
+      break;
+    }
+    m += 64;
+  }
+  const float2* P = reinterpret_cast<const float2*>(part) + lane;
+  float2 acc = P[(size_t)(2 * win + 1) * (HID / 2)];
+  for (int v0 = 0; v0 < m; v0 += JOIN_BATCH) {
+    float2 c[JOIN_BATCH];
+#pragma unroll
+    for (int k = 0; k < JOIN_BATCH; ++k)
+      c[k] = P[(size_t)(2 * (win + 1 + min(v0 + k, m - 1))) * (HID / 2)];
+#pragma unroll
+    for (int k = 0; k < JOIN_BATCH; ++k)
+      if (v0 + k < m) {
+        acc.x += c[k].x;
+        acc.y += c[k].y;
+      }
+  }
+  float2* wp = reinterpret_cast<float2*>(W1 + (size_t)f * HID) + lane;
+  const float2 w = *wp;
+  *wp = make_float2(fmaf(-lr, acc.x, w.x), fmaf(-lr, acc.y, w.y));
+}
+
+hipError_t launch_sparse_update(float* W1, int F, const int32_t* skeys, const int32_t* svals, int n_keys,
+                                const int32_t* row_of, const CsrDev& x, const float* dA1, float lr, int B,
+                                float* b1, const float* loss_rows, float* loss, float* part, hipStream_t st) {
+  const int nwin = n_keys > 0 ? sparse_windows(n_keys) : 0;
+  const int nwb = (nwin + SPU_WAVES - 1) / SPU_WAVES;
+  hipLaunchKernelGGL(k_sparse_pieces, dim3(nwb + 1), dim3(SPU_THREADS), 0, st, W1, F, skeys, svals, n_keys,
+                     row_of, x, dA1, lr, B, b1, loss_rows, loss, part, nwb);
+  if (nwin > 1)
+    hipLaunchKernelGGL(k_sparse_join, dim3(nwb), dim3(SPU_THREADS), 0, st, W1, F, skeys, n_keys, lr, part);
   return hipGetLastError();
 }
 

@@ -172,6 +172,35 @@ def test_step_with_empty_feature_row_and_single_label_rows():
         s.free()
 
 
+def test_step_w1_segments_across_windows():
+    """The sparse W1 update sums each feature's entries window by window (32
+    sorted entries per wavefront) and joins the pieces of features that cross
+    windows: one feature in every row (a segment of B entries), features with
+    tens of entries, and many features seen once, at a batch above 256 rows."""
+    flush("step: W1 segments across windows, B=520")
+    w = synth.TINY
+    rng = np.random.default_rng(11)
+    B = 520
+    ind, val, ip = [], [], [0]
+    lab, lip = [], [0]
+    for i in range(B):
+        f = {0, 1 + i % 7, 100 + i % 40} | set(rng.choice(np.arange(1000, w.n_features), 3, replace=False).tolist())
+        f = np.array(sorted(f), np.int32)
+        ind.append(f)
+        val.append(rng.uniform(0.1, 1.0, len(f)).astype(np.float32))
+        ip.append(ip[-1] + len(f))
+        lb = np.sort(rng.choice(w.n_labels, int(rng.integers(1, 4)), replace=False)).astype(np.int32)
+        lab.append(lb)
+        lip.append(lip[-1] + len(lb))
+    x = synth.CSR(np.array(ip), np.concatenate(ind), np.concatenate(val), w.n_features)
+    y = synth.CSR(np.array(lip), np.concatenate(lab), None, w.n_labels)
+    s = Setup(w, 0, B, ds=synth.Dataset(w, x, y))
+    try:
+        _step_parity(s, 0, B, 0.1, RTOL_FP32, "fp32")
+    finally:
+        s.free()
+
+
 def test_epoch_free_running_fp32():
     flush("epoch: tiny fp32, 16 steps free running")
     w = synth.TINY
