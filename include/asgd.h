@@ -60,7 +60,7 @@ typedef enum asgd_status {
 #define ASGD_VALIDATE 0x1u /* check CSR content on the device and synchronize each step */
 
 typedef struct asgd_config {
-  int32_t n_features;    /* F >= 1 */
+  int32_t n_features;    /* F in [1, 2^22) */
   int32_t n_labels;      /* L in [1, 2^22) */
   int32_t hidden;        /* H; must be 128 */
   int32_t max_batch;     /* largest B any call will use (memory pool sized for it, Sec. 4) */

@@ -343,6 +343,8 @@ asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t s
     return fail(ASGD_ERANGE, "n_features + n_labels must be < 2^30");
   if (cfg->n_labels >= (1 << 22))  // W2 is read through 32-bit buffer offsets
     return fail(ASGD_ERANGE, "n_labels must be < 2^22");
+  if (cfg->n_features >= (1 << 22))  // so are the rows of W1 in its sparse update
+    return fail(ASGD_ERANGE, "n_features must be < 2^22");
   if (cfg->max_batch < 1 || cfg->max_batch > kMaxBatch)
     return fail(ASGD_ERANGE, "max_batch must be in [1, 2048]");
   if (cfg->max_nnz < 0 || cfg->max_label_nnz < 0)

@@ -66,6 +66,7 @@ __device__ void hidden_bias_wg(int B, const float* __restrict__ dA1, float* __re
 // feature in most rows) costs every wave at most one window of entries.  The
 // last workgroup of the first launch updates b1 and the loss.
 constexpr int SPU_WIN = 32;
+constexpr int SPU_BATCH = 16;  // entries whose dA1 and W1 rows are loaded together
 int sparse_windows(int n_keys) { return (n_keys + SPU_WIN - 1) / SPU_WIN; }
 
 __global__ __launch_bounds__(SPU_THREADS) void k_sparse_pieces(
@@ -100,41 +101,52 @@ __global__ __launch_bounds__(SPU_THREADS) void k_sparse_pieces(
     xv = x.values[x.indptr[0] + p];
   }
   const int cnt = __popcll(__ballot(valid));  // valid entries are a prefix of the window
-  const float2* dA = reinterpret_cast<const float2*>(dA1) + lane;  // row r at dA[r * HID / 2]
+  // dA1 and W1 rows through buffer resources: the row offset is a scalar, the
+  // lane's 8 bytes a fixed vector offset, so a load needs no address registers
+  const __amdgpu_buffer_rsrc_t rd =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(dA1), (short)0, B * HID * 4, BUF_RSRC_WORD3);
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(W1, (short)0, F * HID * 4, BUF_RSRC_WORD3);
+  const int voff = lane * 8;
   float2* Wl = reinterpret_cast<float2*>(W1) + lane;
   float2* P = reinterpret_cast<float2*>(part) + lane;
-  int rk[SPU_WIN], fk[SPU_WIN], lk[SPU_WIN];
-  float xk[SPU_WIN];
-  float2 d[SPU_WIN], w[SPU_WIN];
-#pragma unroll
-  for (int k = 0; k < SPU_WIN; ++k) {
-    rk[k] = __builtin_amdgcn_readlane(row, k);
-    fk[k] = __builtin_amdgcn_readlane(valid ? key : 0, k);
-    lk[k] = __builtin_amdgcn_readlane((int)last, k);
-    xk[k] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, xv), k));
-  }
-  // entries past cnt read dA1 row 0 and W1 row 0 and are discarded
-#pragma unroll
-  for (int k = 0; k < SPU_WIN; ++k) {
-    d[k] = dA[(size_t)rk[k] * (HID / 2)];
-    w[k] = Wl[(size_t)fk[k] * (HID / 2)];
-  }
   float2 acc = make_float2(0.0f, 0.0f);
   bool in_first = first_cont;  // the current run continues a segment from the previous window
+  // two batches of SPU_BATCH entries: few enough registers for the kernel to
+  // share a SIMD with the output-layer backward it overlaps
+#pragma unroll 1
+  for (int u = 0; u < cnt; u += SPU_BATCH) {
+    int rk[SPU_BATCH], fk[SPU_BATCH], lk[SPU_BATCH];
+    float xk[SPU_BATCH];
+    float2 d[SPU_BATCH], w[SPU_BATCH];
 #pragma unroll
-  for (int k = 0; k < SPU_WIN; ++k) {
-    if (k < cnt) {
-      acc.x = fmaf(xk[k], d[k].x, acc.x);
-      acc.y = fmaf(xk[k], d[k].y, acc.y);
-      if (lk[k]) {
-        if (in_first)
-          P[(size_t)(2 * win) * (HID / 2)] = acc;
-        else if (k == SPU_WIN - 1 && runs_on)
-          P[(size_t)(2 * win + 1) * (HID / 2)] = acc;
-        else
-          Wl[(size_t)fk[k] * (HID / 2)] = make_float2(fmaf(-lr, acc.x, w[k].x), fmaf(-lr, acc.y, w[k].y));
-        acc = make_float2(0.0f, 0.0f);
-        in_first = false;
+    for (int k = 0; k < SPU_BATCH; ++k) {
+      rk[k] = __builtin_amdgcn_readlane(row, u + k);
+      fk[k] = __builtin_amdgcn_readlane(valid ? key : 0, u + k);
+      lk[k] = __builtin_amdgcn_readlane((int)last, u + k);
+      xk[k] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, xv), u + k));
+    }
+    // entries past cnt read dA1 row 0 and W1 row 0 and are discarded
+#pragma unroll
+    for (int k = 0; k < SPU_BATCH; ++k) {
+      d[k] = __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(rd, voff, rk[k] * (HID * 4), 0));
+      w[k] = __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(rw, voff, fk[k] * (HID * 4), 0));
+    }
+#pragma unroll
+    for (int k = 0; k < SPU_BATCH; ++k) {
+      const int e = u + k;
+      if (e < cnt) {
+        acc.x = fmaf(xk[k], d[k].x, acc.x);
+        acc.y = fmaf(xk[k], d[k].y, acc.y);
+        if (lk[k]) {
+          if (in_first)
+            P[(size_t)(2 * win) * (HID / 2)] = acc;
+          else if (e == SPU_WIN - 1 && runs_on)
+            P[(size_t)(2 * win + 1) * (HID / 2)] = acc;
+          else
+            Wl[(size_t)fk[k] * (HID / 2)] = make_float2(fmaf(-lr, acc.x, w[k].x), fmaf(-lr, acc.y, w[k].y));
+          acc = make_float2(0.0f, 0.0f);
+          in_first = false;
+        }
       }
     }
   }
