@@ -290,14 +290,18 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
 
 // ---------------------------------------------------------------------------
 // Staged batches (B <= 256, bf16) with the next label block's W2 in flight:
-// 4 wavefronts, one per SIMD, each with the full register file.  A wave keeps
-// two blocks' fp32 W2 rows in registers with fixed roles (the block loop is
-// unrolled by two): while it works on one block the other set is loading the
-// block two steps ahead.  Inside a block the logits of row block rb+1 go to
-// the matrix cores while the exponentials of row block rb are formed.
+// 4 wavefronts, one per SIMD, each with the full register file.  While a wave
+// works on one block of 32 labels, the next block's fp32 rows load into
+// registers as whole 512-byte rows (the access pattern of a plain streaming
+// update); at the block's start they go through the wave's LDS staging tile,
+// from which the products' operand layout is read, and the updated rows leave
+// the same way.  Inside a block the logits of row block rb+1 go to the matrix
+// cores while the exponentials of row block rb are formed.
 // ---------------------------------------------------------------------------
 constexpr int BWP_WAVES = 4;
+constexpr int BWP_SLD = 132;  // staging tile row stride (floats): conflict-free both ways
 typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int BWP_THREADS = 64 * BWP_WAVES;
 
 __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
@@ -320,6 +324,9 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
   float* tw_s = reinterpret_cast<float*>(sp);
   sp += bpad * sizeof(float);
   uint32_t* mask = reinterpret_cast<uint32_t*>(sp) + wave * 32 * nrb;
+  sp += BWP_WAVES * 32 * nrb * sizeof(uint32_t);
+  // the wave's W2 staging tile: 32 label rows of 128 fp32, row stride BWP_SLD
+  float* stage = reinterpret_cast<float*>(sp) + wave * 32 * BWP_SLD;
 
   for (int e = tid; e < bpad * 16; e += BWP_THREADS) {
     const int r = e >> 4, c = e & 15;
@@ -338,76 +345,68 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
 
   const int n_blocks = (L + 31) >> 5;
   const int step = gridDim.x * BWP_WAVES;
-  // a block's W2 rows (fp32 master, hidden 32kb + 8q + 4g + 0..3 per lane; labels
-  // past L read the last row and are never stored), its bias and pair range
-  struct Blk {
-    float4 w[4][4];
-    float bias;
-    int lo, hi;
-  };
-  auto load_blk = [&](int b, Blk& o) {
+  // A block's 32 W2 rows move between HBM and the wave's staging tile whole:
+  // load or store k covers rows 2k and 2k+1, 16 bytes per lane, so every
+  // instruction reads or writes two full 512-byte rows.  The operand layout of
+  // the products (lane (g, n): row n, hidden 32kb + 8q + 4g + 0..3) is read
+  // from and written to the tile.  W2 and b2 are raw buffers: the block's
+  // offset is a scalar, the lane's a fixed vector offset plus a constant per
+  // row pair; rows past L read zeros and their stores are dropped by the
+  // buffer's bounds check.  Also loaded: the block's bias (lane n: label
+  // 32 blk + n) and pair range.
+  const int crow_l = lane >> 5, ccol = 4 * (lane & 31);  // this lane's row pair slot and column
+  const __amdgpu_buffer_rsrc_t w2r = __builtin_amdgcn_make_buffer_rsrc(W2, (short)0, L * HID * 4, BUF_RSRC_WORD3);
+  const __amdgpu_buffer_rsrc_t b2r = __builtin_amdgcn_make_buffer_rsrc(b2, (short)0, L * 4, BUF_RSRC_WORD3);
+  const int voff = (crow_l * HID + ccol) * 4;
+  float4 nv[16];
+  float nbias;
+  int nlo, nhi;
+  auto load_blk = [&](int b) {
     b = min(b, n_blocks - 1);
-    const int label = min(b * 32 + n, L - 1);
-    const float* wrow = W2 + (size_t)label * HID;
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) o.w[kb][q] = *reinterpret_cast<const float4*>(wrow + 32 * kb + 8 * q + 4 * g);
-    o.bias = b2[label];
-    o.lo = lbeg[b];
-    o.hi = lbeg[b + 1];
+    for (int k = 0; k < 16; ++k)
+      nv[k] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(w2r, voff + k * 2 * HID * 4,
+                                                                                 b * 32 * HID * 4, 0));
+    nbias = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(b2r, n * 4, b * 32 * 4, 0));
+    nlo = lbeg[b];
+    nhi = lbeg[b + 1];
+  };
+  auto stage_frag = [&](int kb, int q) -> float4& {
+    return *reinterpret_cast<float4*>(stage + n * BWP_SLD + 32 * kb + 8 * q + 4 * g);
   };
 
   const int first = blockIdx.x * BWP_WAVES + wave;
-  Blk nxt;
-  load_blk(first, nxt);
+  load_blk(first);
   for (int blk = first; blk < n_blocks; blk += step) {
-    const Blk cur = nxt;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) *reinterpret_cast<float4*>(stage + (2 * k + crow_l) * BWP_SLD + ccol) = nv[k];
+    const float bias = nbias;
+    const int lo = nlo, hi = nhi;
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    load_blk(blk + step);  // the next block's rows load during this one
     const int label = blk * 32 + n;
     const bool lvalid = label < L;
-    const float bias = cur.bias;
     const float bb = lvalid ? bias * LOG2E : -INFINITY;
     // bf16 fragments of the logits' W2 operand: 8 consecutive hidden units per
-    // lane, from the two lane halves' float4s traded by v_permlane32_swap
+    // lane (32kb + 16c + 8g .. + 7), read from the staging tile; kept in
+    // accumulation registers (matrix instructions read their operands from
+    // either half of the register file), which leaves the vector registers to
+    // the next block's loads and to deep LDS read pipelines
     Fr wf[4][2];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const float4 a4 = cur.w[kb][2 * c], b4 = cur.w[kb][2 * c + 1];
-        const float av[4] = {a4.x, a4.y, a4.z, a4.w}, bv[4] = {b4.x, b4.y, b4.z, b4.w};
+        const float* src = stage + n * BWP_SLD + 32 * kb + 16 * c + 8 * g;
+        const float4 a4 = *reinterpret_cast<const float4*>(src);
+        const float4 b4 = *reinterpret_cast<const float4*>(src + 4);
         Fr f;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const auto sw = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, av[j]),
-                                                           __builtin_bit_cast(unsigned, bv[j]), false, false);
-          f[j] = (bf16)__builtin_bit_cast(float, sw[0]);
-          f[4 + j] = (bf16)__builtin_bit_cast(float, sw[1]);
-        }
-        // kept in accumulation registers too (matrix instructions read their
-        // operands from either half of the register file)
+        f[0] = (bf16)a4.x; f[1] = (bf16)a4.y; f[2] = (bf16)a4.z; f[3] = (bf16)a4.w;
+        f[4] = (bf16)b4.x; f[5] = (bf16)b4.y; f[6] = (bf16)b4.z; f[7] = (bf16)b4.w;
         i32x4 fi = __builtin_bit_cast(i32x4, f);
         asm volatile("" : "+a"(fi));
         wf[kb][c] = __builtin_bit_cast(Fr, fi);
       }
-    // The fp32 master values wait for the update in accumulation registers
-    // (the register file's second half, which vector ALU code cannot use
-    // directly), leaving the vector registers to the next block's loads and
-    // to deep LDS read pipelines.
-    float keep[4][4][4];
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        keep[kb][q][0] = cur.w[kb][q].x;
-        keep[kb][q][1] = cur.w[kb][q].y;
-        keep[kb][q][2] = cur.w[kb][q].z;
-        keep[kb][q][3] = cur.w[kb][q].w;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) asm volatile("" : "+a"(keep[kb][q][j]));
-      }
-    const int lo = cur.lo, hi = cur.hi;
-    load_blk(blk + step, nxt);  // the next block's rows load during this one
 
     const bool has_targets = hi > lo;
     if (has_targets) {
@@ -523,21 +522,28 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
       rows(std::false_type{});
 
     const float db2 = db2p + __shfl_xor(db2p, 32);
-    if (lvalid) {
-      float* wout = W2 + (size_t)label * HID;
+    // W2 -= lr dW2 in the staging tile (the lane's own operand-layout slots),
+    // then out as whole rows
 #pragma unroll
-      for (int hb = 0; hb < 4; ++hb)
+    for (int hb = 0; hb < 4; ++hb)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          float4 o;
-          o.x = fmaf(-lr, accw[hb][4 * q + 0], keep[hb][q][0]);
-          o.y = fmaf(-lr, accw[hb][4 * q + 1], keep[hb][q][1]);
-          o.z = fmaf(-lr, accw[hb][4 * q + 2], keep[hb][q][2]);
-          o.w = fmaf(-lr, accw[hb][4 * q + 3], keep[hb][q][3]);
-          *reinterpret_cast<float4*>(wout + 32 * hb + 8 * q + 4 * g) = o;
-        }
-      if (g == 0) b2[label] = fmaf(-lr, db2, bias);
+      for (int q = 0; q < 4; ++q) {
+        float4& w = stage_frag(hb, q);
+        float4 o;
+        o.x = fmaf(-lr, accw[hb][4 * q + 0], w.x);
+        o.y = fmaf(-lr, accw[hb][4 * q + 1], w.y);
+        o.z = fmaf(-lr, accw[hb][4 * q + 2], w.z);
+        o.w = fmaf(-lr, accw[hb][4 * q + 3], w.w);
+        w = o;
+      }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const float4 o = *reinterpret_cast<const float4*>(stage + (2 * k + crow_l) * BWP_SLD + ccol);
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o), w2r, voff + k * 2 * HID * 4,
+                                             blk * 32 * HID * 4, 0);
     }
+    if (lvalid && g == 0) b2[label] = fmaf(-lr, db2, bias);
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   }
 }
@@ -584,7 +590,8 @@ hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, const void
       attr_done = true;
     }
     const size_t shp = (size_t)BWD_CHUNK * TW_LD * 2 + (size_t)2 * nrb * 32 * sizeof(float) +
-                       (size_t)BWP_WAVES * 32 * nrb * sizeof(uint32_t);
+                       (size_t)BWP_WAVES * 32 * nrb * sizeof(uint32_t) +
+                       (size_t)BWP_WAVES * 32 * BWP_SLD * sizeof(float);
     int gp = (n_blocks + BWP_WAVES - 1) / BWP_WAVES;
     if (gp > n_cu) gp = n_cu;
     hipLaunchKernelGGL(k_out_bwd_prefetch, dim3(gp), dim3(BWP_THREADS), shp, st, W2, b2, L,
