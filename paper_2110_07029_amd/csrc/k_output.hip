@@ -180,7 +180,16 @@ __device__ __forceinline__ typename Mma<BF16>::frag tile_frag_wt(const typename 
 // ---------------------------------------------------------------------------
 // Forward, training: per (split, row) partial max, sum of exponentials and O.
 // ---------------------------------------------------------------------------
-constexpr int FWD_NBUF = 3;  // LDS ring of W2 tiles
+// LDS ring of W2 tiles: one workgroup barrier per FwdRing::P tiles.  Between
+// two barriers the waves read tiles t .. t+P and store t+P+1 .. t+2P, so a ring
+// of 2P+1 tiles keeps what is read and what is written apart.  The bf16 tile
+// (10 KB) allows P = 2; the fp32 operands (two 17-18 KB layouts per tile) keep
+// P = 1.
+template <bool BF16>
+struct FwdRing {
+  static constexpr int P = BF16 ? 2 : 1;
+  static constexpr int N = 2 * P + 1;
+};
 
 // With a label job, workgroup n_fwd of the launch (dispatched last, on a CU
 // the forward leaves free) groups the batch's labels for the backward: it
@@ -199,9 +208,10 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
   constexpr int RB = FwdShape<BF16>::RB;
   constexpr int NCH = 32 / M::KC;
   static_assert(FwdShape<BF16>::NB == 1, "one 32-row block per wave");
-  __shared__ __attribute__((aligned(16))) E wr[FWD_NBUF][tile_elems<BF16>()];
-  __shared__ __attribute__((aligned(16))) E wt[FWD_NBUF][tileT_elems<BF16>()];
-  __shared__ __attribute__((aligned(16))) float bt[FWD_NBUF][OUT_TILE];
+  constexpr int P = FwdRing<BF16>::P, NRING = FwdRing<BF16>::N;
+  __shared__ __attribute__((aligned(16))) E wr[NRING][tile_elems<BF16>()];
+  __shared__ __attribute__((aligned(16))) E wt[NRING][tileT_elems<BF16>()];
+  __shared__ __attribute__((aligned(16))) float bt[NRING][OUT_TILE];
 
   if ((int)blockIdx.x >= n_fwd) {
     extern __shared__ int32_t job_lds[];
@@ -267,18 +277,22 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
   // Software pipeline over a ring of three LDS tiles and two register tiles.
   // In the iteration of tile t: the logits of tile t+1 go to the matrix cores
   // while the softmax numerators of tile t are formed; then O^T += W2_t^T P_t^T
-  // while tile t+2 (loaded into registers two iterations earlier) is converted
-  // into the ring and tile t+4 is loaded in its place.  Tile indices are
-  // clamped to the split's last tile, so every load, store and product is
-  // unconditional (a clamped copy is never consumed).  Every split has at
-  // least one tile.
+  // while tile t+P+1 (loaded into registers two iterations earlier) is
+  // converted into the ring and tile t+P+3 is loaded in its place; a barrier
+  // closes every P-th iteration.  Tile u lives in ring slot (u - t_begin) mod
+  // NRING.  Tile indices are clamped to the split's last tile, so every load,
+  // store and product is unconditional (a clamped copy is never consumed).
+  // Every split has at least one tile.
   TileRegs tr0, tr1;
-  tile_load(src, t_begin, tr0);
-  tile_store<BF16, true>(tr0, L, t_begin, wr[0], wt[0], bt[0]);
-  tile_load(src, min(t_begin + 1, t_last), tr1);
-  tile_store<BF16, true>(tr1, L, min(t_begin + 1, t_last), wr[1], wt[1], bt[1]);
-  tile_load(src, min(t_begin + 2, t_last), tr0);
-  tile_load(src, min(t_begin + 3, t_last), tr1);
+  auto slot = [&](int u) { return (u - t_begin) % NRING; };
+#pragma unroll
+  for (int u = 0; u <= P; ++u) {
+    const int tu = min(t_begin + u, t_last);
+    tile_load(src, tu, tr0);
+    tile_store<BF16, true>(tr0, L, tu, wr[u], wt[u], bt[u]);
+  }
+  tile_load(src, min(t_begin + P + 1, t_last), tr0);
+  tile_load(src, min(t_begin + P + 2, t_last), tr1);
   __syncthreads();
   f32x16 z = z_tile(0);
 
@@ -287,10 +301,8 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
   // by more than LAZY (so p <= 2^LAZY); the final normalisation uses the same
   // reference, so the result is exact up to rounding.
   constexpr float LAZY = 8.0f;
-  int b0 = 0;
   auto iteration = [&](int t, TileRegs& tr) {
-    const int b1 = b0 == FWD_NBUF - 1 ? 0 : b0 + 1;
-    const int b2i = b1 == FWD_NBUF - 1 ? 0 : b1 + 1;
+    const int b0 = slot(t), b1 = slot(t + 1), bst = slot(t + P + 1);
     // Operands of this iteration's two products, read from LDS first so that
     // their latency is covered by the max / rescale work below: A of the next
     // tile's logits (W2 rows, with the biases as the accumulator's start) and
@@ -362,11 +374,10 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
       for (int c = 0; c < NCH; ++c)
         acc_o[hb] = M::mma(BF16 ? oa[hb][c % PRE] : tile_frag_wt<BF16>(wr[b0], wt[b0], cbase, hb, c, lane),
                            pf[c], acc_o[hb]);
-    tile_store<BF16, true>(tr, L, min(t + 2, t_last), wr[b2i], wt[b2i], bt[b2i]);
-    tile_load(src, min(t + 4, t_last), tr);
-    __syncthreads();
+    tile_store<BF16, true>(tr, L, min(t + P + 1, t_last), wr[bst], wt[bst], bt[bst]);
+    tile_load(src, min(t + P + 3, t_last), tr);
+    if ((t - t_begin) % P == P - 1) __syncthreads();
     z = zn;
-    b0 = b1;
   };
   for (int t = t_begin; t < t_end; t += 2) {
     iteration(t, tr0);
