@@ -101,6 +101,36 @@ def kernel_model(w, B, nnz, lnnz, uniq, splits):
     }
 
 
+def measured_peaks(n_floats: int, stream):
+    """What this GPU sustains, measured in the same run beside the datasheet peaks:
+    an in-place streaming update of n_floats fp32 (read and write the same
+    addresses, like the backward's W2 update), and a large bf16 GEMM by the
+    vendor library (a practical matrix-core rate)."""
+    import torch
+    a = torch.ones(n_floats, dtype=torch.float32, device="cuda")
+    x = torch.randn(8192, 8192, dtype=torch.bfloat16, device="cuda")
+    y = torch.randn(8192, 8192, dtype=torch.bfloat16, device="cuda")
+
+    def timed(fn, reps):
+        for _ in range(3):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e-3 / reps
+
+    t_up = timed(lambda: a.mul_(1.0000001), 20)
+    t_mm = timed(lambda: torch.matmul(x, y), 10)
+    del a, x, y
+    return {"hbm_inplace_update_GBs": round(8.0 * n_floats / t_up / 1e9, 1),
+            "bf16_gemm_TFLOPs": round(2.0 * 8192 ** 3 / t_mm / 1e12, 1),
+            "how": "torch mul_ in place over a W2-sized fp32 tensor; torch.matmul 8192^3 bf16"}
+
+
 def measure_merge(w, n_rep, reps_iters, stream):
     """Normalized merge of n_rep replicas of the workload's model (with momentum and
     broadcast, as in the elastic configuration), timed with the library's events."""
@@ -342,6 +372,9 @@ def main():
                 "traffic": None if traffic is None else round(traffic / 1e9, 4)}
     if traffic is not None:
         roofline["traffic_unit"] = "GB per launch"
+    meas = measured_peaks(w.n_labels * H, stream)
+    roofline["measured_peaks"] = meas
+    roofline["frac_of_measured"] = round(d["GB/s"] / meas["hbm_inplace_update_GBs"], 4)
     cpu = None
     if args.cpu_seconds > 0:
         log(f"oracle CPU baseline, ~{args.cpu_seconds:.0f} s budget")
