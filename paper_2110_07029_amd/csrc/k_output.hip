@@ -451,9 +451,11 @@ hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2,
 // ---------------------------------------------------------------------------
 // Per row: merge the splits, log-sum-exp, loss, dA1.  512 threads = 16 split
 // groups x 32 threads x 4 hidden units (16-byte loads) for the
-// softmax-weighted sums, 8 wavefronts x the row's labels for the target terms;
-// every partial is combined in a fixed order, so the result does not depend
-// on scheduling.
+// softmax-weighted sums, 8 wavefronts x the row's labels for the target terms.
+// Each group merges its splits online against its own running maximum (so
+// its loads need not wait for the row's maximum), then the 16 groups are
+// rescaled to the row's maximum; every partial is combined in a fixed order,
+// so the result does not depend on scheduling.
 // ---------------------------------------------------------------------------
 constexpr int CMB_THREADS = 512;
 constexpr int CMB_GROUPS = CMB_THREADS / 32;  // 16
@@ -468,36 +470,35 @@ __global__ __launch_bounds__(CMB_THREADS) void k_out_combine(
     float* __restrict__ loss_rows, float* __restrict__ dA1) {
   __shared__ float red_o[CMB_GROUPS][HID];
   __shared__ float red_s[CMB_GROUPS];
-  __shared__ float red_m[CMB_WAVES];
+  __shared__ float red_m[CMB_GROUPS];
   __shared__ float red_t[CMB_WAVES][HID];
   __shared__ float red_z[CMB_WAVES];
   const int i = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int grp = t >> 5, h4 = (t & 31) * 4;
 
-  float mloc = -INFINITY;
-  for (int s = t; s < splits; s += CMB_THREADS) mloc = fmaxf(mloc, m_part[(size_t)s * ld_part + i]);
-  mloc = wave_max(mloc);
-  if (lane == 0) red_m[w] = mloc;
-  __syncthreads();
-  float M = red_m[0];
-#pragma unroll
-  for (int k = 1; k < CMB_WAVES; ++k) M = fmaxf(M, red_m[k]);
-
-  float St = 0.0f;
+  float mg = -INFINITY, St = 0.0f;
   float4 O = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
 #pragma unroll 8
   for (int s = grp; s < splits; s += CMB_GROUPS) {
     const size_t r = (size_t)s * ld_part + i;
-    const float e = exp_fast(m_part[r] - M);
-    St = fmaf(e, s_part[r], St);
+    const float ms = m_part[r];
+    const float ss = s_part[r];
     const float4 o = *reinterpret_cast<const float4*>(o_part + r * HID + h4);
-    O.x = fmaf(e, o.x, O.x);
-    O.y = fmaf(e, o.y, O.y);
-    O.z = fmaf(e, o.z, O.z);
-    O.w = fmaf(e, o.w, O.w);
+    // (no split has -inf: each holds at least one label of finite bias)
+    const float mn = fmaxf(mg, ms);
+    const float a = exp_fast(mg - mn), e = exp_fast(ms - mn);
+    St = fmaf(e, ss, St * a);
+    O.x = fmaf(e, o.x, O.x * a);
+    O.y = fmaf(e, o.y, O.y * a);
+    O.z = fmaf(e, o.z, O.z * a);
+    O.w = fmaf(e, o.w, O.w * a);
+    mg = mn;
   }
   *reinterpret_cast<float4*>(&red_o[grp][h4]) = O;
-  if ((t & 31) == 0) red_s[grp] = St;
+  if ((t & 31) == 0) {
+    red_s[grp] = St;
+    red_m[grp] = mg;
+  }
 
   // target terms: wave w takes labels q = w, w + 8, ... of row i; lane owns hidden 2l, 2l+1
   float tw0 = 0.0f, tw1 = 0.0f, zw = 0.0f;
@@ -531,11 +532,15 @@ __global__ __launch_bounds__(CMB_THREADS) void k_out_combine(
   }
   __syncthreads();
   if (t < HID) {
-    float Ot = red_o[0][t], Stot = red_s[0];
+    float M = red_m[0];
 #pragma unroll
-    for (int k = 1; k < CMB_GROUPS; ++k) {
-      Ot += red_o[k][t];
-      Stot += red_s[k];
+    for (int k = 1; k < CMB_GROUPS; ++k) M = fmaxf(M, red_m[k]);
+    float Ot = 0.0f, Stot = 0.0f;
+#pragma unroll
+    for (int k = 0; k < CMB_GROUPS; ++k) {
+      const float e = red_m[k] == -INFINITY ? 0.0f : exp_fast(red_m[k] - M);  // groups without a split
+      Ot = fmaf(e, red_o[k][t], Ot);
+      Stot = fmaf(e, red_s[k], Stot);
     }
     const float lse = M + logf(Stot);
     if (t == 0) lse_out[i] = lse;
