@@ -10,18 +10,20 @@
 // lane itself loaded (the accumulator-compatible K order makes the lane that
 // loads a weight the lane that owns its gradient).
 //
-// Workgroups are persistent, 8 wavefronts (2 per SIMD).  With bf16 operands
-// H1 is staged in LDS once, in the conflict-free tile layout of the forward
-// (row stride 160, 16-byte chunks permuted by the row): the logits read H1
-// rows with 16-byte reads, the dW2 product reads H1^T with transposed reads
-// (ds_read_b64_tr_b16) from the same copy.
-//   staged  (B <= 256): the whole batch once per workgroup; each wave then
-//           walks its own sequence of label blocks with no barrier inside
-//           the loop, so loads of one wave overlap the matrix work of another;
-//   chunked (B > 256):  the workgroup takes 8 label blocks at a time and
-//           streams the batch through LDS in 256-row chunks, the dW2
-//           accumulators staying in registers across chunks.
-// fp32 operands read H1 from its L2-resident global copies.
+// With bf16 operands H1 is staged in LDS, in the conflict-free tile layout of
+// the forward (row stride 160, 16-byte chunks permuted by the row): the logits
+// read H1 rows with 16-byte reads, the dW2 product reads H1^T with transposed
+// reads (ds_read_b64_tr_b16) from the same copy.  Three kernels, all with
+// persistent workgroups:
+//   k_out_bwd_prefetch (B <= 256, bf16): 4 wavefronts, the whole batch staged
+//           once per workgroup; each wave walks its own label blocks with no
+//           barrier, W2 rows moving whole through an LDS staging tile;
+//   k_out_bwd, chunked (B > 256, bf16): 8 wavefronts (2 per SIMD); the
+//           workgroup takes 8 label blocks at a time and streams the batch
+//           through LDS in 256-row chunks, the dW2 accumulators staying in
+//           registers across chunks;
+//   k_out_bwd, global (fp32 operands): H1 and H1^T read from their
+//           L2-resident global copies.
 #include <math.h>
 
 #include <type_traits>
@@ -35,7 +37,7 @@ constexpr int BWD_WAVES = 8;
 constexpr int BWD_THREADS = 64 * BWD_WAVES;
 constexpr int BWD_CHUNK = 256;  // rows staged in LDS at a time
 
-enum BwdMode { BWD_GLOBAL = 0, BWD_STAGED = 1, BWD_CHUNKED = 2 };
+enum BwdMode { BWD_GLOBAL = 0, BWD_STAGED = 1, BWD_CHUNKED = 2 };  // STAGED: k_out_bwd_prefetch
 
 // Copy rows [r0, r0 + nrows) of H1 (row-major, ld HID) into the LDS tile (row
 // r of the chunk at tw_off(r, .)); nrows is a multiple of 32 and inside the
@@ -61,6 +63,7 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
   constexpr int NCH = 32 / M::KC;
   constexpr bool LDS_H1 = MODE != BWD_GLOBAL;
   static_assert(!LDS_H1 || BF16, "LDS staging is for bf16 operands");
+  static_assert(MODE != BWD_STAGED, "B <= 256 with bf16 operands runs k_out_bwd_prefetch");
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   const int nrb = (B + 31) >> 5;
   const int bpad = nrb * 32;
@@ -105,11 +108,7 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   };
 
-  if constexpr (MODE == BWD_STAGED) {
-    if constexpr (LDS_H1) stage_h1(h1s, H1, 0, bpad);
-    stage_rows(0, bpad);
-    __syncthreads();
-  } else if constexpr (MODE == BWD_GLOBAL) {
+  if constexpr (MODE == BWD_GLOBAL) {
     stage_rows(0, bpad);
     __syncthreads();
   }
@@ -120,8 +119,8 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
   const int cbase[2] = {tw_col_base(lane, 0), tw_col_base(lane, 1)};
 
   const int n_blocks = (L + 31) >> 5;
-  // staged / global: each wave walks its own blocks; chunked: the workgroup
-  // walks groups of 8 blocks together (a uniform trip count for the barriers)
+  // global: each wave walks its own blocks; chunked: the workgroup walks
+  // groups of 8 blocks together (a uniform trip count for the barriers)
   const int n_iter_units = MODE == BWD_CHUNKED ? (n_blocks + BWD_WAVES - 1) / BWD_WAVES : n_blocks;
   const int first = MODE == BWD_CHUNKED ? blockIdx.x : blockIdx.x * BWD_WAVES + wave;
   const int step = MODE == BWD_CHUNKED ? gridDim.x : gridDim.x * BWD_WAVES;
