@@ -11,6 +11,9 @@
 //   scatter : stable ranks inside the chunk from 64-lane ballots (lanes with the
 //             same digit in one wave), per-wave running counts, then a prefix
 //             over the four waves; keys land at offset + rank.
+// hist and scatter size their LDS counters by the pass's digit width (dynamic
+// LDS, 4 << bits and 16 << bits bytes), not by the widest digit: a narrow pass
+// then fits on a CU beside the output-layer kernels of the other stream.
 #include "asgd_dev.h"
 #include "asgd_kernels.h"
 
@@ -26,7 +29,7 @@ int sort_blocks(int n) { return (n + SORT_CHUNK - 1) / SORT_CHUNK; }
 __global__ __launch_bounds__(SORT_THREADS) void k_sort_hist(const int32_t* __restrict__ keys, int n,
                                                             int shift, int nbits, int nblk,
                                                             int32_t* __restrict__ hist) {
-  __shared__ int cnt[1 << SORT_MAX_BITS];
+  extern __shared__ int cnt[];  // 1 << nbits counters
   const int nd = 1 << nbits;
   for (int d = threadIdx.x; d < nd; d += SORT_THREADS) cnt[d] = 0;
   __syncthreads();
@@ -107,10 +110,11 @@ __global__ __launch_bounds__(SORT_THREADS) void k_sort_scatter(
     const int32_t* __restrict__ keys_in, const int32_t* __restrict__ vals_in, int n, int shift,
     int nbits, int nblk, const int32_t* __restrict__ offs, int32_t* __restrict__ keys_out,
     int32_t* __restrict__ vals_out) {
-  __shared__ int wcnt[SORT_WAVES][1 << SORT_MAX_BITS];
+  extern __shared__ int wcnt_lds[];  // SORT_WAVES x (1 << nbits) counters
   const int nd = 1 << nbits;
+  auto wcnt = [&](int ww, int d) -> int& { return wcnt_lds[ww * nd + d]; };
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  for (int d = lane; d < nd; d += 64) wcnt[w][d] = 0;
+  for (int d = lane; d < nd; d += 64) wcnt(w, d) = 0;
   __syncthreads();
   const int p0 = blockIdx.x * SORT_CHUNK + w * SORT_PER_WAVE;
   const uint64_t below = (1ull << lane) - 1ull;
@@ -130,17 +134,17 @@ __global__ __launch_bounds__(SORT_THREADS) void k_sort_scatter(
       peers &= bit ? bal : ~bal;
     }
     const int before = __popcll(peers & below);
-    const int c = wcnt[w][d];  // every peer reads the count before the leader updates it
+    const int c = wcnt(w, d);  // every peer reads the count before the leader updates it
     rank[it] = c + before;
-    if (valid && before == 0) wcnt[w][d] = c + __popcll(peers);
+    if (valid && before == 0) wcnt(w, d) = c + __popcll(peers);
   }
   __syncthreads();
   for (int d = threadIdx.x; d < nd; d += SORT_THREADS) {
     int run = 0;
 #pragma unroll
     for (int ww = 0; ww < SORT_WAVES; ++ww) {
-      const int c = wcnt[ww][d];
-      wcnt[ww][d] = run;
+      const int c = wcnt(ww, d);
+      wcnt(ww, d) = run;
       run += c;
     }
   }
@@ -150,7 +154,7 @@ __global__ __launch_bounds__(SORT_THREADS) void k_sort_scatter(
     const int p = p0 + it * 64 + lane;
     if (p < n) {
       const int d = (key[it] >> shift) & (nd - 1);
-      const int pos = offs[blockIdx.x * nd + d] + wcnt[w][d] + rank[it];
+      const int pos = offs[blockIdx.x * nd + d] + wcnt(w, d) + rank[it];
       keys_out[pos] = key[it];
       vals_out[pos] = val[it];
     }
@@ -175,11 +179,12 @@ hipError_t launch_sort(const int32_t* keys_in, int n, int key_bits, int32_t* key
   for (int pass = 0; pass < npass; ++pass) {
     const int shift = pass * bits;
     const int nb = key_bits - shift < bits ? key_bits - shift : bits;
-    hipLaunchKernelGGL(k_sort_hist, dim3(nblk), dim3(SORT_THREADS), 0, st, kin, n, shift, nb, nblk,
-                       hist);
+    hipLaunchKernelGGL(k_sort_hist, dim3(nblk), dim3(SORT_THREADS), (size_t)4 << nb, st, kin, n,
+                       shift, nb, nblk, hist);
     hipLaunchKernelGGL(k_sort_scan, dim3(1), dim3(SCAN_THREADS), 0, st, hist, nblk, 1 << nb, offs);
-    hipLaunchKernelGGL(k_sort_scatter, dim3(nblk), dim3(SORT_THREADS), 0, st, kin, vin, n, shift,
-                       nb, nblk, offs, kout, vout);
+    hipLaunchKernelGGL(k_sort_scatter, dim3(nblk), dim3(SORT_THREADS),
+                       (size_t)SORT_WAVES * 4 << nb, st, kin, vin, n, shift, nb, nblk, offs, kout,
+                       vout);
     *keys_out = kout;
     *vals_out = vout;
     kin = kout;
