@@ -131,6 +131,50 @@ def measured_peaks(n_floats: int, stream):
             "how": "torch mul_ in place over a W2-sized fp32 tensor; torch.matmul 8192^3 bf16"}
 
 
+def measure_gather_saturating(w, stream, rows=2048, reps=20):
+    """The first-layer gather at a shape that fills the GPU: top-k prediction over
+    `rows` rows of the workload (the library's largest batch: one workgroup of 8
+    waves per row, about two full passes over the chip; its gather is the training
+    step's kernel without the label work), timed with the library's events.  At the
+    training batch the gather is latency-bound; here its rate shows what the kernel
+    sustains."""
+    import torch
+    import paper_2110_07029_amd as asgd
+    from paper_2110_07029_amd import synth
+    ds = synth.generate(w, n_samples=rows)
+    ip = np.asarray(ds.x.indptr)
+    nnz = int(ip[-1] - ip[0])
+    uniq = len(np.unique(ds.x.indices))
+    dx = asgd.DeviceCSR(ds.x)
+    m = asgd.asgd_model_init(w.n_features, w.n_labels, rows, nnz, 1, gemm_bf16=w.gemm_bf16,
+                             seed=w.init_seed, stream=stream)
+    try:
+        ids = torch.empty((rows, 1), dtype=torch.int32, device="cuda")
+        xb = dx.batch(0, rows)
+        asgd.asgd_predict_topk(m, xb, 1, ids)
+        torch.cuda.synchronize()
+        k = asgd.KERNELS.index("gather")
+        asgd.asgd_model_set_timing(m, True)
+        asgd.asgd_model_get_timing(m, k)
+        for _ in range(reps):
+            asgd.asgd_predict_topk(m, xb, 1, ids)
+        torch.cuda.synchronize()
+        tot, n = asgd.asgd_model_get_timing(m, k)
+        asgd.asgd_model_set_timing(m, False)
+    finally:
+        asgd.asgd_model_free(m)
+    avg_s = tot / n * 1e-3
+    op = 2 if w.gemm_bf16 else 4
+    out_b = rows * H * (4 + 2 * op)
+    compulsory = uniq * H * 4 + nnz * 8 + out_b
+    logical = nnz * H * 4 + nnz * 8 + out_b
+    return {"rows": rows, "nnz": nnz, "unique_features": uniq, "avg_us": round(avg_s * 1e6, 2),
+            "launches": n, "logical_bytes": logical, "logical_GB/s": round(logical / avg_s / 1e9, 1),
+            "logical_hbm_frac": round(logical / avg_s / 1e9 / HBM_PEAK_GBS, 4),
+            "compulsory_bytes": compulsory, "compulsory_GB/s": round(compulsory / avg_s / 1e9, 1),
+            "how": "asgd_predict_topk(k=1) over the rows; logical = every entry's W1 row read once"}
+
+
 def measure_merge(w, n_rep, reps_iters, stream):
     """Normalized merge of n_rep replicas of the workload's model (with momentum and
     broadcast, as in the elastic configuration), timed with the library's events."""
@@ -223,14 +267,12 @@ def run_elastic(args):
     }
 
 
-def cpu_baseline(w, ds, B, budget_s):
-    """The oracle as it stands, timed on this host on a bounded sample of the workload."""
+def _oracle_steps(w, ds, B, budget_s, max_steps):
     from oracle import model as om
     p = om.init_params(w.n_features, w.n_labels, H, w.init_seed)
     ops = "bf16" if w.gemm_bf16 else "fp32"
-    n_steps, samples = 0, 0
+    n_steps, samples, r0 = 0, 0, 0
     t0 = time.perf_counter()
-    r0 = 0
     while True:
         r1 = min(r0 + B, ds.x.n_rows)
         p, *_ = om.train_step(p, ds.x.rows(r0, r1), ds.y.rows(r0, r1), w.lr, ops)
@@ -239,15 +281,39 @@ def cpu_baseline(w, ds, B, budget_s):
         r0 = r1 % ds.x.n_rows
         el = time.perf_counter() - t0
         log(f"oracle step {n_steps}: {el:.1f} s")
-        if el >= budget_s or n_steps >= 64:
-            break
+        if el >= budget_s or n_steps >= max_steps:
+            return n_steps, samples, el
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:  # pragma: no cover - not Linux
+        pass
+    return None
+
+
+def cpu_baseline(w, ds, B, budget_s):
+    """The oracle as it stands, timed on this host on a bounded sample of the
+    workload: with every thread its BLAS starts, then with one thread."""
+    n_steps, samples, el = _oracle_steps(w, ds, B, budget_s, 64)
     try:  # threads of the BLAS the oracle's products ran on (loaded by now)
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover - threadpoolctl is optional
+        threadpool_limits = None
         cores = os.cpu_count() or 1
-    return {"value": samples / el, "unit": "samples/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{n_steps} oracle steps x {B} rows of {w.name} ({samples} samples, {el:.1f} s)"}
+    out = {"value": samples / el, "unit": "samples/s", "cores": int(cores), "kind": "oracle",
+           "sample": f"{n_steps} oracle steps x {B} rows of {w.name} ({samples} samples, {el:.1f} s)",
+           "cpu_model": _cpu_model(), "host_cpus": os.cpu_count()}
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            n1, s1, e1 = _oracle_steps(w, ds, B, budget_s / 2, 64)
+        out["one_thread"] = {"value": s1 / e1, "cores": 1,
+                             "sample": f"{n1} oracle steps x {B} rows ({s1} samples, {e1:.1f} s)"}
+    return out
 
 
 def main():
@@ -365,6 +431,7 @@ def main():
     if args.workload == "wide-label":
         # the merge of the elastic configuration: 4 replicas of this model
         kernels["merge"] = measure_merge(w, 4, 10, stream)
+        kernels["gather_saturating"] = measure_gather_saturating(w, stream)
     d = kernels[dom]
     traffic = measured_traffic(w.name, B, dom)
     roofline = {"kernel": dom, "bound": "hbm", "achieved": d["GB/s"], "peak": HBM_PEAK_GBS,
