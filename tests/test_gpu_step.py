@@ -159,6 +159,20 @@ def test_step_parity_bf16(rows, B):
         s.free()
 
 
+@pytest.mark.parametrize("bf16", [True, False])
+def test_step_parity_at_the_largest_batch(bf16):
+    """The library's largest batch, 2048 rows: eight 256-row blocks in the
+    forward, the backward over 256-row H1 chunks (bf16) or with every row's
+    operands in global memory (fp32), and a sort and W1 update over ~150k
+    entries."""
+    flush(f"step mid-small rows 0..2048 max_batch 2048 bf16={bf16}")
+    s = Setup(SMALL_MID, 2048, 2048, bf16=bf16)
+    try:
+        _step_parity(s, 0, 2048, 0.05, RTOL_BF16 if bf16 else RTOL_FP32, "fp32")
+    finally:
+        s.free()
+
+
 def test_step_with_empty_feature_row_and_single_label_rows():
     flush("step: empty feature rows")
     w = synth.TINY
