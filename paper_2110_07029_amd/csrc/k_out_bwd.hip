@@ -20,8 +20,10 @@
 //           barrier, W2 rows moving whole through an LDS staging tile;
 //   k_out_bwd, chunked (B > 256, bf16): 8 wavefronts (2 per SIMD); the
 //           workgroup takes 8 label blocks at a time and streams the batch
-//           through LDS in 256-row chunks, the dW2 accumulators staying in
-//           registers across chunks;
+//           through two LDS buffers in 128-row chunks, the dW2 accumulators
+//           staying in registers across chunks: while one chunk is in use the
+//           next one is copied from global memory straight into the other
+//           buffer (global_load_lds, no registers in between);
 //   k_out_bwd, global (fp32 operands): H1 and H1^T read from their
 //           L2-resident global copies.
 #include <math.h>
@@ -35,7 +37,8 @@ namespace asgd {
 
 constexpr int BWD_WAVES = 8;
 constexpr int BWD_THREADS = 64 * BWD_WAVES;
-constexpr int BWD_CHUNK = 256;  // rows staged in LDS at a time
+constexpr int BWD_CHUNK = 256;  // batches up to this size are staged whole (k_out_bwd_prefetch)
+constexpr int BWD_CROWS = 128;  // rows per H1 chunk of the chunked kernel (two chunk buffers)
 
 enum BwdMode { BWD_GLOBAL = 0, BWD_STAGED = 1, BWD_CHUNKED = 2 };  // STAGED: k_out_bwd_prefetch
 
@@ -48,6 +51,17 @@ __device__ __forceinline__ void stage_h1(bf16* h1s, const bf16* __restrict__ H1,
     const uint4 v = *reinterpret_cast<const uint4*>(H1 + (size_t)(r0 + r) * HID + c * 8);
     *reinterpret_cast<uint4*>(h1s + r * TW_LD + 8 * (c ^ ((r >> 2) & 3))) = v;
   }
+}
+
+// One 16-byte direct copy per lane from global memory into LDS: lane l's
+// bytes land at LDS byte lds + 16 l (lds: wave-uniform LDS byte address).
+// Written as inline asm so that the compiler's wait-count pass does not treat
+// every later LDS access as dependent on the copy (it cannot tell the target
+// apart from other LDS data): the kernel waits for its copies itself.  No
+// other code in the kernel uses M0.
+__device__ __forceinline__ void lds_copy16(const void* src, unsigned lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds)
+               : "memory");
 }
 
 template <bool BF16, int MODE>
@@ -67,23 +81,23 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   const int nrb = (B + 31) >> 5;
   const int bpad = nrb * 32;
-  // rows whose constants and target bits are held at once
-  const int span = MODE == BWD_CHUNKED ? BWD_CHUNK : bpad;
+  // rows whose target bits are held at once
+  const int span = MODE == BWD_CHUNKED ? BWD_CROWS : bpad;
   const int mstride = span >> 5;  // mask words per label
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, n = lane & 31;
 
   char* sp = smem_raw;
-  E* h1s = nullptr;
+  E* h1b = nullptr;  // two chunk buffers of BWD_CROWS rows
   if constexpr (LDS_H1) {
-    h1s = reinterpret_cast<E*>(sp);
-    sp += BWD_CHUNK * TW_LD * sizeof(E);
+    h1b = reinterpret_cast<E*>(sp);
+    sp += 2 * BWD_CROWS * TW_LD * sizeof(E);
   }
-  // per row: crow = log2(1/B) - lse*log2(e) (-inf for rows past B) so that
-  // dZ = 2^(z*log2(e) + bias*log2(e) + crow) = softmax/B; tw = (1/|Y_i|)/B
+  // per row of the batch: crow = log2(1/B) - lse*log2(e) (-inf for rows past B)
+  // so that dZ = 2^(z*log2(e) + bias*log2(e) + crow) = softmax/B; tw = (1/|Y_i|)/B
   float* crow_s = reinterpret_cast<float*>(sp);
-  sp += span * sizeof(float);
+  sp += bpad * sizeof(float);
   float* tw_s = reinterpret_cast<float*>(sp);
-  sp += span * sizeof(float);
+  sp += bpad * sizeof(float);
   uint32_t* mask = reinterpret_cast<uint32_t*>(sp) + wave * 32 * mstride;
 
   // Row constants of rows [r0, r0 + nrows) at LDS index (row - r0).
@@ -95,23 +109,48 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
     }
   };
   // Target bits of this wave's labels for rows [r0, r0 + nrows): mask[label][row block],
-  // from the block's (row << 5 | label % 32) pairs in lpair[lo, hi).
-  auto build_mask = [&](int lo, int hi, int r0, int nrows) {
+  // from the block's (row << 5 | label % 32) pairs in lpair[lo, hi); pr_first is
+  // the lane's pair lo + lane, loaded once per block (-1: none).
+  auto build_mask = [&](int lo, int hi, int pr_first, int r0, int nrows) {
     for (int k = lane; k < 32 * mstride; k += 64) mask[k] = 0u;
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    for (int q = lo + lane; q < hi; q += 64) {
-      const int pr = lpair[q];
+    auto put = [&](int pr) {
       const int row = (pr >> 5) - r0;
       if (row >= 0 && row < nrows)
         atomicOr(&mask[(pr & 31) * mstride + (row >> 5)], 1u << (row & 31));
-    }
+    };
+    if (pr_first >= 0) put(pr_first);
+    for (int q = lo + 64 + lane; q < hi; q += 64) put(lpair[q]);
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   };
 
-  if constexpr (MODE == BWD_GLOBAL) {
-    stage_rows(0, bpad);
-    __syncthreads();
-  }
+  // Rows [c0, c0 + BWD_CROWS) of H1 into chunk buffer dst, in the tile layout
+  // of stage_h1, by direct global-to-LDS copies: a wave's 16-byte copy fills
+  // 1024 consecutive LDS bytes (lane l at byte 16 l), so each lane picks the
+  // global chunk that belongs at its LDS slot; the 4 pad slots of a row (bytes
+  // 256..319) take an arbitrary chunk of the row.  The rows read stay below
+  // round_up(B, BWD_CROWS), inside the H1 buffer (checked by the host).
+  auto issue_chunk = [&](int c0, E* dst) {
+    if constexpr (MODE == BWD_CHUNKED) {
+      constexpr int ROW_B = TW_LD * (int)sizeof(E);  // 320 bytes
+      constexpr int N_COPY = BWD_CROWS * ROW_B / 1024;
+      static_assert(N_COPY % BWD_WAVES == 0, "chunk copies split evenly over the waves");
+      const int wv = __builtin_amdgcn_readfirstlane(wave);
+#pragma unroll
+      for (int j = 0; j < N_COPY / BWD_WAVES; ++j) {
+        const int blk_b = (j * BWD_WAVES + wv) * 1024;
+        const int o = blk_b + lane * 16;
+        const int r = o / ROW_B;
+        const int slot = (o - r * ROW_B) >> 4;
+        const int c = slot < 16 ? (slot ^ ((r >> 2) & 3)) : 0;
+        lds_copy16(H1 + (size_t)(c0 + r) * HID + 8 * c,
+                   __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)dst + blk_b));
+      }
+    }
+  };
+
+  stage_rows(0, bpad);
+  __syncthreads();
   // the lane's bases in the LDS tile: H1 row fragments (rows 32 rb + n) and
   // transposed H1^T fragments (hidden 32 hb + n); every offset below is rb, kb,
   // hb, c or hi times a constant
@@ -124,6 +163,11 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
   const int n_iter_units = MODE == BWD_CHUNKED ? (n_blocks + BWD_WAVES - 1) / BWD_WAVES : n_blocks;
   const int first = MODE == BWD_CHUNKED ? blockIdx.x : blockIdx.x * BWD_WAVES + wave;
   const int step = MODE == BWD_CHUNKED ? gridDim.x : gridDim.x * BWD_WAVES;
+  // chunked: chunks are consumed in the order (unit, chunk); kc counts them,
+  // and chunk kc lives in buffer kc & 1.  The first one is requested here.
+  const int nch = (bpad + BWD_CROWS - 1) / BWD_CROWS;
+  int kc = 0;
+  if (MODE == BWD_CHUNKED && first < n_iter_units) issue_chunk(0, h1b);
   for (int unit = first; unit < n_iter_units; unit += step) {
     const int blk = MODE == BWD_CHUNKED ? unit * BWD_WAVES + wave : unit;
     const bool bactive = blk < n_blocks;
@@ -177,6 +221,7 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
       hi = lbeg[blk + 1];
     }
     const bool has_targets = hi > lo;
+    const int pr0 = lo + lane < hi ? lpair[lo + lane] : -1;
 
     f32x16 accw[4];
 #pragma unroll
@@ -185,13 +230,14 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
       for (int r = 0; r < 16; ++r) accw[hb][r] = 0.0f;
     float db2p = 0.0f;
 
-    // one 32-row block: rb indexes the rows held in LDS / the row constants
-    auto row_block = [&](int rb, int grow0) {
+    // one 32-row block of the batch (rows grow0 ..): rb indexes its rows in
+    // the H1 chunk buffer hbuf and in the target mask
+    auto row_block = [&](const E* hbuf, int rb, int grow0) {
       f32x16 z;
 #pragma unroll
       for (int r = 0; r < 16; ++r) z[r] = 0.0f;
       if constexpr (LDS_H1) {
-        const E* t = h1s + rb * 32 * TW_LD;
+        const E* t = hbuf + rb * 32 * TW_LD;
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -208,7 +254,7 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
       float cr[16];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const float4 c4 = *reinterpret_cast<const float4*>(crow_s + rb * 32 + 8 * q + 4 * g);
+        const float4 c4 = *reinterpret_cast<const float4*>(crow_s + grow0 + 8 * q + 4 * g);
         cr[4 * q + 0] = c4.x; cr[4 * q + 1] = c4.y; cr[4 * q + 2] = c4.z; cr[4 * q + 3] = c4.w;
       }
       float dz[16];
@@ -220,7 +266,7 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int rl = 8 * (r >> 2) + 4 * g + (r & 3);
-            if ((mw >> rl) & 1u) dz[r] -= tw_s[rb * 32 + rl];
+            if ((mw >> rl) & 1u) dz[r] -= tw_s[grow0 + rl];
           }
         }
       }
@@ -235,7 +281,7 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
         if constexpr (LDS_H1) {
 #pragma unroll
           for (int c = 0; c < NCH; ++c) {
-            const E* o = h1s + (rb * 32 + 16 * c) * TW_LD + 32 * hb;
+            const E* o = hbuf + (rb * 32 + 16 * c) * TW_LD + 32 * hb;
             const bf16x4 lo4 = lds_read_tr16(o + cbase[0]), hi4 = lds_read_tr16(o + cbase[1]);
             bf16x8 af;
             af[0] = lo4[0]; af[1] = lo4[1]; af[2] = lo4[2]; af[3] = lo4[3];
@@ -251,19 +297,23 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
     };
 
     if constexpr (MODE == BWD_CHUNKED) {
-      for (int c0 = 0; c0 < bpad; c0 += BWD_CHUNK) {
-        const int crows = min(BWD_CHUNK, bpad - c0);
-        __syncthreads();  // every wave is done with the previous chunk
-        if constexpr (LDS_H1) stage_h1(h1s, H1, c0, crows);
-        stage_rows(c0, crows);
-        if (has_targets) build_mask(lo, hi, c0, crows);
+      for (int ci = 0; ci < nch; ++ci, ++kc) {
+        const int c0 = ci * BWD_CROWS;
+        const int crows = min(BWD_CROWS, bpad - c0);
+        const E* cur = h1b + (kc & 1) * (BWD_CROWS * TW_LD);
+        // this thread's copies into cur have landed; after the barrier all of
+        // cur is there and every wave is done with the other buffer
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
+        if (ci + 1 < nch || unit + step < n_iter_units)
+          issue_chunk(ci + 1 < nch ? c0 + BWD_CROWS : 0, h1b + ((kc + 1) & 1) * (BWD_CROWS * TW_LD));
+        if (has_targets) build_mask(lo, hi, pr0, c0, crows);
         if (bactive)
-          for (int rb = 0; rb < (crows >> 5); ++rb) row_block(rb, c0 + rb * 32);
+          for (int rb = 0; rb < (crows >> 5); ++rb) row_block(cur, rb, c0 + rb * 32);
       }
     } else {
-      if (has_targets) build_mask(lo, hi, 0, bpad);
-      for (int rb = 0; rb < nrb; ++rb) row_block(rb, rb * 32);
+      if (has_targets) build_mask(lo, hi, pr0, 0, bpad);
+      for (int rb = 0; rb < nrb; ++rb) row_block(nullptr, rb, rb * 32);
     }
 
     const float db2 = db2p + __shfl_xor(db2p, 32);
@@ -572,9 +622,14 @@ hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, const void
                           hipStream_t st) {
   const int nrb = (B + 31) / 32;
   const int mode = !use_bf16 ? BWD_GLOBAL : (B <= BWD_CHUNK ? BWD_STAGED : BWD_CHUNKED);
-  const int span = mode == BWD_CHUNKED ? BWD_CHUNK : nrb * 32;
-  size_t shm = (size_t)2 * span * sizeof(float) + (size_t)BWD_WAVES * 32 * (span / 32) * sizeof(uint32_t);
-  if (mode != BWD_GLOBAL) shm += (size_t)BWD_CHUNK * TW_LD * 2;
+  const int bpad = nrb * 32;
+  const int mspan = mode == BWD_CHUNKED ? BWD_CROWS : bpad;  // rows of one target mask
+  size_t shm = (size_t)2 * bpad * sizeof(float) + (size_t)BWD_WAVES * 32 * (mspan / 32) * sizeof(uint32_t);
+  if (mode == BWD_CHUNKED) {
+    // the chunk copies read whole chunks of H1 rows (ld_t rows allocated)
+    if ((B + BWD_CROWS - 1) / BWD_CROWS * BWD_CROWS > ld_t) return hipErrorInvalidValue;
+    shm += (size_t)2 * BWD_CROWS * TW_LD * 2;
+  }
   const int n_blocks = (L + 31) / 32;
   int grid = (n_blocks + BWD_WAVES - 1) / BWD_WAVES;
   const int cap = mode == BWD_GLOBAL ? 2 * n_cu : n_cu;
