@@ -599,7 +599,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_topk(
   constexpr int NCH = 32 / M::KC;
   constexpr int WROWS = 32 * NB;
   __shared__ __attribute__((aligned(16))) E wr[2][tile_elems<BF16>()];
-  __shared__ float bt[2][OUT_TILE];
+  __shared__ __attribute__((aligned(16))) float bt[2][OUT_TILE];
   __shared__ float ls[FwdShape<BF16>::WAVES][WROWS][TOPK_MAX];
   __shared__ int li[FwdShape<BF16>::WAVES][WROWS][TOPK_MAX];
 
@@ -625,22 +625,37 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_topk(
 #pragma unroll
       for (int c = 0; c < NCH; ++c) hf[nb][kb][c] = h1_frag<BF16>(hrow, kb, c, g);
   }
-  TileRegs tr;
+  // W2 tiles are loaded three ahead: at the start of iteration t, tile t is in
+  // LDS buffer (t - t_begin) & 1 and tiles t+1, t+2, t+3 are in the register
+  // sets tr0, tr1, tr2 in turn (the loop is unrolled by three so that every
+  // set is named statically); iteration t moves tile t+1 into the other
+  // buffer and reloads its set with tile t+4.
+  const int t_last = t_end - 1;
+  TileRegs tr0, tr1, tr2;
   if (t_begin < t_end) {
-    tile_load(src, t_begin, tr);
-    tile_store<BF16, false>(tr, L, t_begin, wr[0], nullptr, bt[0]);
+    tile_load(src, t_begin, tr0);
+    tile_store<BF16, false>(tr0, L, t_begin, wr[0], nullptr, bt[0]);
+    tile_load(src, min(t_begin + 1, t_last), tr0);
+    tile_load(src, min(t_begin + 2, t_last), tr1);
+    tile_load(src, min(t_begin + 3, t_last), tr2);
   }
   __syncthreads();
-  for (int t = t_begin; t < t_end; ++t) {
+  auto iteration = [&](int t, TileRegs& trn) {
     const int buf = (t - t_begin) & 1;
-    const bool has_next = t + 1 < t_end;
-    if (has_next) tile_load(src, t + 1, tr);
     if (active) {
+      // the accumulators start from the biases of the tile's labels (rows of Z^T)
       f32x16 z[NB];
+      {
+        const float4* bq = reinterpret_cast<const float4*>(bt[buf]);
+        f32x16 zb;
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
+        for (int q = 0; q < 4; ++q) {
+          const float4 bv = bq[2 * q + g];
+          zb[4 * q + 0] = bv.x; zb[4 * q + 1] = bv.y; zb[4 * q + 2] = bv.z; zb[4 * q + 3] = bv.w;
+        }
 #pragma unroll
-        for (int r = 0; r < 16; ++r) z[nb][r] = 0.0f;
+        for (int nb = 0; nb < NB; ++nb) z[nb] = zb;
+      }
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -653,17 +668,26 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_topk(
       for (int nb = 0; nb < NB; ++nb) {
         const int rloc = nb * 32 + n;
         const bool rvalid = row0 + rloc < B;
+        // skip the tile unless some lane's best score reaches its row's k-th
+        // entry (NaN never does; ties go to the exact test below)
+        float m = z[nb][0];
+#pragma unroll
+        for (int r = 1; r < 16; ++r) m = fmaxf(m, z[nb][r]);
+        if (!__any(rvalid && m >= ls[wave][rloc][k - 1])) continue;
         for (int half = 0; half < 2; ++half) {
           if (g == half && rvalid) {
             float* lsr = ls[wave][rloc];
             int* lir = li[wave][rloc];
+            // the row's current k-th entry, re-read only after an insertion:
+            // most scores fail this test and touch no LDS
+            float ts = lsr[k - 1];
+            int ti = lir[k - 1];
             for (int r = 0; r < 16; ++r) {
               const int ll = 8 * (r >> 2) + 4 * g + (r & 3);
               const int id = t * OUT_TILE + ll;
-              if (id >= L) continue;
-              const float sc = z[nb][r] + bt[buf][ll];
-              if (!(sc == sc)) continue;  // NaN scores are never ranked
-              if (!better(sc, id, lsr[k - 1], lir[k - 1])) continue;
+              const float sc = z[nb][r];
+              if (id >= L || !(sc == sc)) continue;  // NaN scores are never ranked
+              if (!better(sc, id, ts, ti)) continue;
               int pos = k - 1;
               while (pos > 0 && better(sc, id, lsr[pos - 1], lir[pos - 1])) {
                 lsr[pos] = lsr[pos - 1];
@@ -672,13 +696,23 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_topk(
               }
               lsr[pos] = sc;
               lir[pos] = id;
+              ts = lsr[k - 1];
+              ti = lir[k - 1];
             }
           }
         }
       }
     }
-    if (has_next) tile_store<BF16, false>(tr, L, t + 1, wr[buf ^ 1], nullptr, bt[buf ^ 1]);
+    if (t + 1 < t_end) tile_store<BF16, false>(trn, L, t + 1, wr[buf ^ 1], nullptr, bt[buf ^ 1]);
+    if (t + 4 <= t_last) tile_load(src, t + 4, trn);
     __syncthreads();
+  };
+  for (int t = t_begin; t < t_end; t += 3) {
+    iteration(t, tr0);
+    if (t + 1 >= t_end) break;
+    iteration(t + 1, tr1);
+    if (t + 2 >= t_end) break;
+    iteration(t + 2, tr2);
   }
   if (active) {
     for (int e = lane; e < WROWS * k; e += 64) {

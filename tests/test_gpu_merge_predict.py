@@ -104,9 +104,13 @@ def test_l2_per_param_matches_numpy():
         asgd.asgd_model_free(m)
 
 
-@pytest.mark.parametrize("w,bf16,k", [(synth.TINY, False, 5), (synth.TINY, True, 1),
-                                      (synth.MID, True, 8)])
-def test_topk_ids_bit_exact_on_tie_free_rows(w, bf16, k):
+# min_frac: share of the rows whose top k + 1 logits must be far enough apart
+# to be compared id by id; at k = 32 all 32 consecutive gaps must clear the
+# bound, which ~10-15 % of these rows do (every row's scores are checked anyway)
+@pytest.mark.parametrize("w,bf16,k,min_frac", [(synth.TINY, False, 5, 0.5), (synth.TINY, True, 1, 0.5),
+                                               (synth.MID, True, 8, 0.5), (synth.TINY, False, 32, 0.1),
+                                               (synth.TINY, True, 32, 0.1)])
+def test_topk_ids_bit_exact_on_tie_free_rows(w, bf16, k, min_frac):
     import torch
     flush(f"top-k: {w.name} bf16={bf16} k={k}")
     s = Setup(w, 300, 300, bf16=bf16)
@@ -146,7 +150,7 @@ def test_topk_ids_bit_exact_on_tie_free_rows(w, bf16, k):
             zi = Z[i, gi[i]]
             assert np.all(np.abs(gs[i] - zi) <= tol * (1.0 + np.abs(zi)) + fb[i, gi[i]]), i
             assert np.all(np.diff(gs[i]) <= 0)
-        assert checked > B // 2
+        assert checked > B * min_frac
     finally:
         s.free()
 
