@@ -319,8 +319,8 @@ def cpu_baseline(w, ds, B, budget_s):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only: every run in this build uses a single MI355X "
-              f"(got --gpus {args.gpus}); the multi-GPU merge is a design, not a measured path.",
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the replicas of the elastic "
+              f"configuration share a single MI355X, and the multi-GPU merge is a design, not a measured path.",
               file=sys.stderr)
         sys.exit(2)
     import torch
