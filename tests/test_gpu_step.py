@@ -17,6 +17,10 @@ pytestmark = pytest.mark.gpu
 
 SMALL_MID = synth.Workload("mid-small", 20_000, 3_000, 4_000, 256, 0.01, True, "lognormal", 4.0,
                            0.8, 2_000, 1.05, "uniform", "poisson", 4.0, 1.2, 2)
+# feature ids up to 2^22 - 1, the library's limit: the feature sort then runs two
+# passes of 11-bit digits, its widest (the largest LDS counter arrays)
+WIDE_IDS = synth.Workload("ids-22-bit", (1 << 22) - 1, 500, 512, 256, 0.01, True, "lognormal", 4.0,
+                          0.8, 2_000, 1.05, "uniform", "poisson", 4.0, 1.2, 2)
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -96,7 +100,8 @@ def test_one_hot_rows_are_exact_rows_of_w1():
         s.free()
 
 
-@pytest.mark.parametrize("w,rows", [(synth.TINY, (0, 128)), (SMALL_MID, (0, 256)), (SMALL_MID, (100, 101))])
+@pytest.mark.parametrize("w,rows", [(synth.TINY, (0, 128)), (SMALL_MID, (0, 256)), (SMALL_MID, (100, 101)),
+                                    (WIDE_IDS, (0, 256))])
 def test_touched_rows_bit_exact(w, rows):
     import torch
     flush(f"touched rows: {w.name} {rows}")
@@ -169,6 +174,20 @@ def test_step_parity_at_the_largest_batch(bf16):
     s = Setup(SMALL_MID, 2048, 2048, bf16=bf16)
     try:
         _step_parity(s, 0, 2048, 0.05, RTOL_BF16 if bf16 else RTOL_FP32, "fp32")
+    finally:
+        s.free()
+
+
+def test_step_parity_with_22_bit_feature_ids():
+    """F = 2^22 - 1 (W1 is 2 GiB): the batch's ids spread over the whole 22-bit
+    range, so both 11-bit digit passes of the feature sort are exercised."""
+    flush("step: 22-bit feature ids, F = 2^22 - 1, rows 0..256")
+    s = Setup(WIDE_IDS, 512, 256)
+    try:
+        xh, _ = s.host_batch(0, 256)
+        ids = np.asarray(xh.indices[int(xh.indptr[0]):int(xh.indptr[-1])])
+        assert ids.max() >= 1 << 21 and ids.min() < 1 << 11
+        _step_parity(s, 0, 256, 0.05, RTOL_BF16, "fp32")
     finally:
         s.free()
 
