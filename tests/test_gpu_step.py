@@ -192,6 +192,23 @@ def test_step_parity_with_22_bit_feature_ids():
         s.free()
 
 
+# more 32-label blocks than the forward launch's LDS holds counters for: the
+# label grouping then counts in global memory
+MANY_LABELS = synth.Workload("labels-1m", 5_000, 1_000_003, 128, 64, 0.01, True, "lognormal", 4.0,
+                             0.8, 2_000, 1.05, "uniform", "poisson", 4.0, 1.2, 2)
+
+
+def test_step_parity_with_label_counters_in_global_memory():
+    """L = 1,000,003 (ragged last tile): 31,251 label blocks do not fit the
+    forward's LDS, so the label grouping takes its global-memory path."""
+    flush("step: L = 1,000,003, rows 0..64")
+    s = Setup(MANY_LABELS, 128, 64)
+    try:
+        _step_parity(s, 0, 64, 0.05, RTOL_BF16, "fp32")
+    finally:
+        s.free()
+
+
 def test_step_with_empty_feature_row_and_single_label_rows():
     flush("step: empty feature rows")
     w = synth.TINY
