@@ -209,6 +209,22 @@ def test_step_parity_with_label_counters_in_global_memory():
         s.free()
 
 
+def test_step_parity_when_the_running_maximum_rises():
+    """Biases rising by 6 per 32-label tile: on every tile of a split the row
+    maximum exceeds the forward's running reference by more than its lazy
+    rescale margin (8 in base 2, about 5.5), so the rescale of the running sum
+    and of the O accumulators runs on every tile."""
+    flush("step: rising biases (forward rescale path), mid rows 0..256")
+    w = synth.MID
+    s = Setup(w, 256, 256)
+    try:
+        b2 = (6.0 * (np.arange(w.n_labels) // 32)).astype(np.float32)
+        asgd.asgd_model_set_params(s.m, asgd.ASGD_PARAM_B2, b2)
+        _step_parity(s, 0, 256, 0.05, RTOL_BF16, "fp32")
+    finally:
+        s.free()
+
+
 def test_step_with_empty_feature_row_and_single_label_rows():
     flush("step: empty feature rows")
     w = synth.TINY
