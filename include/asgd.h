@@ -63,9 +63,10 @@ typedef struct asgd_config {
   int32_t n_features;    /* F in [1, 2^22) */
   int32_t n_labels;      /* L in [1, 2^22) */
   int32_t hidden;        /* H; must be 128 */
-  int32_t max_batch;     /* largest B any call will use (memory pool sized for it, Sec. 4) */
-  int32_t max_nnz;       /* largest sum of nnz over the rows of one batch */
-  int32_t max_label_nnz; /* largest sum of |Y_i| over the rows of one batch */
+  int32_t max_batch;     /* largest B any call will use, in [1, 2048] (memory pool sized for it, Sec. 4) */
+  int32_t max_nnz;       /* largest sum of nnz over the rows of one batch (>= 0) */
+  int32_t max_label_nnz; /* largest sum of |Y_i| over the rows of one batch (>= 0;
+                            max_nnz + max_label_nnz < 2^30) */
   int32_t gemm_bf16;     /* 1: output-layer products on bf16 operands with fp32 accumulation
                             (fp32 master weights); 0: fp32 operands */
   uint32_t flags;        /* ASGD_VALIDATE or 0 */
@@ -113,7 +114,12 @@ enum {
  * fl32(fl32(2u-1) * a) with u = (splitmix64(seed ^ (t << 56) ^ e) >> 40) * 2^-24,
  * splitmix64 being the published generator's output for that state.  Biases
  * start at 0.  Initialisation runs on `hip_stream`; the call returns once it
- * has completed.  *out receives the model; nothing is allocated on error. */
+ * has completed.  *out receives the model; nothing is allocated on error.
+ * Errors: EINVAL for a NULL argument, a count below 1 (0 for the nnz maxima),
+ * hidden != 128, gemm_bf16 not 0 or 1 or unknown flag bits; ERANGE for F or L
+ * at or above 2^22 (F + L below 2^30), max_batch outside [1, 2048] or
+ * max_nnz + max_label_nnz at or above 2^30; ENOMEM / EHIP when the device
+ * allocation or the initialisation fails. */
 asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t seed,
                             void* hip_stream);
 
