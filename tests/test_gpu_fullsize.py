@@ -55,6 +55,41 @@ def test_full_size_step(name, B):
         s.free()
 
 
+def test_full_size_step_after_training():
+    """The same comparison from a trained model instead of the initial one: 49
+    steps at lr 20 on distinct batches move the weights well away from their
+    small initial values (sharper softmax rows, larger W1 rows for hot
+    features), then one step at the workload's lr is compared with the oracle
+    started from the GPU's state."""
+    w = synth.WIDE_LABEL
+    B, n_pre = 256, 49
+    flush(f"full-size step after {n_pre} training steps: wide-label B={B}")
+    s = Setup(w, (n_pre + 1) * B, B)
+    try:
+        p0 = s.params()
+        for i in range(n_pre):
+            asgd.asgd_train_step(s.m, s.xb(i * B, (i + 1) * B), s.yb(i * B, (i + 1) * B), 20.0)
+        before = s.params()
+        assert all(np.all(np.isfinite(v)) for v in before.values())
+        moved = np.linalg.norm(before["W2"] - p0["W2"]) / np.linalg.norm(p0["W2"])
+        flush(f"  W2 moved by {moved:.3f} of its initial norm")
+        assert moved > 1e-2
+        r0, r1 = n_pre * B, (n_pre + 1) * B
+        loss = asgd.asgd_train_step(s.m, s.xb(r0, r1), s.yb(r0, r1), w.lr, want_loss=True)
+        after = s.params()
+        xh, yh = s.host_batch(r0, r1)
+        ref, ref_loss, g, fw = om.train_step(before, xh, yh, w.lr, "fp32")
+        flush(f"  loss gpu {loss:.6f} oracle {ref_loss:.6f}")
+        assert abs(loss - ref_loss) <= 1e-3 * abs(ref_loss)
+        mag = step_magnitudes(before, xh, yh, g, fw, w.lr)
+        for k in ("b1", "W2", "b2"):
+            assert_update_close(k, before[k], after[k], ref[k], RTOL_BF16, mag[k])
+        t = g["touched"]
+        assert_update_close("W1[touched]", before["W1"][t], after["W1"][t], ref["W1"][t], RTOL_BF16, mag["W1"])
+    finally:
+        s.free()
+
+
 def test_full_size_top1():
     import torch
     w = synth.WIDE_LABEL
