@@ -17,9 +17,12 @@ Readings where the paper is silent (each is listed in the design notes):
 * only W1 rows whose feature occurs in the batch are written by the update.
 
 Arithmetic is float64 on float32-stored parameters; each updated parameter is
-rounded to float32 once.  With ``operands="bf16"`` the products of the output
-layer use bfloat16-rounded operands (round-to-nearest-even), as a kernel with
-bf16 matrix-core operands and wide accumulation would, still summed in float64.
+rounded to float32 once.  With ``operands="bf16"`` the three products of the
+output layer take bfloat16-rounded operands (round-to-nearest-even of the
+float32 value) and are still summed in float64: Z = bf16(H1) bf16(W2)^T + b2,
+dW2 = bf16(dZ)^T bf16(H1) and dH1 = bf16(dZ) bf16(W2).  Nothing else is
+rounded: the softmax, the loss, dZ itself, db2 and the first layer stay in
+float64.
 """
 from __future__ import annotations
 
@@ -161,15 +164,13 @@ def backward(p: dict, x, y, fw: dict, operands: str = "fp32") -> dict:
     P = np.exp(fw["Z"] - fw["lse"][:, None])
     T = targets(y, L)
     dZ = (P - T) / B
-    H1 = fw["H1"]
-    dW2 = _operand(dZ.astype(F32), operands).T @ _operand(H1, operands) if operands == "bf16" else dZ.T @ H1
+    # the two products of the output layer take their operands in `operands`:
+    # with bf16, dZ (stored as float32 first), H1 and the pre-update W2 are
+    # rounded; the bias gradient is a plain sum of the unrounded dZ
+    dZo = _operand(dZ.astype(F32), operands) if operands == "bf16" else dZ
+    dW2 = dZo.T @ _operand(fw["H1"], operands)
     db2 = dZ.sum(axis=0)
-    if operands == "bf16":
-        # (P - T) W2 / B with the dense softmax product on bf16 operands
-        dH1 = (_operand(P.astype(F32), operands) @ _operand(p["W2"], operands)
-               - T @ p["W2"].astype(F64)) / B
-    else:
-        dH1 = dZ @ p["W2"].astype(F64)    # uses the pre-update W2
+    dH1 = dZo @ _operand(p["W2"], operands)    # uses the pre-update W2
     dA1 = dH1 * (fw["A1"] > 0.0)
     db1 = dA1.sum(axis=0)
     ind, val, rows = _entries(x)

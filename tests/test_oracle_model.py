@@ -253,6 +253,56 @@ def test_bf16_operands_close_to_exact():
     assert 1e-5 < rel < 1e-2
 
 
+def _one_row_problem(w1_row, w2):
+    """F = 1, H = 2, L = 3, B = 1: one feature of value 1, label {0}, b1 = b2 = 0."""
+    x = synth.CSR(np.array([0, 1]), np.array([0], np.int32), np.array([1.0], np.float32), 1)
+    y = synth.CSR(np.array([0, 1]), np.array([0], np.int32), None, 3)
+    p = dict(W1=np.array([w1_row], np.float32), b1=np.zeros(2, np.float32),
+             W2=np.array(w2, np.float32), b2=np.zeros(3, np.float32))
+    return x, y, p
+
+
+# Hand-derived values for the bf16 pins.  With Z = 0 over L = 3 labels the softmax
+# is 1/3 everywhere, so dZ = (1/3 - 1, 1/3, 1/3) for the target {0}.  As float32
+# these are 0xBF2AAAAB and 0x3EAAAAAB; rounded to nearest bf16 (ties to even) they
+# become 0xBF2B = -171/256 and 0x3EAB = 171/512 (truncation would give 0xBF2A =
+# -170/256 and 0x3EAA = 170/512).  The hidden value 1.005859375 = 0x3F80C000
+# rounds up to 0x3F81 = 129/128 (truncation: 1.0); 0.5 is a bf16 value.
+DZ0_B, DZ1_B, H_B = -171 / 256, 171 / 512, 129 / 128
+
+
+def test_bf16_backward_rounds_dz_h1_and_w2_to_nearest_even_dw2():
+    # W2 = 0 and H1 = (1.005859375, 0.5): dW2 = bf16(dZ)^T bf16(H1), exactly
+    x, y, p = _one_row_problem([1.005859375, 0.5], np.zeros((3, 2)))
+    fw = om.forward(p, x, y, "bf16")
+    assert np.all(fw["Z"] == 0.0)
+    g = om.backward(p, x, y, fw, "bf16")
+    want = np.array([[DZ0_B * H_B, DZ0_B * 0.5], [DZ1_B * H_B, DZ1_B * 0.5], [DZ1_B * H_B, DZ1_B * 0.5]])
+    assert np.array_equal(g["dW2"], want)
+    assert want[1, 0] == 22059 / 65536           # 0.3365936279296875 (no rounding: 0.33528...)
+    # the bias gradient is the unrounded dZ; the update with lr = 1 stores -dW2
+    assert np.allclose(g["db2"], [-2 / 3, 1 / 3, 1 / 3], rtol=0, atol=1e-15)
+    q, *_ = om.train_step(p, x, y, 1.0, "bf16")
+    assert np.array_equal(q["W2"].astype(np.float64), -want)
+    # fp32 operands: the exact products
+    g32 = om.backward(p, x, y, om.forward(p, x, y, "fp32"), "fp32")
+    assert np.allclose(g32["dW2"][1], [1.005859375 / 3, 0.5 / 3], rtol=1e-15, atol=0)
+
+
+def test_bf16_backward_rounds_dz_and_w2_in_dh1():
+    # H1 = 0 (both pre-activations negative), so Z = b2 = 0 whatever W2 is; then
+    # dH1 = bf16(dZ) bf16(W2) with W2 row 0 = (1.005859375, 0.5), the others 0
+    x, y, p = _one_row_problem([-1.0, -2.0], [[1.005859375, 0.5], [0.0, 0.0], [0.0, 0.0]])
+    fw = om.forward(p, x, y, "bf16")
+    assert np.all(fw["H1"] == 0.0) and np.all(fw["Z"] == 0.0)
+    g = om.backward(p, x, y, fw, "bf16")
+    assert np.array_equal(g["dH1"], [[DZ0_B * H_B, DZ0_B * 0.5]])
+    assert g["dH1"][0, 0] == -22059 / 32768       # -0.673187255859375 (no rounding: -0.67057...)
+    assert np.all(g["dA1"] == 0.0)                # ReLU'(A1 < 0) = 0
+    g32 = om.backward(p, x, y, om.forward(p, x, y, "fp32"), "fp32")
+    assert np.allclose(g32["dH1"], [[-2 / 3 * 1.005859375, -1 / 3]], rtol=1e-15, atol=0)
+
+
 def test_gradient_aggregation_equals_model_averaging_after_one_step():
     # Sec. 2.2: averaging after every batch makes model averaging equal gradient
     # aggregation: n replicas, one step each on disjoint batches of size b, merged
