@@ -32,10 +32,18 @@ def test_one_based_ids_unsorted_rows_and_no_header(tmp_path):
 
 
 def test_rows_without_labels_or_features(tmp_path):
+    # a row with no features is a valid batch row (A1 = b1); a row with no labels
+    # is not (the loss is undefined), so it is dropped by default
     p = tmp_path / "e.txt"
-    p.write_text("2 10 4\n 3:1.5\n1,2\n")
+    p.write_text("3 10 4\n 3:1.5\n1,2\n0 4:1 5:2\n")
     ds = libsvm.load(str(p))
-    assert ds.x.indptr.tolist() == [0, 1, 1] and ds.y.indptr.tolist() == [0, 0, 2]
+    assert ds.x.n_rows == 2 and ds.workload.n_samples == 2
+    assert ds.x.indptr.tolist() == [0, 0, 2] and ds.x.indices.tolist() == [4, 5]
+    assert ds.y.indptr.tolist() == [0, 2, 3] and ds.y.indices.tolist() == [1, 2, 0]
+    kept = libsvm.load(str(p), unlabeled="keep")
+    assert kept.x.indptr.tolist() == [0, 1, 1, 3] and kept.y.indptr.tolist() == [0, 0, 2, 3]
+    with pytest.raises(ValueError, match="1 rows have no labels"):
+        libsvm.load(str(p), unlabeled="error")
 
 
 @pytest.mark.parametrize("text,what", [
