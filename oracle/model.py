@@ -9,6 +9,10 @@ update with the learning rate.
 
 Readings where the paper is silent (each is listed in the design notes):
 * two weight matrices, F -> H (ReLU) -> L, with biases b1 and b2 (zero init);
+  the other reading of "3-layer MLP", a second dense hidden layer H -> H
+  (ReLU) with weights Wh [H x H] and bias bh, is available with
+  ``extra_hidden_layers=1`` (its product is always exact: the bf16 rounding
+  applies to the output layer only);
 * multi-label target distribution T[i, y] = 1/|Y_i| on the true labels, loss
   = mean over the batch of the cross-entropy between T and the softmax;
 * gradients averaged over the batch (mean), ReLU'(0) = 0;
@@ -41,6 +45,7 @@ _M2 = np.uint64(0x94D049BB133111EB)
 
 TENSOR_W1 = 0
 TENSOR_W2 = 1
+TENSOR_WH = 2
 
 
 def splitmix64(x: np.ndarray) -> np.ndarray:
@@ -67,16 +72,22 @@ def xavier_bound(fan_in: int, fan_out: int) -> np.float32:
     return F32(np.sqrt(6.0 / (fan_in + fan_out)))
 
 
-def init_params(n_features: int, n_labels: int, hidden: int, seed: int) -> dict:
-    """W1 [F,H], W2 [L,H] Xavier-uniform; b1 [H], b2 [L] zero.  w = fl32(fl32(2u-1) * a)."""
-    a1 = xavier_bound(n_features, hidden)
-    a2 = xavier_bound(hidden, n_labels)
-    u1 = init_uniform24(seed, TENSOR_W1, n_features * hidden)
-    u2 = init_uniform24(seed, TENSOR_W2, n_labels * hidden)
-    w1 = (2.0 * u1 - 1.0).astype(F32) * a1   # 2u-1 is exact in float32; one rounding in the product
-    w2 = (2.0 * u2 - 1.0).astype(F32) * a2
-    return dict(W1=w1.reshape(n_features, hidden), b1=np.zeros(hidden, F32),
-                W2=w2.reshape(n_labels, hidden), b2=np.zeros(n_labels, F32))
+def _xavier_tensor(seed: int, tensor: int, fan_in: int, fan_out: int, count: int) -> np.ndarray:
+    a = xavier_bound(fan_in, fan_out)
+    u = init_uniform24(seed, tensor, count)
+    return (2.0 * u - 1.0).astype(F32) * a   # 2u-1 is exact in float32; one rounding in the product
+
+
+def init_params(n_features: int, n_labels: int, hidden: int, seed: int, extra_hidden_layers: int = 0) -> dict:
+    """W1 [F,H], W2 [L,H] (and Wh [H,H]) Xavier-uniform; biases zero.  w = fl32(fl32(2u-1) * a)."""
+    p = dict(W1=_xavier_tensor(seed, TENSOR_W1, n_features, hidden, n_features * hidden).reshape(n_features, hidden),
+             b1=np.zeros(hidden, F32))
+    if extra_hidden_layers:
+        p["Wh"] = _xavier_tensor(seed, TENSOR_WH, hidden, hidden, hidden * hidden).reshape(hidden, hidden)
+        p["bh"] = np.zeros(hidden, F32)
+    p["W2"] = _xavier_tensor(seed, TENSOR_W2, hidden, n_labels, n_labels * hidden).reshape(n_labels, hidden)
+    p["b2"] = np.zeros(n_labels, F32)
+    return p
 
 
 # ----------------------------------------------------------------------------
@@ -137,16 +148,23 @@ def targets(y, n_labels: int) -> np.ndarray:
 # Forward, backward, update
 # ----------------------------------------------------------------------------
 def forward(p: dict, x, y=None, operands: str = "fp32") -> dict:
-    """A1 = X W1 + b1; H1 = ReLU(A1); Z = H1 W2^T + b2; lse; per-row and mean loss."""
+    """A1 = X W1 + b1; H1 = ReLU(A1); [A2 = H1 Wh^T + bh; H2 = ReLU(A2)]; Z = H W2^T + b2
+    with H the last hidden activation; lse; per-row and mean loss."""
     B = len(x.indptr) - 1
     ind, val, rows = _entries(x)
     A1 = np.tile(p["b1"].astype(F64), (B, 1))
     np.add.at(A1, rows, val[:, None] * p["W1"][ind].astype(F64))
     H1 = np.maximum(A1, 0.0)
-    Z = _operand(H1, operands) @ _operand(p["W2"], operands).T + p["b2"].astype(F64)
+    out = dict(A1=A1, H1=H1)
+    Hout = H1
+    if "Wh" in p:
+        A2 = H1 @ p["Wh"].astype(F64).T + p["bh"].astype(F64)
+        Hout = np.maximum(A2, 0.0)
+        out.update(A2=A2, H2=Hout)
+    Z = _operand(Hout, operands) @ _operand(p["W2"], operands).T + p["b2"].astype(F64)
     m = Z.max(axis=1)
     lse = m + np.log(np.exp(Z - m[:, None]).sum(axis=1))
-    out = dict(A1=A1, H1=H1, Z=Z, lse=lse)
+    out.update(Z=Z, lse=lse)
     if y is not None:
         L = Z.shape[1]
         yind, _, yrows = _entries(y)
@@ -168,17 +186,25 @@ def backward(p: dict, x, y, fw: dict, operands: str = "fp32") -> dict:
     # with bf16, dZ (stored as float32 first), H1 and the pre-update W2 are
     # rounded; the bias gradient is a plain sum of the unrounded dZ
     dZo = _operand(dZ.astype(F32), operands) if operands == "bf16" else dZ
-    dW2 = dZo.T @ _operand(fw["H1"], operands)
+    extra = "Wh" in p
+    dW2 = dZo.T @ _operand(fw["H2"] if extra else fw["H1"], operands)
     db2 = dZ.sum(axis=0)
-    dH1 = dZo @ _operand(p["W2"], operands)    # uses the pre-update W2
+    dHo = dZo @ _operand(p["W2"], operands)    # at the output layer's input; the pre-update W2
+    g = dict(dZ=dZ, dW2=dW2, db2=db2)
+    if extra:
+        dA2 = dHo * (fw["A2"] > 0.0)
+        g.update(dH2=dHo, dA2=dA2, dWh=dA2.T @ fw["H1"], dbh=dA2.sum(axis=0))
+        dH1 = dA2 @ p["Wh"].astype(F64)          # the pre-update Wh
+    else:
+        dH1 = dHo
     dA1 = dH1 * (fw["A1"] > 0.0)
     db1 = dA1.sum(axis=0)
     ind, val, rows = _entries(x)
     T_ids, inv = np.unique(ind, return_inverse=True)
     dW1 = np.zeros((len(T_ids), p["W1"].shape[1]), F64)
     np.add.at(dW1, inv, val[:, None] * dA1[rows])
-    return dict(dZ=dZ, dW2=dW2, db2=db2, dH1=dH1, dA1=dA1, db1=db1,
-                touched=T_ids.astype(np.int32), dW1_rows=dW1)
+    g.update(dH1=dH1, dA1=dA1, db1=db1, touched=T_ids.astype(np.int32), dW1_rows=dW1)
+    return g
 
 
 def sgd_update(p: dict, g: dict, lr) -> dict:
@@ -188,6 +214,9 @@ def sgd_update(p: dict, g: dict, lr) -> dict:
     t = g["touched"]
     q["W1"][t] = (p["W1"][t].astype(F64) - lr * g["dW1_rows"]).astype(F32)
     q["b1"] = (p["b1"].astype(F64) - lr * g["db1"]).astype(F32)
+    if "Wh" in p:
+        q["Wh"] = (p["Wh"].astype(F64) - lr * g["dWh"]).astype(F32)
+        q["bh"] = (p["bh"].astype(F64) - lr * g["dbh"]).astype(F32)
     q["W2"] = (p["W2"].astype(F64) - lr * g["dW2"]).astype(F32)
     q["b2"] = (p["b2"].astype(F64) - lr * g["db2"]).astype(F32)
     return q
@@ -214,16 +243,23 @@ def predict_topk(p: dict, x, k: int, operands: str = "fp32"):
     return ids, sc
 
 
+PARAM_ORDER = ("W1", "b1", "Wh", "bh", "W2", "b2")
+
+
 def flat_params(p: dict) -> np.ndarray:
-    """The model as one float32 vector in the order W1, b1, W2, b2."""
-    return np.concatenate([p["W1"].ravel(), p["b1"], p["W2"].ravel(), p["b2"]]).astype(F32)
+    """The model as one float32 vector in the order W1, b1, [Wh, bh,] W2, b2."""
+    return np.concatenate([p[k].ravel() for k in PARAM_ORDER if k in p]).astype(F32)
 
 
-def unflat_params(v: np.ndarray, n_features: int, n_labels: int, hidden: int) -> dict:
+def unflat_params(v: np.ndarray, n_features: int, n_labels: int, hidden: int,
+                  extra_hidden_layers: int = 0) -> dict:
     o = 0
     out = {}
-    for name, shape in (("W1", (n_features, hidden)), ("b1", (hidden,)),
-                        ("W2", (n_labels, hidden)), ("b2", (n_labels,))):
+    shapes = [("W1", (n_features, hidden)), ("b1", (hidden,))]
+    if extra_hidden_layers:
+        shapes += [("Wh", (hidden, hidden)), ("bh", (hidden,))]
+    shapes += [("W2", (n_labels, hidden)), ("b2", (n_labels,))]
+    for name, shape in shapes:
         n = int(np.prod(shape))
         out[name] = np.asarray(v[o:o + n], F32).reshape(shape).copy()
         o += n

@@ -210,6 +210,88 @@ def test_gradients_match_central_finite_differences(seed):
         assert err < 1e-6, (name, err)
 
 
+def _with_extra_layer(p, seed, H, scale=1.0):
+    rng = np.random.default_rng(seed)
+    q = {k: p[k] for k in ("W1", "b1")}
+    q["Wh"] = rng.normal(0, scale, (H, H))
+    q["bh"] = rng.normal(0, 0.1, H)
+    q["W2"], q["b2"] = p["W2"], p["b2"]
+    return q
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_extra_hidden_layer_gradients_match_central_finite_differences(seed):
+    # the other reading of the "3-layer MLP": F -> H (ReLU) -> H (ReLU) -> L
+    x, y, p = tiny_problem(seed=seed + 40)
+    p = _with_extra_layer(p, seed + 50, 5)
+    fw = om.forward(p, x, y)
+    assert np.min(np.abs(fw["A1"])) > 1e-3 and np.min(np.abs(fw["A2"])) > 1e-3   # away from the kinks
+    g = om.backward(p, x, y, fw)
+    eps = 1e-6
+    dense_dW1 = np.zeros_like(p["W1"])
+    dense_dW1[g["touched"]] = g["dW1_rows"]
+    for name, ana in (("W1", dense_dW1), ("b1", g["db1"]), ("Wh", g["dWh"]), ("bh", g["dbh"]),
+                      ("W2", g["dW2"]), ("b2", g["db2"])):
+        num = np.zeros_like(p[name])
+        it = np.nditer(p[name], flags=["multi_index"])
+        for _ in it:
+            j = it.multi_index
+            q = {k: v.copy() for k, v in p.items()}
+            q[name][j] += eps
+            lp = _loss_of(q, x, y)
+            q[name][j] -= 2 * eps
+            lm = _loss_of(q, x, y)
+            num[j] = (lp - lm) / (2 * eps)
+        err = np.max(np.abs(num - ana)) / max(np.max(np.abs(ana)), 1e-12)
+        assert err < 1e-6, (name, err)
+
+
+def test_extra_hidden_layer_dense_form_and_identity_reduction():
+    x, y, p = tiny_problem(seed=45)
+    q = _with_extra_layer(p, 46, 5)
+    fw = om.forward(q, x, y)
+    X = dense_x(x)
+    H1 = np.maximum(X @ p["W1"] + p["b1"], 0)
+    H2 = np.maximum(H1 @ q["Wh"].T + q["bh"], 0)
+    assert np.allclose(fw["Z"], H2 @ p["W2"].T + p["b2"], rtol=1e-13, atol=1e-13)
+    # Wh = I, bh = 0: H2 = ReLU(H1) = H1, so the model is the two-matrix one; its
+    # gradients carry over, and dWh = dA2^T H1 with dA2 = dH1 [H1 > 0]
+    q["Wh"] = np.eye(5)
+    q["bh"] = np.zeros(5)
+    f3, f2 = om.forward(q, x, y), om.forward(p, x, y)
+    assert np.allclose(f3["loss_rows"], f2["loss_rows"], rtol=1e-14, atol=1e-15)
+    g3, g2 = om.backward(q, x, y, f3), om.backward(p, x, y, f2)
+    for k in ("dW2", "db2", "db1", "dW1_rows"):
+        assert np.allclose(g3[k], g2[k], rtol=1e-13, atol=1e-15), k
+    dA2 = g2["dH1"] * (H1 > 0)
+    assert np.allclose(g3["dWh"], dA2.T @ H1, rtol=1e-13, atol=1e-15)
+    assert np.allclose(g3["dbh"], dA2.sum(axis=0), rtol=1e-13, atol=1e-15)
+
+
+def test_extra_hidden_layer_init_and_flat_order():
+    p = om.init_params(40, 9, 128, seed=7, extra_hidden_layers=1)
+    assert list(p) == ["W1", "b1", "Wh", "bh", "W2", "b2"]
+    a = float(om.xavier_bound(128, 128))
+    assert math.isclose(a, math.sqrt(6 / 256), rel_tol=1e-7)
+    assert np.all(np.abs(p["Wh"]) <= a) and np.all(p["bh"] == 0)
+    # tensor 2 of the same seed; the other tensors are those of the two-matrix model
+    u = om.init_uniform24(7, 2, 128 * 128)
+    assert np.array_equal(p["Wh"].ravel(), (2.0 * u - 1.0).astype(np.float32) * np.float32(a))
+    p2 = om.init_params(40, 9, 128, seed=7)
+    assert all(np.array_equal(p[k], p2[k]) for k in p2)
+    v = om.flat_params(p)
+    assert v.size == 40 * 128 + 128 + 128 * 128 + 128 + 9 * 128 + 9
+    back = om.unflat_params(v, 40, 9, 128, extra_hidden_layers=1)
+    assert all(np.array_equal(back[k], p[k]) for k in p)
+    # an SGD step updates Wh and bh against their gradients
+    x = synth.CSR(np.array([0, 2]), np.array([3, 7], np.int32), np.array([0.6, 0.8], np.float32), 40)
+    y = synth.CSR(np.array([0, 1]), np.array([4], np.int32), None, 9)
+    q, loss, g, _ = om.train_step(p, x, y, 0.5)
+    d = q["Wh"].astype(np.float64) - p["Wh"]
+    ulp = np.spacing(np.maximum(np.abs(p["Wh"]), np.abs(q["Wh"]))).astype(np.float64)
+    assert np.all(np.abs(d + 0.5 * g["dWh"]) <= ulp)
+
+
 def test_gradient_invariants():
     x, y, p = tiny_problem(seed=20, B=9, F=30, L=11)
     fw = om.forward(p, x, y)
