@@ -75,7 +75,34 @@ def parse():
                     help="only run 10 plain device copies of 256 MiB (scale for the HBM byte counters)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="budget of the oracle CPU baseline (0 disables it)")
+    ap.add_argument("--ramp", type=int, default=0,
+                    help="only time N steps one by one from an idle GPU (per-step HIP events) and print "
+                         "the step times by window: how long the clocks take to reach their loaded state")
+    ap.add_argument("--settle-ms", type=float, default=400.0,
+                    help="untimed load before the warm-up steps, so that the GPU's clocks have left "
+                         "their idle state (0 disables it)")
     return ap.parse_args()
+
+
+def settle(step, ms: float) -> int:
+    """Run `step(i)` untimed until `ms` milliseconds of wall time have passed.
+
+    After idle the GPU takes tens of milliseconds of load to reach its loaded
+    clocks: per-step event times of the wide-label step measured from a cold
+    start were 0.35 ms for steps 5-25, 0.31 ms for 25-50 and 0.27 ms after
+    step 100, and a 20-step window taken after 0.5 s of idle ran at 0.34 ms.
+    A short timed region right after data generation would measure that ramp,
+    not the kernels, so the warm-up steps start from a loaded GPU."""
+    import torch
+    if ms <= 0:
+        return 0
+    n, t0 = 0, time.perf_counter()
+    while (time.perf_counter() - t0) * 1e3 < ms:
+        for _ in range(8):
+            step(n)
+            n += 1
+        torch.cuda.synchronize()
+    return n
 
 
 def kernel_model(w, B, nnz, lnnz, uniq, splits):
@@ -83,8 +110,10 @@ def kernel_model(w, B, nnz, lnnz, uniq, splits):
     F, L = w.n_features, w.n_labels
     op = 2 if w.gemm_bf16 else 4
     return {
-        # reads the touched W1 rows once, the batch's (id, value) pairs; writes A1 and H1 (2 layouts)
-        "gather": dict(bytes=uniq * H * 4 + nnz * 8 + B * H * (4 + 2 * op), flops=2.0 * nnz * H),
+        # reads the touched W1 rows once, the batch's (id, value) pairs; writes A1 (fp32) and H1
+        # in the operand type (and its transpose, for fp32 operands only)
+        "gather": dict(bytes=uniq * H * 4 + nnz * 8 + B * H * (4 + op * (1 if w.gemm_bf16 else 2)),
+                       flops=2.0 * nnz * H),
         # two radix passes over (key, position) of every feature entry
         "sort": dict(bytes=2 * nnz * 4 * 5, flops=0.0),
         # label entries: read (label, row), write the grouped pairs and the block offsets
@@ -93,8 +122,8 @@ def kernel_model(w, B, nnz, lnnz, uniq, splits):
         "out_fwd": dict(bytes=4.0 * L * (H + 1), flops=4.0 * B * H * L),
         # reads the forward's per-(split, row) partials (max, sum, O), A1 and the target rows of W2
         "out_combine": dict(bytes=splits * B * (H + 2) * 4 + B * H * 4 * 2 + lnnz * H * 4, flops=2.0 * lnnz * H),
-        # reads and writes W2 and b2 once; dW2 = dZ^T H1 (the Z recompute is not counted)
-        "out_bwd": dict(bytes=8.0 * L * (H + 1), flops=2.0 * B * H * L),
+        # reads and writes W2 and b2 once; the logits recomputed (Z = H1 W2^T) and dW2 = dZ^T H1
+        "out_bwd": dict(bytes=8.0 * L * (H + 1), flops=4.0 * B * H * L),
         # reads and writes the touched W1 rows once, the sorted (key, position) pairs, the
         # entries' rows and values; its last workgroup reads dA1 for the b1 update
         "w1_update": dict(bytes=uniq * H * 8 + nnz * 16 + B * H * 4, flops=2.0 * nnz * H + B * H),
@@ -131,13 +160,13 @@ def measured_peaks(n_floats: int, stream):
             "how": "torch mul_ in place over a W2-sized fp32 tensor; torch.matmul 8192^3 bf16"}
 
 
-def measure_gather_saturating(w, stream, rows=2048, reps=20):
+def measure_gather_saturating(w, stream, rows=16384, reps=10):
     """The first-layer gather at a shape that fills the GPU: top-k prediction over
-    `rows` rows of the workload (the library's largest batch: one workgroup of 8
-    waves per row, about two full passes over the chip; its gather is the training
-    step's kernel without the label work), timed with the library's events.  At the
-    training batch the gather is latency-bound; here its rate shows what the kernel
-    sustains."""
+    `rows` rows of the workload (the library's largest prediction batch: one
+    workgroup of 8 waves per row, 16 waves of workgroups per CU; its gather is the
+    training step's kernel without the label work), timed with the library's
+    events.  At the training batch the gather is latency-bound; here its rate shows
+    what the kernel sustains."""
     import torch
     import paper_2110_07029_amd as asgd
     from paper_2110_07029_amd import synth
@@ -165,7 +194,7 @@ def measure_gather_saturating(w, stream, rows=2048, reps=20):
         asgd.asgd_model_free(m)
     avg_s = tot / n * 1e-3
     op = 2 if w.gemm_bf16 else 4
-    out_b = rows * H * (4 + 2 * op)
+    out_b = rows * H * (4 + op * (1 if w.gemm_bf16 else 2))
     compulsory = uniq * H * 4 + nnz * 8 + out_b
     logical = nnz * H * 4 + nnz * 8 + out_b
     return {"rows": rows, "nnz": nnz, "unique_features": uniq, "avg_us": round(avg_s * 1e6, 2),
@@ -225,7 +254,8 @@ def run_elastic(args):
     max_lnnz = int(np.max(ipy[b_max:] - ipy[:-b_max]))
     dx, dy = asgd.DeviceCSR(ds.x), asgd.DeviceCSR(ds.y)
     xa, ya = dx.batch(0, ds.x.n_rows), dy.batch(0, ds.y.n_rows)
-    mcfg = asgd.asgd_config(w.n_features, w.n_labels, H, b_max, max_nnz, max_lnnz, 1 if w.gemm_bf16 else 0, 0)
+    mcfg = asgd.asgd_config(n_features=w.n_features, n_labels=w.n_labels, hidden=H, max_batch=b_max,
+                            max_nnz=max_nnz, max_label_nnz=max_lnnz, gemm_bf16=1 if w.gemm_bf16 else 0)
     ec = asgd.asgd_elastic_config()
     ec.n_replicas, ec.b_min, ec.b_max, ec.beta = n, b_min, b_max, b_min / 2.0
     ec.lr, ec.gamma, ec.weight_mode, ec.perturb = w.lr, 0.9, asgd.ASGD_WEIGHTS_SAMPLES, 0
@@ -235,10 +265,11 @@ def run_elastic(args):
     e = asgd.asgd_elastic_create(ec, mcfg, cfg5["index"] + 2000, streams, gstream)
     xi, yi = ipx.astype(np.int32), ipy.astype(np.int32)
     try:
+        n_settle = settle(lambda i: asgd.asgd_elastic_round(e, xa, ya, xi, yi), args.settle_ms)
         for _ in range(W):
             asgd.asgd_elastic_round(e, xa, ya, xi, yi)
         torch.cuda.synchronize()
-        log(f"warmup done ({W} rounds)")
+        log(f"settle ({n_settle} rounds) and warmup ({W} rounds) done")
         t0 = time.perf_counter()
         samples, bs = 0, []
         for r in range(K):
@@ -251,6 +282,10 @@ def run_elastic(args):
         asgd.asgd_elastic_free(e)
     log(f"timed {K} rounds: {el * 1e3:.1f} ms, final batch sizes {bs[-1] if bs else None}")
     merge = measure_merge(w, n, 10, gstream)
+    cpu = None
+    if args.cpu_seconds > 0:
+        log(f"oracle CPU baseline, ~{args.cpu_seconds:.0f} s budget")
+        cpu = cpu_baseline_elastic(w, ds, b_max, n, mega, args.cpu_seconds)
     return {
         "metric": METRIC, "value": round(samples / el, 1), "unit": "samples/s", "n_gpus": 1, "steps": K,
         "warmup": W, "ms_per_step": round(el * 1e3 / K, 3), "higher_is_better": True, "scaling": "weak",
@@ -261,7 +296,8 @@ def run_elastic(args):
                    "parallelism": "4 replicas on 4 HIP streams", "step": "one round (dispatch + merge)"},
         "roofline": {"kernel": "merge", "bound": "hbm", "achieved": merge["GB/s"], "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": merge["hbm_frac"], "traffic": None},
-        "cpu_baseline": None,
+        "cpu_baseline": cpu,
+        "settle": {"ms": args.settle_ms, "rounds": n_settle},
         "kernels": {"merge": merge},
         "batch_sizes_per_round": bs,
     }
@@ -293,6 +329,51 @@ def _cpu_model():
     except OSError:  # pragma: no cover - not Linux
         pass
     return None
+
+
+def ramp(m, xs, ys, lr, n, stream, idle_s=2.0):
+    """Step times from an idle GPU: after `idle_s` seconds without work, n steps
+    each bracketed by HIP events on the model's stream."""
+    import torch
+    import paper_2110_07029_amd as asgd
+    torch.cuda.synchronize()
+    time.sleep(idle_s)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    ev[0].record(stream)
+    for i in range(n):
+        asgd.asgd_train_step(m, xs[i % len(xs)], ys[i % len(xs)], lr)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    t = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(n)])
+    edges = [e for e in (0, 5, 25, 50, 100, 200, 400, 800, 1600) if e < n] + [n]
+    return {"idle_s": idle_s, "steps": n, "first_10_ms": [round(v, 4) for v in t[:10]],
+            "windows_ms": {f"{a}-{b}": round(float(t[a:b].mean()), 4) for a, b in zip(edges, edges[1:])}}
+
+
+def cpu_baseline_elastic(w, ds, b, n_rep, mega, budget_s):
+    """The oracle on a bounded sample of an elastic round: steps of one replica at
+    batch b (the replicas' starting size) within most of the budget, and one
+    oracle merge of n_rep replicas with momentum; a round of `mega` samples is
+    then mega/b such steps plus one merge."""
+    from oracle import elastic as oe
+    from oracle import model as om
+    n_steps, samples, el = _oracle_steps(w, ds, b, 0.75 * budget_s, 4)
+    g = om.flat_params(om.init_params(w.n_features, w.n_labels, H, w.init_seed))
+    reps = [g.copy() for _ in range(n_rep)]
+    t0 = time.perf_counter()
+    oe.merge(g, g, reps, [1.0 / n_rep] * n_rep, 0.9)
+    t_merge = time.perf_counter() - t0
+    t_step = el / n_steps
+    t_round = (mega / b) * t_step + t_merge
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        cores = os.cpu_count() or 1
+    return {"value": mega / t_round, "unit": "samples/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{n_steps} oracle steps x {b} rows of {w.name} ({t_step:.1f} s each) and one oracle "
+                      f"merge of {n_rep} replicas ({t_merge:.1f} s), scaled to a round of {mega} samples",
+            "cpu_model": _cpu_model(), "host_cpus": os.cpu_count()}
 
 
 def cpu_baseline(w, ds, B, budget_s):
@@ -346,6 +427,8 @@ def main():
     w = synth.WORKLOADS[args.workload]
     B = args.batch or w.batch
     K, W = args.steps, args.warmup
+    if args.ramp:
+        K, W = args.ramp, 0
     n_samples = min(w.n_samples, (K + W) * B)
     log(f"workload {w.name}: F={w.n_features} L={w.n_labels} B={B}; generating {n_samples} samples")
     ds = synth.generate(w, n_samples=n_samples)
@@ -362,10 +445,14 @@ def main():
                              seed=w.init_seed, stream=stream)
     try:
         lr = w.lr
+        if args.ramp:
+            print(json.dumps(ramp(m, xs, ys, lr, args.ramp, stream)), flush=True)
+            return
+        n_settle = settle(lambda i: asgd.asgd_train_step(m, xs[i % n_full], ys[i % n_full], lr), args.settle_ms)
         for i in range(W):
             asgd.asgd_train_step(m, xs[i % n_full], ys[i % n_full], lr)
         torch.cuda.synchronize()
-        log(f"warmup done ({W} steps)")
+        log(f"settle ({n_settle} steps, {args.settle_ms:.0f} ms) and warmup ({W} steps) done")
         # timed region: K steps with no per-kernel events on the stream
         t_start = torch.cuda.Event(enable_timing=True)
         t_end = torch.cuda.Event(enable_timing=True)
@@ -456,6 +543,8 @@ def main():
                    "parallelism": "single replica"},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "settle": {"ms": args.settle_ms, "steps": n_settle,
+                   "why": "untimed load before the warm-up steps: the GPU's clocks ramp for tens of ms after idle"},
         "kernels": kernels,
     }
     print(json.dumps(out), flush=True)

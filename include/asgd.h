@@ -13,8 +13,11 @@
  * Model:  A1 = X W1 + b1 ; H1 = ReLU(A1) ; Z = H1 W2^T + b2
  *         loss = mean_i [ logsumexp_j Z_ij - (1/|Y_i|) sum_{y in Y_i} Z_iy ]
  *         (target distribution 1/|Y_i| on each true label; mean over the batch)
+ *         With extra_hidden_layers = 1 (the other reading of the paper's
+ *         "3-layer MLP"): A2 = H1 Wh^T + bh ; H2 = ReLU(A2) ; Z = H2 W2^T + b2.
  * Shapes: W1 [F x H] row-major, b1 [H], W2 [L x H] row-major (label-major),
- *         b2 [L]; H = 128.  Parameters are float32.
+ *         b2 [L], Wh [H x H] row-major (output unit, input unit), bh [H];
+ *         H = 128.  Parameters are float32.
  *
  * Conventions shared by every entry point
  *  - Every call returns an asgd_status and never throws or aborts.  On a
@@ -57,19 +60,24 @@ typedef enum asgd_status {
 } asgd_status;
 
 /* asgd_config.flags */
-#define ASGD_VALIDATE 0x1u /* check CSR content on the device and synchronize each step */
+#define ASGD_VALIDATE 0x1u       /* check CSR content on the device and synchronize each step */
+#define ASGD_UNFUSED_OUTPUT 0x2u /* materialize the logits Z [B x L] fp32 and run the softmax and
+                                    cross-entropy as a standalone pass over them (the textbook
+                                    layer-by-layer output layer); default: fused, Z never stored */
 
 typedef struct asgd_config {
   int32_t n_features;    /* F in [1, 2^22) */
   int32_t n_labels;      /* L in [1, 2^22) */
   int32_t hidden;        /* H; must be 128 */
-  int32_t max_batch;     /* largest B any call will use, in [1, 2048] (memory pool sized for it, Sec. 4) */
+  int32_t extra_hidden_layers; /* 0, or 1 for a second dense ReLU layer H -> H (Wh, bh) */
+  int32_t max_batch;     /* largest B any call will use, in [1, 16384] (memory pool sized for it,
+                            Sec. 4); training steps take at most 2048 rows, prediction all 16384 */
   int32_t max_nnz;       /* largest sum of nnz over the rows of one batch (>= 0) */
   int32_t max_label_nnz; /* largest sum of |Y_i| over the rows of one batch (>= 0;
                             max_nnz + max_label_nnz < 2^30) */
   int32_t gemm_bf16;     /* 1: output-layer products on bf16 operands with fp32 accumulation
                             (fp32 master weights); 0: fp32 operands */
-  uint32_t flags;        /* ASGD_VALIDATE or 0 */
+  uint32_t flags;        /* ASGD_VALIDATE | ASGD_UNFUSED_OUTPUT, or 0 */
 } asgd_config;
 
 /* A CSR row block living in device memory.  Row i spans entries
@@ -92,7 +100,9 @@ enum {
   ASGD_PARAM_W1 = 0,
   ASGD_PARAM_B1 = 1,
   ASGD_PARAM_W2 = 2,
-  ASGD_PARAM_B2 = 3
+  ASGD_PARAM_B2 = 3,
+  ASGD_PARAM_WH = 4, /* models with extra_hidden_layers = 1 only (EINVAL otherwise) */
+  ASGD_PARAM_BH = 5
 };
 
 /* Merge-weight modes (Alg. 2). */
@@ -110,14 +120,15 @@ enum {
 /* Create a model and its workspace (Sec. 4 "Scalable Memory Management":
  * everything is allocated once, for the largest batch).  W1 and W2 are
  * Xavier-uniform with half-width a = fl32(sqrt(6/(fan_in+fan_out))), fans
- * (F,H) and (H,L); element e of tensor t (0 = W1, 1 = W2, row-major) is
+ * (F,H), (H,L) and (H,H); element e of tensor t (0 = W1, 1 = W2, 2 = Wh, row-major) is
  * fl32(fl32(2u-1) * a) with u = (splitmix64(seed ^ (t << 56) ^ e) >> 40) * 2^-24,
  * splitmix64 being the published generator's output for that state.  Biases
  * start at 0.  Initialisation runs on `hip_stream`; the call returns once it
  * has completed.  *out receives the model; nothing is allocated on error.
  * Errors: EINVAL for a NULL argument, a count below 1 (0 for the nnz maxima),
- * hidden != 128, gemm_bf16 not 0 or 1 or unknown flag bits; ERANGE for F or L
- * at or above 2^22 (F + L below 2^30), max_batch outside [1, 2048] or
+ * hidden != 128, gemm_bf16 or extra_hidden_layers not 0 or 1 or unknown flag
+ * bits; ERANGE for F or L
+ * at or above 2^22 (F + L below 2^30), max_batch outside [1, 16384] or
  * max_nnz + max_label_nnz at or above 2^30; ENOMEM / EHIP when the device
  * allocation or the initialisation fails. */
 asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t seed,
@@ -134,11 +145,11 @@ asgd_status asgd_model_set_stream(asgd_model* m, void* hip_stream);
  * stream after src's pending work. */
 asgd_status asgd_model_copy(asgd_model* dst, const asgd_model* src);
 
-/* Number of parameters P = F*H + H + L*H + L. */
+/* Number of parameters P = F*H + H + L*H + L (+ H*H + H with the second hidden layer). */
 asgd_status asgd_model_num_params(const asgd_model* m, int64_t* out);
 
 /* Copy one parameter tensor to / from host memory (synchronous).  `bytes`
- * must equal the tensor's size in bytes (F*H*4, H*4, L*H*4 or L*4). */
+ * must equal the tensor's size in bytes (F*H*4, H*4, L*H*4, L*4, H*H*4 or H*4). */
 asgd_status asgd_model_get_params(const asgd_model* m, int32_t which, void* host, size_t bytes);
 asgd_status asgd_model_set_params(asgd_model* m, int32_t which, const void* host, size_t bytes);
 
@@ -146,7 +157,8 @@ asgd_status asgd_model_set_params(asgd_model* m, int32_t which, const void* host
 /* The per-replica step (Sec. 2.1: forward, backward, update)                */
 /* ------------------------------------------------------------------------ */
 
-/* One SGD step on the batch (x, y), B = x->n_rows = y->n_rows, 1 <= B <= max_batch:
+/* One SGD step on the batch (x, y), B = x->n_rows = y->n_rows, 1 <= B <= min(max_batch, 2048)
+ * (ERANGE above):
  * gradients of the mean loss, then theta <- theta - lr * g for W2, b2, b1 and
  * for the rows of W1 whose feature occurs in the batch; other W1 rows are
  * not written.  If loss_out is non-NULL the call synchronizes the stream and
@@ -162,7 +174,7 @@ asgd_status asgd_model_last_loss(asgd_model* m, float* loss_out);
 /* Top-k labels per row of x by logit Z (ties: smaller label id first), the
  * prediction used for the paper's top-1 accuracy (Sec. 5.1 "Methodology").
  * ids_dev: device int32 [B x k]; scores_dev: device float [B x k] or NULL.
- * 1 <= k <= 32 and k <= L.  Asynchronous. */
+ * 1 <= k <= 32 and k <= L; B up to max_batch (16384 at most).  Asynchronous. */
 asgd_status asgd_predict_topk(asgd_model* m, const asgd_csr* x, int32_t k, int32_t* ids_dev,
                               float* scores_dev);
 
@@ -300,11 +312,14 @@ asgd_status asgd_elastic_model(asgd_elastic* e, int32_t which /* -1 global, else
 /* Inspection of intermediates (parity tests)                                */
 /* ------------------------------------------------------------------------ */
 
-/* Forward pass only (no update): a1_dev [B x H] pre-activation, lse_dev [B]
+/* Forward pass only (no update): a1_dev [B x H] the first layer's
+ * pre-activation, z_dev [B x L] the logits Z (row-major; written by the
+ * logits kernel of the stored-logits path, in either output mode), lse_dev [B]
  * log-sum-exp of the logits, loss_rows_dev [B] per-row loss (needs y; may be
- * NULL together with y).  Device outputs, asynchronous. */
+ * NULL together with y).  Every output may be NULL.  Device outputs,
+ * asynchronous. */
 asgd_status asgd_debug_forward(asgd_model* m, const asgd_csr* x, const asgd_csr* y, float* a1_dev,
-                               float* lse_dev, float* loss_rows_dev);
+                               float* z_dev, float* lse_dev, float* loss_rows_dev);
 
 /* Sorted distinct feature ids of the batch (the W1 rows a step writes), as
  * computed by the step's sort-by-feature pass.  ids_dev: device [>= nnz];
@@ -359,7 +374,12 @@ enum {
   ASGD_K_MERGE = 7,       /* normalized merge (timed on the global model) */
   ASGD_K_LABELS = 8,      /* (label, row) pairs grouped by label block: a workgroup of the
                              OUT_FWD launch, so never recorded on its own */
-  ASGD_K_COUNT = 9
+  ASGD_K_DENSE_FWD = 9,   /* second hidden layer forward (extra_hidden_layers = 1) */
+  ASGD_K_DENSE_BWD = 10,  /* second hidden layer: dA1, and the Wh / bh update */
+  ASGD_K_LOGITS = 11,     /* unfused output: the logits Z written to memory */
+  ASGD_K_SOFTMAX = 12,    /* unfused output: the softmax / cross-entropy pass over Z (lse, loss) */
+  ASGD_K_DH = 13,         /* unfused output: dH = dZ W2 from the stored Z, and dA */
+  ASGD_K_COUNT = 14
 };
 
 /* enable != 0: from now on, bracket each kernel group launched for this model

@@ -5,8 +5,8 @@ the work; this package holds its ctypes binding (same names as the C entry
 points), device-resident datasets and the seeded synthetic input generator.
 """
 from ._binding import (  # noqa: F401
-    ASGD_OK, ASGD_EINVAL, ASGD_ERANGE, ASGD_ENOMEM, ASGD_EHIP, ASGD_ESTATE, ASGD_VALIDATE,
-    ASGD_PARAM_W1, ASGD_PARAM_B1, ASGD_PARAM_W2, ASGD_PARAM_B2, ASGD_WEIGHTS_ALG2,
+    ASGD_OK, ASGD_EINVAL, ASGD_ERANGE, ASGD_ENOMEM, ASGD_EHIP, ASGD_ESTATE, ASGD_VALIDATE, ASGD_UNFUSED_OUTPUT,
+    ASGD_PARAM_W1, ASGD_PARAM_B1, ASGD_PARAM_W2, ASGD_PARAM_B2, ASGD_PARAM_WH, ASGD_PARAM_BH, ASGD_WEIGHTS_ALG2,
     ASGD_WEIGHTS_SAMPLES, ASGD_WEIGHTS_UNIFORM, ASGD_DISPATCH_DYNAMIC, ASGD_DISPATCH_STATIC, EXPORTS, HIDDEN, AsgdError, asgd_config, asgd_csr, load, library_path,
     asgd_last_error, asgd_model_init, asgd_model_free, asgd_model_set_stream, asgd_model_copy,
     asgd_model_num_params, asgd_model_get_params, asgd_model_set_params, asgd_train_step,

@@ -18,7 +18,8 @@ LIB_PATH = os.path.join(_PKG, "libasgd.so")
 
 ASGD_OK, ASGD_EINVAL, ASGD_ERANGE, ASGD_ENOMEM, ASGD_EHIP, ASGD_ESTATE = 0, -1, -2, -3, -4, -5
 ASGD_VALIDATE = 0x1
-ASGD_PARAM_W1, ASGD_PARAM_B1, ASGD_PARAM_W2, ASGD_PARAM_B2 = 0, 1, 2, 3
+ASGD_UNFUSED_OUTPUT = 0x2
+ASGD_PARAM_W1, ASGD_PARAM_B1, ASGD_PARAM_W2, ASGD_PARAM_B2, ASGD_PARAM_WH, ASGD_PARAM_BH = 0, 1, 2, 3, 4, 5
 ASGD_WEIGHTS_ALG2, ASGD_WEIGHTS_SAMPLES, ASGD_WEIGHTS_UNIFORM = 0, 1, 2
 ASGD_DISPATCH_DYNAMIC, ASGD_DISPATCH_STATIC = 0, 1
 HIDDEN = 128
@@ -37,7 +38,8 @@ EXPORTS = (
 ASGD_CLOCK_TIMED, ASGD_CLOCK_VIRTUAL = 0, 1
 
 # Kernel groups of asgd_model_get_timing.
-KERNELS = ("gather", "sort", "out_fwd", "out_combine", "hidden", "out_bwd", "w1_update", "merge", "labels")
+KERNELS = ("gather", "sort", "out_fwd", "out_combine", "hidden", "out_bwd", "w1_update", "merge", "labels",
+           "dense_fwd", "dense_bwd", "logits", "softmax", "dh")
 
 
 class AsgdError(RuntimeError):
@@ -48,7 +50,7 @@ class AsgdError(RuntimeError):
 
 class asgd_config(ctypes.Structure):
     _fields_ = [("n_features", c_int32), ("n_labels", c_int32), ("hidden", c_int32),
-                ("max_batch", c_int32), ("max_nnz", c_int32), ("max_label_nnz", c_int32),
+                ("extra_hidden_layers", c_int32), ("max_batch", c_int32), ("max_nnz", c_int32), ("max_label_nnz", c_int32),
                 ("gemm_bf16", c_int32), ("flags", c_uint32)]
 
 
@@ -100,7 +102,7 @@ def _declare(lib):
                                          c_int32, POINTER(c_double), c_double, c_double, POINTER(c_float)]),
         "asgd_scale_batches": (c_int32, [c_int32, POINTER(c_int32), POINTER(c_int32), POINTER(c_float),
                                          c_int32, c_int32, c_double]),
-        "asgd_debug_forward": (c_int32, [P, POINTER(asgd_csr), POINTER(asgd_csr), P, P, P]),
+        "asgd_debug_forward": (c_int32, [P, POINTER(asgd_csr), POINTER(asgd_csr), P, P, P, P]),
         "asgd_debug_touched_rows": (c_int32, [P, POINTER(asgd_csr), P, POINTER(c_int32)]),
         "asgd_libsvm_scan": (c_int32, [ctypes.c_char_p, c_int32, POINTER(asgd_libsvm_info)]),
         "asgd_libsvm_read": (c_int32, [ctypes.c_char_p, c_int32, POINTER(asgd_libsvm_info), P, P, P, P, P]),
@@ -169,9 +171,10 @@ def asgd_last_error() -> str:
 
 def asgd_model_init(n_features: int, n_labels: int, max_batch: int, max_nnz: int, max_label_nnz: int,
                     gemm_bf16: bool = True, seed: int = 0, stream=None, flags: int = 0,
-                    hidden: int = HIDDEN) -> int:
-    cfg = asgd_config(n_features, n_labels, hidden, max_batch, max_nnz, max_label_nnz,
-                      1 if gemm_bf16 else 0, flags)
+                    hidden: int = HIDDEN, extra_hidden_layers: int = 0) -> int:
+    cfg = asgd_config(n_features=n_features, n_labels=n_labels, hidden=hidden,
+                      extra_hidden_layers=extra_hidden_layers, max_batch=max_batch, max_nnz=max_nnz,
+                      max_label_nnz=max_label_nnz, gemm_bf16=1 if gemm_bf16 else 0, flags=flags)
     h = c_void_p()
     _check(load().asgd_model_init(byref(h), byref(cfg), c_uint64(seed & (2 ** 64 - 1)), _stream(stream)),
            "asgd_model_init")
@@ -197,8 +200,8 @@ def asgd_model_num_params(m: int) -> int:
 
 
 def _param_shape(which: int, F: int, L: int):
-    return {ASGD_PARAM_W1: (F, HIDDEN), ASGD_PARAM_B1: (HIDDEN,),
-            ASGD_PARAM_W2: (L, HIDDEN), ASGD_PARAM_B2: (L,)}[which]
+    return {ASGD_PARAM_W1: (F, HIDDEN), ASGD_PARAM_B1: (HIDDEN,), ASGD_PARAM_W2: (L, HIDDEN),
+            ASGD_PARAM_B2: (L,), ASGD_PARAM_WH: (HIDDEN, HIDDEN), ASGD_PARAM_BH: (HIDDEN,)}[which]
 
 
 def asgd_model_get_params(m: int, which: int, shape) -> np.ndarray:
@@ -267,9 +270,9 @@ def asgd_scale_batches(u, b, lr, b_min: int, b_max: int, beta: float):
     return list(Bv[:]), [float(v) for v in LR[:]]
 
 
-def asgd_debug_forward(m: int, x: asgd_csr, y, a1_dev=None, lse_dev=None, loss_rows_dev=None):
+def asgd_debug_forward(m: int, x: asgd_csr, y, a1_dev=None, z_dev=None, lse_dev=None, loss_rows_dev=None):
     _check(load().asgd_debug_forward(m, byref(x), byref(y) if y is not None else None,
-                                     _ptr(a1_dev), _ptr(lse_dev), _ptr(loss_rows_dev)),
+                                     _ptr(a1_dev), _ptr(z_dev), _ptr(lse_dev), _ptr(loss_rows_dev)),
            "asgd_debug_forward")
 
 

@@ -1,7 +1,7 @@
 // Model object, memory pool and the C ABI of include/asgd.h.
 //
-// A model owns one parameter allocation [W1 | b1 | W2 | b2] (each section
-// padded to 64 floats so the merge streams it as one float4 vector) and one
+// A model owns one parameter allocation [W1 | b1 | (Wh | bh) | W2 | b2] (each
+// section padded to 64 floats so the merge streams it as one float4 vector) and one
 // workspace allocation carved into the buffers every call needs, sized once
 // for the largest batch (the memory pool of Sec. 4 "Scalable Memory
 // Management": nothing is allocated while training).
@@ -38,7 +38,8 @@ asgd_status fail_hip(hipError_t e, const char* what) {
   } while (0)
 
 constexpr int64_t kAlign = 64;  // floats
-constexpr int kMaxBatch = 2048;
+constexpr int kMaxBatch = 16384;      // rows of one prediction call
+constexpr int kMaxTrainBatch = 2048;  // rows of one training step (and of the inspection calls)
 // The output-layer forward runs one persistent workgroup per CU except
 // kAuxCus, which stay free for the feature sort on the internal stream and
 // the forward launch's own label-grouping workgroup.
@@ -69,6 +70,8 @@ struct asgd_model {
   asgd_config cfg;
   int F = 0, L = 0;
   bool bf16 = true;
+  bool extra = false;    // second dense hidden layer (Wh, bh)
+  bool unfused = false;  // logits stored, softmax / cross-entropy as a pass of its own
   hipStream_t stream = nullptr;
   int device = 0;
   int n_cu = 256;
@@ -80,9 +83,11 @@ struct asgd_model {
 
   // parameters
   float* params = nullptr;
-  int64_t off_b1 = 0, off_W2 = 0, off_b2 = 0, n_pad = 0, n_params = 0;
+  int64_t off_b1 = 0, off_Wh = 0, off_bh = 0, off_W2 = 0, off_b2 = 0, n_pad = 0, n_params = 0;
   float* W1() const { return params; }
   float* b1() const { return params + off_b1; }
+  float* Wh() const { return params + off_Wh; }
+  float* bh() const { return params + off_bh; }
   float* W2() const { return params + off_W2; }
   float* b2() const { return params + off_b2; }
 
@@ -91,7 +96,9 @@ struct asgd_model {
   int rows_pad_max = 0;  // rows of the output-layer operands
   int elem = 2;          // bytes per operand element
   float* A1 = nullptr;
-  void* H1 = nullptr;
+  float* A2 = nullptr;   // second hidden layer: pre-activation and its gradient
+  float* dA2 = nullptr;
+  void* H1 = nullptr;    // the output layer's input in its operand type (H1, or H2 with the extra layer)
   void* H1T = nullptr;
   float* dA1 = nullptr;
   float* lse = nullptr;
@@ -116,6 +123,10 @@ struct asgd_model {
   float* s_part = nullptr;
   float* o_part = nullptr;
   int64_t part_rows = 0;  // capacity in (split, row) pairs
+  float* Z = nullptr;     // stored logits [rows_pad_max x ldz] (unfused output only)
+  int ldz = 0;
+  float* sm_m = nullptr;  // softmax partials per (column chunk, row)
+  float* sm_s = nullptr;
   float* tk_s = nullptr;
   int32_t* tk_i = nullptr;
   int64_t tk_rows = 0;
@@ -159,6 +170,8 @@ int64_t layout_workspace(asgd_model* m, char* base) {
   }
   char* p = base;
   m->A1 = carve<float>(p, (int64_t)rp * HID);
+  m->A2 = carve<float>(p, m->extra ? (int64_t)rp * HID : 0);
+  m->dA2 = carve<float>(p, m->extra ? (int64_t)rp * HID : 0);
   m->H1 = carve<char>(p, (int64_t)rp * HID * m->elem);
   m->H1T = carve<char>(p, (int64_t)rp * HID * m->elem);
   m->dA1 = carve<float>(p, (int64_t)rp * HID);
@@ -187,6 +200,11 @@ int64_t layout_workspace(asgd_model* m, char* base) {
   m->s_part = carve<float>(p, part_rows);
   m->o_part = carve<float>(p, part_rows * HID);
   m->part_rows = part_rows;
+  m->ldz = n_tiles * OUT_TILE;
+  const int64_t sm_rows = m->unfused ? (int64_t)softmax_splits(m->ldz) * rp : 0;
+  m->Z = carve<float>(p, m->unfused ? (int64_t)rp * m->ldz : 0);
+  m->sm_m = carve<float>(p, sm_rows);
+  m->sm_s = carve<float>(p, sm_rows);
   m->tk_s = carve<float>(p, tk_rows * 32);
   m->tk_i = carve<int32_t>(p, tk_rows * 32);
   m->tk_rows = tk_rows;
@@ -212,11 +230,13 @@ CsrDev dev(const asgd_csr* a) {
   return CsrDev{a->n_rows, a->n_cols, a->nnz, a->indptr, a->indices, a->values};
 }
 
-asgd_status check_batch(asgd_model* m, const asgd_csr* x, const asgd_csr* y) {
+asgd_status check_batch(asgd_model* m, const asgd_csr* x, const asgd_csr* y, bool train = true) {
   asgd_status s = check_csr(x, "x", m->F, true, m->cfg.max_nnz);
   if (s) return s;
   if (x->n_rows > m->cfg.max_batch)
     return fail(ASGD_ERANGE, "batch larger than the model's max_batch");
+  if (train && x->n_rows > kMaxTrainBatch)
+    return fail(ASGD_ERANGE, "batches of more than 2048 rows are for prediction only");
   if (y) {
     s = check_csr(y, "y", m->L, false, m->cfg.max_label_nnz);
     if (s) return s;
@@ -277,6 +297,9 @@ asgd_status run_gather(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int*
   TIMED(m, ASGD_K_GATHER, launch_gather_fwd(m->bf16, xd, y ? &yd : nullptr, m->W1(), m->b1(), m->F, m->L, m->A1,
                             m->H1, m->H1T, rows_pad, m->rows_pad_max, m->keys, m->row_of, m->lkeys, m->lrow,
                             m->rw, m->err, validate ? 1 : 0, m->stream));
+  if (m->extra)
+    TIMED(m, ASGD_K_DENSE_FWD, launch_dense_fwd(m->bf16, m->A1, m->Wh(), m->bh(), B, rows_pad, m->A2, m->H1,
+                                                m->H1T, m->rows_pad_max, m->stream));
   if (validate) {
     int32_t e = 0;
     HIP_TRY(hipMemcpyAsync(&e, m->err, sizeof(e), hipMemcpyDeviceToHost, m->stream));
@@ -314,8 +337,33 @@ asgd_status run_forward(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int
                                m->s_part, m->o_part, rows_pad, labels, &m->label_plan, m->stream));
   CsrDev yd = y ? dev(y) : CsrDev{};
   TIMED(m, ASGD_K_OUT_COMBINE, launch_out_combine(m->bf16, B, s_eff, m->m_part, m->s_part, m->o_part, rows_pad, m->W2(),
-                             m->b2(), m->L, m->H1, m->A1, y ? &yd : nullptr, m->lse, m->loss_rows,
-                             m->dA1, m->stream));
+                             m->b2(), m->L, m->H1, m->extra ? m->A2 : m->A1, y ? &yd : nullptr, m->lse,
+                             m->loss_rows, m->extra ? m->dA2 : m->dA1, m->stream));
+  return ASGD_OK;
+}
+
+// The output layer with stored logits: the labels grouped for the backward (a
+// launch of its own here), Z written by the logits kernel, lse and the loss rows
+// from one pass over Z, then dA (dA2 with the second hidden layer) from P W2
+// with P read back from Z.
+asgd_status run_forward_unfused(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int rows_pad,
+                                const LabelJob* labels) {
+  const int B = x->n_rows;
+  const int splits = fwd_splits(m, B);
+  const int n_tiles = (m->L + OUT_TILE - 1) / OUT_TILE;
+  const int tps = (n_tiles + splits - 1) / splits;
+  const int s_eff = (n_tiles + tps - 1) / tps;
+  if ((int64_t)s_eff * rows_pad > m->part_rows) return fail(ASGD_ERANGE, "partial buffer too small");
+  if (labels) TIMED(m, ASGD_K_LABELS, launch_label_blocks(*labels, m->L, m->stream));
+  TIMED(m, ASGD_K_LOGITS, launch_out_logits(m->bf16, m->W2(), m->b2(), m->L, m->H1, B, m->Z, m->ldz, 0,
+                                            m->stream));
+  CsrDev yd = y ? dev(y) : CsrDev{};
+  TIMED(m, ASGD_K_SOFTMAX, launch_softmax_ce(m->Z, m->ldz, B, m->sm_m, m->sm_s, rows_pad, y ? &yd : nullptr,
+                                             m->lse, m->loss_rows, m->stream));
+  if (y)
+    TIMED(m, ASGD_K_DH, launch_unfused_dh(m->bf16, m->W2(), m->b2(), m->L, m->Z, m->ldz, m->lse, B, splits,
+                                          m->o_part, rows_pad, yd, m->rw, m->extra ? m->A2 : m->A1,
+                                          m->extra ? m->dA2 : m->dA1, m->stream));
   return ASGD_OK;
 }
 
@@ -346,13 +394,15 @@ asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t s
   if (cfg->n_features >= (1 << 22))  // so are the rows of W1 in its sparse update
     return fail(ASGD_ERANGE, "n_features must be < 2^22");
   if (cfg->max_batch < 1 || cfg->max_batch > kMaxBatch)
-    return fail(ASGD_ERANGE, "max_batch must be in [1, 2048]");
+    return fail(ASGD_ERANGE, "max_batch must be in [1, 16384]");
   if (cfg->max_nnz < 0 || cfg->max_label_nnz < 0)
     return fail(ASGD_EINVAL, "max_nnz and max_label_nnz must be >= 0");
   if ((int64_t)cfg->max_nnz + cfg->max_label_nnz >= (1LL << 30))
     return fail(ASGD_ERANGE, "max_nnz + max_label_nnz must be < 2^30");
   if (cfg->gemm_bf16 != 0 && cfg->gemm_bf16 != 1) return fail(ASGD_EINVAL, "gemm_bf16 must be 0 or 1");
-  if (cfg->flags & ~ASGD_VALIDATE) return fail(ASGD_EINVAL, "unknown flag bits");
+  if (cfg->extra_hidden_layers != 0 && cfg->extra_hidden_layers != 1)
+    return fail(ASGD_EINVAL, "extra_hidden_layers must be 0 or 1");
+  if (cfg->flags & ~(ASGD_VALIDATE | ASGD_UNFUSED_OUTPUT)) return fail(ASGD_EINVAL, "unknown flag bits");
 
   asgd_model* m = new (std::nothrow) asgd_model();
   if (!m) return fail(ASGD_ENOMEM, "host allocation failed");
@@ -360,15 +410,19 @@ asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t s
   m->F = cfg->n_features;
   m->L = cfg->n_labels;
   m->bf16 = cfg->gemm_bf16 == 1;
+  m->extra = cfg->extra_hidden_layers == 1;
+  m->unfused = (cfg->flags & ASGD_UNFUSED_OUTPUT) != 0;
   m->elem = m->bf16 ? 2 : 4;
   m->stream = (hipStream_t)hip_stream;
   m->rows_pad_max = (int)round_up(cfg->max_batch, out_rows_per_block(m->bf16));
   const int64_t F = m->F, L = m->L;
   m->off_b1 = round_up(F * HID, kAlign);
-  m->off_W2 = m->off_b1 + round_up(HID, kAlign);
+  m->off_Wh = m->off_b1 + round_up(HID, kAlign);
+  m->off_bh = m->off_Wh + (m->extra ? round_up(HID * HID, kAlign) : 0);
+  m->off_W2 = m->off_bh + (m->extra ? round_up(HID, kAlign) : 0);
   m->off_b2 = m->off_W2 + round_up(L * HID, kAlign);
   m->n_pad = m->off_b2 + round_up(L, kAlign);
-  m->n_params = F * HID + HID + L * HID + L;
+  m->n_params = F * HID + HID + (m->extra ? HID * HID + HID : 0) + L * HID + L;
 
   hipError_t e = hipGetDevice(&m->device);
   if (e == hipSuccess)
@@ -402,6 +456,8 @@ asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t s
   e = hipMemsetAsync(m->params, 0, m->n_pad * sizeof(float), m->stream);
   if (e == hipSuccess) e = launch_init_uniform(m->W1(), F * HID, seed ^ (0ull << 56), a1, m->stream);
   if (e == hipSuccess) e = launch_init_uniform(m->W2(), L * HID, seed ^ (1ull << 56), a2, m->stream);
+  if (e == hipSuccess && m->extra)
+    e = launch_init_uniform(m->Wh(), HID * HID, seed ^ (2ull << 56), (float)sqrt(6.0 / (2.0 * HID)), m->stream);
   if (e == hipSuccess) e = hipMemsetAsync(m->ws, 0, ws_bytes, m->stream);
   if (e == hipSuccess) e = hipStreamSynchronize(m->stream);
   if (e != hipSuccess) {
@@ -467,6 +523,12 @@ static asgd_status param_span(const asgd_model* m, int32_t which, float** p, siz
     case ASGD_PARAM_B1: *p = m->b1(); *bytes = (size_t)HID * 4; return ASGD_OK;
     case ASGD_PARAM_W2: *p = m->W2(); *bytes = (size_t)(L * HID * 4); return ASGD_OK;
     case ASGD_PARAM_B2: *p = m->b2(); *bytes = (size_t)(L * 4); return ASGD_OK;
+    case ASGD_PARAM_WH:
+    case ASGD_PARAM_BH:
+      if (!m->extra) return fail(ASGD_EINVAL, "the model has no second hidden layer");
+      *p = which == ASGD_PARAM_WH ? m->Wh() : m->bh();
+      *bytes = (size_t)(which == ASGD_PARAM_WH ? HID * HID * 4 : HID * 4);
+      return ASGD_OK;
     default: return fail(ASGD_EINVAL, "unknown parameter selector");
   }
 }
@@ -518,8 +580,11 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   s = run_sort(m, m->aux, x->nnz, &sk, &sv);
   if (s) return s;
   const LabelJob labels{m->lkeys, y->nnz, m->lrow, m->lbeg, m->lpair, m->lcnt, 0};
-  s = run_forward(m, x, y, rows_pad, &labels);
+  s = m->unfused ? run_forward_unfused(m, x, y, rows_pad, &labels) : run_forward(m, x, y, rows_pad, &labels);
   if (s) return s;
+  if (m->extra)  // dA1 from dA2 through the second hidden layer, whose update follows
+    TIMED(m, ASGD_K_DENSE_BWD, launch_dense_bwd(m->dA2, m->A1, m->Wh(), m->bh(), B, rows_pad, lr, m->dA1,
+                                                m->stream));
   HIP_TRY(hipEventRecord(m->ev_dA1, m->stream));
   HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_dA1, 0));
   CsrDev xd = dev(x);
@@ -546,7 +611,7 @@ asgd_status asgd_model_last_loss(asgd_model* m, float* loss_out) {
 asgd_status asgd_predict_topk(asgd_model* m, const asgd_csr* x, int32_t k, int32_t* ids_dev,
                               float* scores_dev) {
   if (!m) return fail(ASGD_EINVAL, "model is NULL");
-  asgd_status s = check_batch(m, x, nullptr);
+  asgd_status s = check_batch(m, x, nullptr, false);
   if (s) return s;
   if (k < 1 || k > 32 || k > m->L) return fail(ASGD_EINVAL, "k must be in [1, min(32, L)]");
   if (!ids_dev) return fail(ASGD_EINVAL, "ids_dev is NULL");
@@ -647,7 +712,7 @@ asgd_status asgd_model_get_timing(asgd_model* m, int32_t kernel, double* total_m
 }
 
 asgd_status asgd_debug_forward(asgd_model* m, const asgd_csr* x, const asgd_csr* y, float* a1_dev,
-                               float* lse_dev, float* loss_rows_dev) {
+                               float* z_dev, float* lse_dev, float* loss_rows_dev) {
   if (!m) return fail(ASGD_EINVAL, "model is NULL");
   asgd_status s = check_batch(m, x, y);
   if (s) return s;
@@ -656,8 +721,15 @@ asgd_status asgd_debug_forward(asgd_model* m, const asgd_csr* x, const asgd_csr*
   int rows_pad = 0;
   s = run_gather(m, x, y, &rows_pad);
   if (s) return s;
-  s = run_forward(m, x, y, rows_pad, nullptr);
+  s = m->unfused ? run_forward_unfused(m, x, y, rows_pad, nullptr) : run_forward(m, x, y, rows_pad, nullptr);
   if (s) return s;
+  if (z_dev) {
+    if (m->unfused)  // the step's own stored logits, without their padding columns
+      HIP_TRY(hipMemcpy2DAsync(z_dev, (size_t)m->L * 4, m->Z, (size_t)m->ldz * 4, (size_t)m->L * 4, B,
+                               hipMemcpyDeviceToDevice, m->stream));
+    else
+      HIP_TRY(launch_out_logits(m->bf16, m->W2(), m->b2(), m->L, m->H1, B, z_dev, m->L, 1, m->stream));
+  }
   if (a1_dev)
     HIP_TRY(hipMemcpyAsync(a1_dev, m->A1, (size_t)B * HID * 4, hipMemcpyDeviceToDevice, m->stream));
   if (lse_dev) HIP_TRY(hipMemcpyAsync(lse_dev, m->lse, (size_t)B * 4, hipMemcpyDeviceToDevice, m->stream));

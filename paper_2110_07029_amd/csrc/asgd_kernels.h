@@ -96,6 +96,36 @@ hipError_t launch_sparse_update(float* W1, int F, const int32_t* skeys, const in
 hipError_t launch_touched(const int32_t* skeys, int n_keys, int F, int32_t* ids, int32_t* count_dev,
                           hipStream_t st);
 
+// ---- the optional second dense hidden layer (k_dense.hip) -------------------------
+// A2 = ReLU(A1) Wh^T + bh (fp32, [rows_pad x 128]) and H2 = ReLU(A2) in the operand
+// type into Hop (row-major) and, for fp32 operands, HopT ([128 x ld_t]); rows in
+// [B, rows_pad) are zero.  Wh [128 x 128] row-major (output, input).
+hipError_t launch_dense_fwd(bool use_bf16, const float* A1, const float* Wh, const float* bh, int B,
+                            int rows_pad, float* A2, void* Hop, void* HopT, int ld_t, hipStream_t st);
+// dA1 = (dA2 Wh) * [A1 > 0] with the pre-update Wh, then Wh -= lr dA2^T ReLU(A1)
+// and bh -= lr 1^T dA2 (two launches in that order).
+hipError_t launch_dense_bwd(const float* dA2, const float* A1, float* Wh, float* bh, int B, int rows_pad,
+                            float lr, float* dA1, hipStream_t st);
+
+// ---- output layer with stored logits (k_unfused.hip) ----------------------------
+// Z = H W2^T + b2 into Z [B x ldz] fp32.  exact = 0: ldz >= ceil(L/32)*32 and the
+// columns past L hold -inf; exact = 1: ldz >= L and only labels < L are written.
+hipError_t launch_out_logits(bool use_bf16, const float* W2, const float* b2, int L, const void* H1, int B,
+                             float* Z, int ldz, int exact, hipStream_t st);
+// lse and, with y, loss rows from the stored Z (one pass over it); m_part / s_part
+// hold softmax_splits(ldz) x ld_part floats each.
+int softmax_splits(int ldz);
+hipError_t launch_softmax_ce(const float* Z, int ldz, int B, float* m_part, float* s_part, int ld_part,
+                             const CsrDev* y, float* lse, float* loss_rows, hipStream_t st);
+// dA = ((P W2 - rw sum_{y in Y_i} W2[y]) / B) * [A > 0] with P = exp(Z - lse) from the stored Z;
+// o_part: splits x ld_part x 128 floats.
+int unfused_dh_splits(int n_cu, int aux_cus, int B, bool use_bf16, int n_tiles);
+hipError_t launch_unfused_dh(bool use_bf16, const float* W2, const float* b2, int L, const float* Z, int ldz,
+                             const float* lse, int B, int splits, float* o_part, int ld_part, const CsrDev& y,
+                             const float* rw, const float* A, float* dA, hipStream_t st);
+// The label grouping of LabelJob as a launch of its own.
+hipError_t launch_label_blocks(const LabelJob& job, int L, hipStream_t st);
+
 // ---- prediction ---------------------------------------------------------------
 int topk_splits(int B, int n_tiles);
 hipError_t launch_out_fwd_topk(bool use_bf16, const float* W2, const float* b2, int L, const void* H1,

@@ -58,6 +58,7 @@ asgd_status asgd_elastic_create(asgd_elastic** out, const asgd_elastic_config* c
   if (n < 1 || n > 16) return efail(ASGD_EINVAL, "n_replicas must be in [1, 16]");
   if (cfg->b_min < 1 || cfg->b_max < cfg->b_min) return efail(ASGD_EINVAL, "need 1 <= b_min <= b_max");
   if (cfg->b_max > model_cfg->max_batch) return efail(ASGD_ERANGE, "b_max exceeds the models' max_batch");
+  if (cfg->b_max > 2048) return efail(ASGD_ERANGE, "b_max exceeds 2048, the largest training batch");
   if (cfg->megabatch < 1) return efail(ASGD_EINVAL, "megabatch must be >= 1");
   if (cfg->clock != ASGD_CLOCK_TIMED && cfg->clock != ASGD_CLOCK_VIRTUAL)
     return efail(ASGD_EINVAL, "unknown clock mode");

@@ -101,8 +101,8 @@ def run(mode: str, planted: synth.Planted = synth.PLANTED_SMALL, budget_s: float
     ip, lp = np.asarray(train.x.indptr, np.int64), np.asarray(train.y.indptr, np.int64)
     win = lambda a, b: int(np.max(a[b:] - a[:-b])) if len(a) > b else int(a[-1] - a[0])
     max_nnz = max(win(ip, b_max), win(np.asarray(test.x.indptr, np.int64), b_max), 1)
-    mcfg = B.asgd_config(planted.n_features, planted.n_labels, synth.HIDDEN, b_max, max_nnz,
-                         max(win(lp, b_max), 1), 1, 0)
+    mcfg = B.asgd_config(n_features=planted.n_features, n_labels=planted.n_labels, hidden=synth.HIDDEN,
+                         max_batch=b_max, max_nnz=max_nnz, max_label_nnz=max(win(lp, b_max), 1), gemm_bf16=1)
     slow = list(slow)[:n_replicas]
     cfg = elastic_config(mode, n_replicas, max(1, b_max // 8), b_max, lr,
                          batches_per_round * n_replicas * b_max, slow, cost, gamma)

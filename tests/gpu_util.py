@@ -24,18 +24,20 @@ def flush(msg: str):
     print(msg, flush=True)
 
 
-def read_params(m, F, L) -> dict:
-    return dict(W1=asgd.asgd_model_get_params(m, asgd.ASGD_PARAM_W1, (F, H)),
-                b1=asgd.asgd_model_get_params(m, asgd.ASGD_PARAM_B1, (H,)),
-                W2=asgd.asgd_model_get_params(m, asgd.ASGD_PARAM_W2, (L, H)),
-                b2=asgd.asgd_model_get_params(m, asgd.ASGD_PARAM_B2, (L,)))
+SELECT = {"W1": asgd.ASGD_PARAM_W1, "b1": asgd.ASGD_PARAM_B1, "Wh": asgd.ASGD_PARAM_WH,
+          "bh": asgd.ASGD_PARAM_BH, "W2": asgd.ASGD_PARAM_W2, "b2": asgd.ASGD_PARAM_B2}
+
+
+def read_params(m, F, L, extra=False) -> dict:
+    """Parameters in the oracle's order (W1, b1, [Wh, bh,] W2, b2)."""
+    shapes = {"W1": (F, H), "b1": (H,), "Wh": (H, H), "bh": (H,), "W2": (L, H), "b2": (L,)}
+    names = ["W1", "b1"] + (["Wh", "bh"] if extra else []) + ["W2", "b2"]
+    return {k: asgd.asgd_model_get_params(m, SELECT[k], shapes[k]) for k in names}
 
 
 def write_params(m, p: dict):
-    asgd.asgd_model_set_params(m, asgd.ASGD_PARAM_W1, p["W1"])
-    asgd.asgd_model_set_params(m, asgd.ASGD_PARAM_B1, p["b1"])
-    asgd.asgd_model_set_params(m, asgd.ASGD_PARAM_W2, p["W2"])
-    asgd.asgd_model_set_params(m, asgd.ASGD_PARAM_B2, p["b2"])
+    for k, v in p.items():
+        asgd.asgd_model_set_params(m, SELECT[k], v)
 
 
 def max_batch_nnz(csr, batch: int) -> int:
@@ -51,7 +53,7 @@ class Setup:
     """A dataset staged on the device plus a model sized for it."""
 
     def __init__(self, w: synth.Workload, n_samples: int, batch: int, bf16=None, flags=0, seed=None,
-                 ds=None, max_batch=None):
+                 ds=None, max_batch=None, extra=0):
         import torch
         self.w = w
         self.ds = ds if ds is not None else synth.generate(w, n_samples=n_samples)
@@ -64,9 +66,10 @@ class Setup:
         self.max_nnz = max(max_batch_nnz(self.ds.x, mb), 1)
         self.max_lnnz = max(max_batch_nnz(self.ds.y, mb), 1)
         self.seed = w.init_seed if seed is None else seed
+        self.extra = extra
         self.m = asgd.asgd_model_init(self.F, self.L, mb, self.max_nnz, self.max_lnnz,
                                       gemm_bf16=self.bf16, seed=self.seed, flags=flags,
-                                      stream=torch.cuda.current_stream())
+                                      stream=torch.cuda.current_stream(), extra_hidden_layers=extra)
         self.stream = torch.cuda.current_stream()
 
     def free(self):
@@ -84,7 +87,7 @@ class Setup:
         return self.ds.x.rows(r0, r1), self.ds.y.rows(r0, r1)
 
     def params(self):
-        return read_params(self.m, self.F, self.L)
+        return read_params(self.m, self.F, self.L, self.extra)
 
 
 def update_error(before, gpu, ref):
@@ -139,8 +142,9 @@ def assert_rel_close(name, got, ref, rtol, floor_frac=0.1):
 
 def step_magnitudes(p, x, y, g, fw, lr):
     """|lr| times each parameter gradient evaluated on absolute values along the whole
-    chain: |dZ| <= (P + T)/B, |dH1| <= (P + T)|W2|/B, |dA1| <= |dH1| [A1 > 0], then
-    |X|^T |dA1| for W1 and sums over rows for the biases."""
+    chain: |dZ| <= (P + T)/B, |dH| <= (P + T)|W2|/B at the output layer's input; with
+    the second hidden layer |dA2| <= |dH| [A2 > 0] and |dH1| <= |dA2||Wh|; |dA1| <=
+    |dH1| [A1 > 0], then |X|^T |dA1| for W1 and sums over rows for the biases."""
     from oracle.model import row_ids, targets
     s0, e0 = int(x.indptr[0]), int(x.indptr[-1])
     ind = np.asarray(x.indices[s0:e0], np.int64)
@@ -149,13 +153,21 @@ def step_magnitudes(p, x, y, g, fw, lr):
     B, L = fw["Z"].shape
     P = np.exp(fw["Z"] - fw["lse"][:, None])
     PT = (P + targets(y, L)) / B
-    dA1m = (PT @ np.abs(p["W2"]).astype(np.float64)) * (fw["A1"] > 0)
+    dHm = PT @ np.abs(p["W2"]).astype(np.float64)
+    lr = abs(float(lr))
+    out = {}
+    Hin = fw["H1"]
+    if "Wh" in p:
+        dA2m = dHm * (fw["A2"] > 0)
+        out.update(Wh=lr * (dA2m.T @ np.abs(fw["H1"])), bh=lr * dA2m.sum(0))
+        dHm = dA2m @ np.abs(p["Wh"]).astype(np.float64)
+        Hin = fw["H2"]
+    dA1m = dHm * (fw["A1"] > 0)
     inv = np.searchsorted(g["touched"], ind)
     mW1 = np.zeros((len(g["touched"]), dA1m.shape[1]))
     np.add.at(mW1, inv, val[:, None] * dA1m[rows])
-    lr = abs(float(lr))
-    return dict(W2=lr * (PT.T @ np.abs(fw["H1"])), b2=lr * PT.sum(0), b1=lr * dA1m.sum(0),
-                W1=lr * mW1)
+    out.update(W2=lr * (PT.T @ np.abs(Hin)), b2=lr * PT.sum(0), b1=lr * dA1m.sum(0), W1=lr * mW1)
+    return out
 
 
 def a1_bound(p, x):

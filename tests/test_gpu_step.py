@@ -58,7 +58,7 @@ def test_forward_parity(w, B, rows):
         a1 = torch.empty((n, 128), dtype=torch.float32, device="cuda")
         lse = torch.empty(n, dtype=torch.float32, device="cuda")
         lr_ = torch.empty(n, dtype=torch.float32, device="cuda")
-        asgd.asgd_debug_forward(s.m, s.xb(r0, r1), s.yb(r0, r1), a1, lse, lr_)
+        asgd.asgd_debug_forward(s.m, s.xb(r0, r1), s.yb(r0, r1), a1_dev=a1, lse_dev=lse, loss_rows_dev=lr_)
         torch.cuda.synchronize()
         xh, yh = s.host_batch(r0, r1)
         p = s.params()
@@ -91,7 +91,7 @@ def test_one_hot_rows_are_exact_rows_of_w1():
         b1 = np.linspace(-0.5, 0.5, 128).astype(np.float32)
         asgd.asgd_model_set_params(s.m, asgd.ASGD_PARAM_B1, b1)
         a1 = torch.empty((5, 128), dtype=torch.float32, device="cuda")
-        asgd.asgd_debug_forward(s.m, s.xb(0, 5), None, a1, None, None)
+        asgd.asgd_debug_forward(s.m, s.xb(0, 5), None, a1_dev=a1)
         torch.cuda.synchronize()
         W1 = s.params()["W1"]
         want = (W1[fs].astype(np.float64) + b1.astype(np.float64)).astype(np.float32)
