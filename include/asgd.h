@@ -199,6 +199,14 @@ asgd_status asgd_merge(asgd_model* global, asgd_model* prev_global, asgd_model* 
  * (Alg. 2's regularization gate "||w_i||_2 / |w|").  Synchronous. */
 asgd_status asgd_model_l2_per_param(asgd_model* m, double* out);
 
+/* The same for n models at once (1 <= n <= 16, all of one shape): their
+ * sums of squares in one launch on models[0]'s stream, after the pending work
+ * of every model's stream, and one host synchronization; out: host [n],
+ * out[i] = ||w_i||_2 / |w_i|.  ERANGE for n outside [1, 16], EINVAL for a NULL
+ * argument or models of different shapes.  The elastic rounds call it for the
+ * perturbation gate (Alg. 2) over all replicas. */
+asgd_status asgd_models_l2_per_param(asgd_model* const* models, int32_t n, double* out);
+
 /* Alg. 2 weight computation (host only).  u: updates per replica since the
  * last merge; b: batch sizes; samples: samples processed (used by
  * ASGD_WEIGHTS_SAMPLES, may be NULL otherwise); ASGD_WEIGHTS_UNIFORM gives

@@ -109,6 +109,8 @@ struct asgd_model {
   int32_t* count = nullptr;
   double* sq_part = nullptr;
   double* sq_out = nullptr;
+  double* sqm_part = nullptr;  // sums of squares of up to MERGE_MAX models (this model hosts them)
+  double* sqm_out = nullptr;
   int32_t* keys = nullptr;
   int32_t *ka = nullptr, *va = nullptr, *kb = nullptr, *vb = nullptr;
   int32_t* hist = nullptr;
@@ -183,6 +185,8 @@ int64_t layout_workspace(asgd_model* m, char* base) {
   m->count = carve<int32_t>(p, 1);
   m->sq_part = carve<double>(p, SQNORM_BLOCKS);
   m->sq_out = carve<double>(p, 1);
+  m->sqm_part = carve<double>(p, (int64_t)MERGE_MAX * SQNORM_BLOCKS);
+  m->sqm_out = carve<double>(p, MERGE_MAX);
   m->keys = carve<int32_t>(p, n_keys + 1);
   m->ka = carve<int32_t>(p, n_keys + 1);
   m->va = carve<int32_t>(p, n_keys + 1);
@@ -684,6 +688,43 @@ asgd_status asgd_model_l2_per_param(asgd_model* m, double* out) {
   HIP_TRY(hipStreamSynchronize(m->stream));
   *out = sqrt(s) / (double)m->n_params;
   return ASGD_OK;
+}
+
+namespace {
+// Models whose sums of squares are taken together: same parameter layout; the
+// first one's stream runs the kernels after every model's pending work.
+asgd_status check_norm_models(asgd_model* const* models, int32_t n, const double* out) {
+  if (!models || !out) return fail(ASGD_EINVAL, "NULL argument");
+  if (n < 1 || n > MERGE_MAX) return fail(ASGD_ERANGE, "n must be in [1, 16]");
+  for (int i = 0; i < n; ++i) {
+    if (!models[i]) return fail(ASGD_EINVAL, "model is NULL");
+    if (models[i]->n_pad != models[0]->n_pad) return fail(ASGD_EINVAL, "models differ in shape");
+  }
+  return ASGD_OK;
+}
+
+asgd_status norms_on(asgd_model* const* models, int32_t n, double* partial, double* sums_dev, double* out) {
+  asgd_model* m0 = models[0];
+  hipStream_t st = m0->stream;
+  for (int i = 1; i < n; ++i) {
+    asgd_status s = sync_events_into(st, models[i]);
+    if (s) return s;
+  }
+  const float* w[MERGE_MAX];
+  for (int i = 0; i < n; ++i) w[i] = models[i]->params;
+  HIP_TRY(launch_sqnorm_multi(w, n, m0->n_pad, partial, sums_dev, 0.0, st));
+  double sums[MERGE_MAX];
+  HIP_TRY(hipMemcpyAsync(sums, sums_dev, (size_t)n * sizeof(double), hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  for (int i = 0; i < n; ++i) out[i] = sqrt(sums[i]) / (double)models[i]->n_params;
+  return ASGD_OK;
+}
+}  // namespace
+
+asgd_status asgd_models_l2_per_param(asgd_model* const* models, int32_t n, double* out) {
+  asgd_status s = check_norm_models(models, n, out);
+  if (s) return s;
+  return norms_on(models, n, models[0]->sqm_part, models[0]->sqm_out, out);
 }
 
 asgd_status asgd_model_set_timing(asgd_model* m, int32_t enable) {

@@ -146,5 +146,10 @@ hipError_t launch_merge(float* out, const float* g, const float* gp, const float
 hipError_t launch_sqnorm(const float* w, int64_t count, double* partial, double* out,
                          hipStream_t st);
 constexpr int SQNORM_BLOCKS = 1024;
+// Sums of squares (float64) of n vectors of `count` floats (a multiple of 4) in one
+// launch plus a fixed-order reduction: partial n x SQNORM_BLOCKS doubles, out n doubles
+// (device): the sums, or sqrt(sum) / l2_div when l2_div > 0.  1 <= n <= MERGE_MAX.
+hipError_t launch_sqnorm_multi(const float* const* w, int n, int64_t count, double* partial, double* out,
+                               double l2_div, hipStream_t st);
 
 }  // namespace asgd

@@ -179,11 +179,10 @@ asgd_status asgd_elastic_round(asgd_elastic* e, const asgd_csr* x_all, const asg
   }
 
   double l2[16] = {};
-  if (c.perturb)
-    for (int i = 0; i < n; ++i) {
-      asgd_status s = asgd_model_l2_per_param(e->reps[i], &l2[i]);
-      if (s) return s;
-    }
+  if (c.perturb) {  // every replica's norm in one launch and one host synchronization
+    asgd_status s = asgd_models_l2_per_param(e->reps.data(), n, l2);
+    if (s) return s;
+  }
   float alpha[16];
   asgd_status s = asgd_merge_weights(n, u, e->b.data(), samples, c.weight_mode, c.perturb ? l2 : nullptr,
                                      c.pert_thr, c.delta, alpha);

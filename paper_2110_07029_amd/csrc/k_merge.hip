@@ -96,6 +96,60 @@ __global__ __launch_bounds__(256) void k_sqnorm_final(const double* __restrict__
   if (threadIdx.x == 0) *out = ((red[0] + red[1]) + red[2]) + red[3];
 }
 
+// The sums of squares of n parameter vectors in one launch: blockIdx.y picks
+// the vector, SQNORM_BLOCKS workgroups stream it in float4 loads, and each
+// writes its partial; a second launch reduces every vector's partials in a
+// fixed order.  partial: n x SQNORM_BLOCKS doubles; out: n doubles, the sums,
+// or sqrt(sum) / l2_div when l2_div > 0 (the L2 norm per parameter).
+struct SqArgs {
+  const float4* w[MERGE_MAX];
+};
+
+__global__ __launch_bounds__(256) void k_sqnorm_multi_part(SqArgs a, int64_t count4,
+                                                           double* __restrict__ partial) {
+  __shared__ double red[4];
+  const float4* __restrict__ w = a.w[blockIdx.y];
+  double s = 0.0;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < count4; e += stride) {
+    const float4 v = w[e];
+    s = fma((double)v.x, (double)v.x, s);
+    s = fma((double)v.y, (double)v.y, s);
+    s = fma((double)v.z, (double)v.z, s);
+    s = fma((double)v.w, (double)v.w, s);
+  }
+  s = wave_sum_d(s);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) partial[(size_t)blockIdx.y * SQNORM_BLOCKS + blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
+}
+
+__global__ __launch_bounds__(256) void k_sqnorm_multi_final(const double* __restrict__ partial,
+                                                            double* __restrict__ out, double l2_div) {
+  __shared__ double red[4];
+  const double* p = partial + (size_t)blockIdx.x * SQNORM_BLOCKS;
+  double s = 0.0;
+  for (int e = threadIdx.x; e < SQNORM_BLOCKS; e += 256) s += p[e];
+  s = wave_sum_d(s);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const double t = ((red[0] + red[1]) + red[2]) + red[3];
+    out[blockIdx.x] = l2_div > 0.0 ? sqrt(t) / l2_div : t;
+  }
+}
+
+hipError_t launch_sqnorm_multi(const float* const* w, int n, int64_t count, double* partial, double* out,
+                               double l2_div, hipStream_t st) {
+  // count is a multiple of 4 (parameter sections are padded); 1 <= n <= MERGE_MAX
+  if (n < 1 || n > MERGE_MAX || count % 4) return hipErrorInvalidValue;
+  SqArgs a{};
+  for (int i = 0; i < n; ++i) a.w[i] = reinterpret_cast<const float4*>(w[i]);
+  hipLaunchKernelGGL(k_sqnorm_multi_part, dim3(SQNORM_BLOCKS, n), dim3(256), 0, st, a, count / 4, partial);
+  hipLaunchKernelGGL(k_sqnorm_multi_final, dim3(n), dim3(256), 0, st, partial, out, l2_div);
+  return hipGetLastError();
+}
+
 hipError_t launch_sqnorm(const float* w, int64_t count, double* partial, double* out,
                          hipStream_t st) {
   hipLaunchKernelGGL(k_sqnorm_part, dim3(SQNORM_BLOCKS), dim3(256), 0, st, w, count, partial);

@@ -104,6 +104,32 @@ def test_l2_per_param_matches_numpy():
         asgd.asgd_model_free(m)
 
 
+def test_l2_per_param_of_several_models_in_one_call():
+    """The perturbation gate's norms for all replicas at once (one launch, one
+    synchronization): equal to NumPy's float64 norms and to the one-model call."""
+    import torch
+    flush("l2 per parameter, several models")
+    w = synth.TINY
+    ms = _models(3, w)
+    try:
+        rng = np.random.default_rng(3)
+        for i, m in enumerate(ms):   # make the models differ
+            asgd.asgd_model_set_params(m, asgd.ASGD_PARAM_B2, rng.normal(0, 1 + i, w.n_labels).astype(np.float32))
+        torch.cuda.synchronize()
+        got = asgd.asgd_models_l2_per_param(ms)
+        for m, g in zip(ms, got):
+            f = _flat(m, w).astype(np.float64)
+            want = np.sqrt(np.sum(f * f)) / f.size
+            assert abs(g - want) <= 1e-12 * want
+            assert abs(g - asgd.asgd_model_l2_per_param(m)) <= 1e-13 * want
+        assert asgd.asgd_models_l2_per_param(ms[1:2]) == got[1:2]
+        with pytest.raises(asgd.AsgdError):
+            asgd.asgd_models_l2_per_param([ms[0]] * 17)
+    finally:
+        for m in ms:
+            asgd.asgd_model_free(m)
+
+
 # min_frac: share of the rows whose top k + 1 logits must be far enough apart
 # to be compared id by id; at k = 32 all 32 consecutive gaps must clear the
 # bound, which ~10-15 % of these rows do (every row's scores are checked anyway)
