@@ -207,6 +207,18 @@ asgd_status asgd_model_l2_per_param(asgd_model* m, double* out);
  * perturbation gate (Alg. 2) over all replicas. */
 asgd_status asgd_models_l2_per_param(asgd_model* const* models, int32_t n, double* out);
 
+/* asgd_models_l2_per_param for callers that cannot allocate memory or wait
+ * on the host (code under HIP graph capture, tight serving loops): the same
+ * norms, computed by the same kernels, written to out_dev (device, [n]
+ * doubles) on models[0]'s stream, asynchronously; nothing is allocated and
+ * the host does not wait.  The partial sums live in a fixed device array of
+ * the library (16 x 1024 doubles, 128 KiB per device, held until the process
+ * ends) instead of a model's workspace; it is shared by every call on that
+ * device, so calls that overlap on one device (other streams, other threads)
+ * race and must be ordered by the caller.  ERANGE for n outside [1, 16] (the
+ * array's capacity); EINVAL for a NULL argument or models of different shapes. */
+asgd_status asgd_models_l2_per_param_noalloc(asgd_model* const* models, int32_t n, double* out_dev);
+
 /* Alg. 2 weight computation (host only).  u: updates per replica since the
  * last merge; b: batch sizes; samples: samples processed (used by
  * ASGD_WEIGHTS_SAMPLES, may be NULL otherwise); ASGD_WEIGHTS_UNIFORM gives

@@ -11,6 +11,7 @@ from ._binding import (  # noqa: F401
     asgd_last_error, asgd_model_init, asgd_model_free, asgd_model_set_stream, asgd_model_copy,
     asgd_model_num_params, asgd_model_get_params, asgd_model_set_params, asgd_train_step,
     asgd_model_last_loss, asgd_predict_topk, asgd_merge, asgd_model_l2_per_param, asgd_models_l2_per_param,
+    asgd_models_l2_per_param_noalloc,
     asgd_merge_weights, asgd_scale_batches, asgd_debug_forward, asgd_debug_touched_rows,
     asgd_model_set_timing, asgd_model_get_timing, KERNELS, ASGD_CLOCK_TIMED, ASGD_CLOCK_VIRTUAL,
     asgd_elastic_config, asgd_elastic_log, asgd_elastic_create, asgd_elastic_free, asgd_elastic_round,

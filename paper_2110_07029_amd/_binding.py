@@ -29,7 +29,8 @@ EXPORTS = (
     "asgd_model_init", "asgd_model_free", "asgd_model_set_stream", "asgd_model_copy",
     "asgd_model_num_params", "asgd_model_get_params", "asgd_model_set_params",
     "asgd_train_step", "asgd_model_last_loss", "asgd_predict_topk", "asgd_merge",
-    "asgd_model_l2_per_param", "asgd_models_l2_per_param", "asgd_merge_weights", "asgd_scale_batches",
+    "asgd_model_l2_per_param", "asgd_models_l2_per_param", "asgd_models_l2_per_param_noalloc",
+    "asgd_merge_weights", "asgd_scale_batches",
     "asgd_debug_forward", "asgd_debug_touched_rows", "asgd_libsvm_scan", "asgd_libsvm_read",
     "asgd_model_set_timing",
     "asgd_model_get_timing", "asgd_elastic_create", "asgd_elastic_free", "asgd_elastic_round",
@@ -99,6 +100,7 @@ def _declare(lib):
         "asgd_merge": (c_int32, [P, P, POINTER(c_void_p), POINTER(c_float), c_int32, c_float, c_int32]),
         "asgd_model_l2_per_param": (c_int32, [P, POINTER(c_double)]),
         "asgd_models_l2_per_param": (c_int32, [POINTER(c_void_p), c_int32, POINTER(c_double)]),
+        "asgd_models_l2_per_param_noalloc": (c_int32, [POINTER(c_void_p), c_int32, P]),
         "asgd_merge_weights": (c_int32, [c_int32, POINTER(c_int32), POINTER(c_int32), POINTER(c_int64),
                                          c_int32, POINTER(c_double), c_double, c_double, POINTER(c_float)]),
         "asgd_scale_batches": (c_int32, [c_int32, POINTER(c_int32), POINTER(c_int32), POINTER(c_float),
@@ -255,6 +257,13 @@ def asgd_models_l2_per_param(models) -> list:
     out = (c_double * n)()
     _check(load().asgd_models_l2_per_param(arr, n, out), "asgd_models_l2_per_param")
     return list(out)
+
+
+def asgd_models_l2_per_param_noalloc(models, out_dev):
+    """Asynchronous; out_dev: device float64 [len(models)] (e.g. a torch tensor)."""
+    n = len(models)
+    arr = (c_void_p * n)(*models)
+    _check(load().asgd_models_l2_per_param_noalloc(arr, n, _ptr(out_dev)), "asgd_models_l2_per_param_noalloc")
 
 
 def asgd_merge_weights(u, b, samples=None, mode: int = ASGD_WEIGHTS_ALG2, l2_per_param=None,

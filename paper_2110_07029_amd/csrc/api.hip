@@ -10,6 +10,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -65,6 +66,34 @@ int bit_width(uint32_t v) {
 namespace asgd {
 asgd_status set_error(asgd_status s, const char* msg) { return fail(s, msg); }
 }  // namespace asgd
+
+// Device memory of asgd_models_l2_per_param_noalloc: the per-workgroup partial
+// sums of squares of up to MERGE_MAX models (128 KiB), one copy per device,
+// held until the process ends.  Host code must not use this name as an address
+// (it is a host-side stand-in): the device address comes from
+// hipGetSymbolAddress, taken once per device by scratch_on_device().
+static __device__ __align__(256) double scratch[MERGE_MAX * SQNORM_BLOCKS];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+double* g_scratch_dev[kMaxDevices] = {};
+
+// The device address of `scratch` on `device`, which must be the current device
+// the first time (asgd_model_init runs this for its device).
+asgd_status scratch_on_device(int device, double** out) {
+  if (device < 0 || device >= kMaxDevices) return fail(ASGD_ERANGE, "device ordinal beyond 63");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return fail_hip(e, "hipGetSymbolAddress(scratch)");
+    g_scratch_dev[device] = static_cast<double*>(p);
+  }
+  *out = g_scratch_dev[device];
+  return ASGD_OK;
+}
+}  // namespace
 
 struct asgd_model {
   asgd_config cfg;
@@ -431,6 +460,14 @@ asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t s
   hipError_t e = hipGetDevice(&m->device);
   if (e == hipSuccess)
     e = hipDeviceGetAttribute(&m->n_cu, hipDeviceAttributeMultiprocessorCount, m->device);
+  if (e == hipSuccess) {
+    double* sp = nullptr;
+    const asgd_status ss = scratch_on_device(m->device, &sp);
+    if (ss) {
+      delete m;
+      return ss;
+    }
+  }
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev, kSyncEventFlags);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_fork, kSyncEventFlags);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_join, kSyncEventFlags);
@@ -725,6 +762,25 @@ asgd_status asgd_models_l2_per_param(asgd_model* const* models, int32_t n, doubl
   asgd_status s = check_norm_models(models, n, out);
   if (s) return s;
   return norms_on(models, n, models[0]->sqm_part, models[0]->sqm_out, out);
+}
+
+asgd_status asgd_models_l2_per_param_noalloc(asgd_model* const* models, int32_t n, double* out_dev) {
+  asgd_status s = check_norm_models(models, n, out_dev);
+  if (s) return s;
+  double* partial = nullptr;
+  s = scratch_on_device(models[0]->device, &partial);  // resolved when the model was created
+  if (s) return s;
+  asgd_model* m0 = models[0];
+  hipStream_t st = m0->stream;
+  for (int i = 1; i < n; ++i) {
+    s = sync_events_into(st, models[i]);
+    if (s) return s;
+  }
+  const float* w[MERGE_MAX];
+  for (int i = 0; i < n; ++i) w[i] = models[i]->params;
+  // every partial the reduction reads is written first by the same enqueued work
+  HIP_TRY(launch_sqnorm_multi(w, n, m0->n_pad, partial, out_dev, (double)m0->n_params, st));
+  return ASGD_OK;
 }
 
 asgd_status asgd_model_set_timing(asgd_model* m, int32_t enable) {
