@@ -28,7 +28,8 @@ METRIC = "training samples/sec at 1 GPU + % of HBM/MFMA roofline per kernel"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}
 H = 128
-OVERLAPPED = ("sort", "labels", "w1_update")  # on the library's second stream or inside another launch
+# on the library's second stream (beside the output layer) or inside another launch
+OVERLAPPED = ("gather", "sort", "labels", "hidden", "dense_fwd", "dense_bwd", "w1_update")
 
 # HBM traffic of a kernel from `rocprofv3 --pmc FETCH_SIZE` and `--pmc WRITE_SIZE` runs of this bench
 # (KiB per dispatch, averaged; profiles/wide_label_hbm_counters.md), scaled by what the same counters
@@ -75,6 +76,11 @@ def parse():
                     help="only run 10 plain device copies of 256 MiB (scale for the HBM byte counters)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="budget of the oracle CPU baseline (0 disables it)")
+    ap.add_argument("--unfused", action="store_true",
+                    help="the output layer with stored logits and a standalone softmax / cross-entropy pass "
+                         "(ASGD_UNFUSED_OUTPUT) instead of the fused one")
+    ap.add_argument("--extra-hidden", action="store_true",
+                    help="the model with a second dense hidden layer (extra_hidden_layers = 1)")
     ap.add_argument("--ramp", type=int, default=0,
                     help="only time N steps one by one from an idle GPU (per-step HIP events) and print "
                          "the step times by window: how long the clocks take to reach their loaded state")
@@ -109,7 +115,18 @@ def kernel_model(w, B, nnz, lnnz, uniq, splits):
     """Algorithmic bytes and flops of one launch of each kernel group."""
     F, L = w.n_features, w.n_labels
     op = 2 if w.gemm_bf16 else 4
+    ldz = -(-L // 32) * 32          # stored logits: whole 32-label tiles per row
     return {
+        # unfused output: reads W2 and b2 once, writes Z [B x ldz] fp32
+        "logits": dict(bytes=4.0 * L * (H + 1) + 4.0 * B * ldz, flops=2.0 * B * H * L),
+        # unfused output: reads Z once (the online-max pass) and the target logits; writes lse, loss
+        "softmax": dict(bytes=4.0 * B * ldz + 4.0 * lnnz + 8.0 * B, flops=0.0),
+        # unfused output: reads Z and W2 once, writes the split partials of P W2, then dA
+        "dh": dict(bytes=4.0 * B * ldz + 4.0 * L * (H + 1) + splits * B * H * 4.0 + lnnz * H * 4.0 + B * H * 8.0,
+                   flops=2.0 * B * H * L),
+        # second hidden layer: A1 and Wh read, A2 and H2 written; backward reads dA2, A1, Wh, writes dA1, Wh
+        "dense_fwd": dict(bytes=B * H * 4.0 + H * H * 4.0 + B * H * (4.0 + op), flops=2.0 * B * H * H),
+        "dense_bwd": dict(bytes=3 * B * H * 4.0 + 3 * H * H * 4.0, flops=4.0 * B * H * H),
         # reads the touched W1 rows once, the batch's (id, value) pairs; writes A1 (fp32) and H1
         # in the operand type (and its transpose, for fp32 operands only)
         "gather": dict(bytes=uniq * H * 4 + nnz * 8 + B * H * (4 + op * (1 if w.gemm_bf16 else 2)),
@@ -120,8 +137,11 @@ def kernel_model(w, B, nnz, lnnz, uniq, splits):
         "labels": dict(bytes=lnnz * 12 + (L // 32 + 1) * 4, flops=0.0),
         # reads W2 and b2 once; Z = H1 W2^T and O = P W2 (the dense part of dH1)
         "out_fwd": dict(bytes=4.0 * L * (H + 1), flops=4.0 * B * H * L),
-        # reads the forward's per-(split, row) partials (max, sum, O), A1 and the target rows of W2
-        "out_combine": dict(bytes=splits * B * (H + 2) * 4 + B * H * 4 * 2 + lnnz * H * 4, flops=2.0 * lnnz * H),
+        # reads the forward's per-(split, row) maxima and sums and the target rows of W2; writes
+        # lse, the loss rows and the rows' mean target weights
+        "out_combine": dict(bytes=splits * B * 2 * 4 + lnnz * H * 4 + B * H * 4, flops=2.0 * lnnz * H),
+        # reads the forward's partials (max, sum, O), the mean target weights and A1; writes dA1
+        "hidden": dict(bytes=splits * B * (H + 2) * 4 + B * H * 4 * 3, flops=0.0),
         # reads and writes W2 and b2 once; the logits recomputed (Z = H1 W2^T) and dW2 = dZ^T H1
         "out_bwd": dict(bytes=8.0 * L * (H + 1), flops=4.0 * B * H * L),
         # reads and writes the touched W1 rows once, the sorted (key, position) pairs, the
@@ -441,8 +461,10 @@ def main():
     xs = [dx.batch(a, b) for a, b in bounds]
     ys = [dy.batch(a, b) for a, b in bounds]
     stream = torch.cuda.current_stream()
+    flags = asgd.ASGD_UNFUSED_OUTPUT if args.unfused else 0
     m = asgd.asgd_model_init(w.n_features, w.n_labels, B, max(nnz), max(lnnz), gemm_bf16=w.gemm_bf16,
-                             seed=w.init_seed, stream=stream)
+                             seed=w.init_seed, stream=stream, flags=flags,
+                             extra_hidden_layers=1 if args.extra_hidden else 0)
     try:
         lr = w.lr
         if args.ramp:
@@ -493,7 +515,8 @@ def main():
     mean_lnnz = float(np.mean([lnnz[j] for j in used]))
     uniq = float(np.mean([len(np.unique(ds.x.indices[ipx[bounds[j][0]]:ipx[bounds[j][1]]]))
                           for j in used[:32]]))
-    # label splits of the forward: one persistent workgroup per CU but 16, shared by the 256-row blocks
+    # label splits of the forward (and of the unfused path's P W2): one persistent workgroup per CU
+    # but 16, shared by the 256-row blocks
     n_cu = torch.cuda.get_device_properties(0).multi_processor_count
     splits = min((w.n_labels + 31) // 32, -(-(n_cu - 16) // -(-B // 256)))
     model = kernel_model(w, B, mean_nnz, mean_lnnz, uniq, splits)
@@ -540,6 +563,8 @@ def main():
         "config": {"workload": w.name, "n_features": w.n_features, "n_labels": w.n_labels,
                    "hidden": H, "batch": B, "global_batch": B, "mean_nnz_per_batch": round(mean_nnz, 1),
                    "mean_labels_per_batch": round(mean_lnnz, 1), "master_weights": "fp32",
+                   "output_layer": "unfused (stored logits)" if args.unfused else "fused",
+                   "hidden_layers": 2 if args.extra_hidden else 1,
                    "parallelism": "single replica"},
         "roofline": roofline,
         "cpu_baseline": cpu,

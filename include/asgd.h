@@ -386,14 +386,14 @@ enum {
   ASGD_K_GATHER = 0,      /* first-layer gather + sort keys */
   ASGD_K_SORT = 1,        /* radix sort of the batch's feature ids (internal stream) */
   ASGD_K_OUT_FWD = 2,     /* output-layer forward over all labels */
-  ASGD_K_OUT_COMBINE = 3, /* per-row merge of label splits, loss, dA1 */
-  ASGD_K_HIDDEN = 4,      /* b1 gradient / update and mean loss: a workgroup of the
-                             W1_UPDATE launch, so never recorded on its own */
+  ASGD_K_OUT_COMBINE = 3, /* per-row merge of the label splits: lse, loss, target terms */
+  ASGD_K_HIDDEN = 4,      /* per-row dA1 from the forward's partials (internal stream,
+                             beside the backward) */
   ASGD_K_OUT_BWD = 5,     /* output-layer backward + W2/b2 update */
   ASGD_K_W1_UPDATE = 6,   /* sparse W1 gradient + update, b1 update, mean loss (internal stream) */
   ASGD_K_MERGE = 7,       /* normalized merge (timed on the global model) */
   ASGD_K_LABELS = 8,      /* (label, row) pairs grouped by label block: a workgroup of the
-                             OUT_FWD launch, so never recorded on its own */
+                             OUT_FWD (or LOGITS) launch, so never recorded on its own */
   ASGD_K_DENSE_FWD = 9,   /* second hidden layer forward (extra_hidden_layers = 1) */
   ASGD_K_DENSE_BWD = 10,  /* second hidden layer: dA1, and the Wh / bh update */
   ASGD_K_LOGITS = 11,     /* unfused output: the logits Z written to memory */

@@ -108,6 +108,7 @@ struct asgd_model {
   hipStream_t aux = nullptr;
   hipEvent_t ev_fork = nullptr, ev_dA1 = nullptr, ev_join = nullptr;
   LabelJobPlan label_plan{};  // LDS of the forward launch's label-grouping workgroup
+  LabelJobPlan label_plan_unf{};  // the same in the stored-logits path's logits launch
   hipEvent_t ev = nullptr;
 
   // parameters
@@ -129,6 +130,18 @@ struct asgd_model {
   float* dA2 = nullptr;
   void* H1 = nullptr;    // the output layer's input in its operand type (H1, or H2 with the extra layer)
   void* H1T = nullptr;
+  // H1, H1T and rw are double-buffered: the gather of a step writes one copy
+  // while the previous step's backward may still read the other.  H1, H1T and
+  // rw above point at the copy of the current call.
+  void* H1b[2] = {};
+  void* H1Tb[2] = {};
+  float* rwb[2] = {};
+  int par = 0;
+  // true while the last call on the model was a fused training step: its
+  // internal stream may then start the next step's gather without waiting for
+  // the model's stream (the previous backward only reads the other copies)
+  bool pipe = false;
+  float* tw = nullptr;   // per row: mean of W2[y] over the row's labels (pre-update)
   float* dA1 = nullptr;
   float* lse = nullptr;
   float* loss_rows = nullptr;
@@ -203,12 +216,18 @@ int64_t layout_workspace(asgd_model* m, char* base) {
   m->A1 = carve<float>(p, (int64_t)rp * HID);
   m->A2 = carve<float>(p, m->extra ? (int64_t)rp * HID : 0);
   m->dA2 = carve<float>(p, m->extra ? (int64_t)rp * HID : 0);
-  m->H1 = carve<char>(p, (int64_t)rp * HID * m->elem);
-  m->H1T = carve<char>(p, (int64_t)rp * HID * m->elem);
+  for (int b = 0; b < 2; ++b) {
+    m->H1b[b] = carve<char>(p, (int64_t)rp * HID * m->elem);
+    m->H1Tb[b] = carve<char>(p, (int64_t)rp * HID * m->elem);
+    m->rwb[b] = carve<float>(p, rp);
+  }
+  m->H1 = m->H1b[0];
+  m->H1T = m->H1Tb[0];
+  m->rw = m->rwb[0];
+  m->tw = carve<float>(p, (int64_t)rp * HID);
   m->dA1 = carve<float>(p, (int64_t)rp * HID);
   m->lse = carve<float>(p, rp);
   m->loss_rows = carve<float>(p, rp);
-  m->rw = carve<float>(p, rp);
   m->loss = carve<float>(p, 1);
   m->err = carve<int32_t>(p, 1);
   m->count = carve<int32_t>(p, 1);
@@ -318,25 +337,31 @@ hipEvent_t timer_start(asgd_model* m, int k, hipStream_t st, hipEvent_t* stop) {
   } while (0)
 #define TIMED(m, k, expr) TIMED_ON(m, k, (m)->stream, expr)
 
-// Gather forward (+ keys), optional validation check.  Leaves H1 / A1 ready.
-asgd_status run_gather(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int* rows_pad_out) {
+// Gather forward (+ keys) on stream st into the next copy of H1 / H1T / rw,
+// optional validation check.  Leaves H1 / A1 ready.
+asgd_status run_gather(asgd_model* m, const asgd_csr* x, const asgd_csr* y, hipStream_t st, int* rows_pad_out) {
   const int B = x->n_rows;
   const int RB = out_rows_per_block(m->bf16);
   const int rows_pad = (int)round_up(B, RB);
   const bool validate = (m->cfg.flags & ASGD_VALIDATE) != 0;
-  if (validate) HIP_TRY(launch_fill_int(m->err, 0, 1, m->stream));
+  m->par ^= 1;
+  m->H1 = m->H1b[m->par];
+  m->H1T = m->H1Tb[m->par];
+  m->rw = m->rwb[m->par];
+  if (validate) HIP_TRY(launch_fill_int(m->err, 0, 1, st));
   CsrDev xd = dev(x);
   CsrDev yd = y ? dev(y) : CsrDev{};
-  TIMED(m, ASGD_K_GATHER, launch_gather_fwd(m->bf16, xd, y ? &yd : nullptr, m->W1(), m->b1(), m->F, m->L, m->A1,
-                            m->H1, m->H1T, rows_pad, m->rows_pad_max, m->keys, m->row_of, m->lkeys, m->lrow,
-                            m->rw, m->err, validate ? 1 : 0, m->stream));
+  TIMED_ON(m, ASGD_K_GATHER, st, launch_gather_fwd(m->bf16, xd, y ? &yd : nullptr, m->W1(), m->b1(), m->F, m->L,
+                                                   m->A1, m->H1, m->H1T, rows_pad, m->rows_pad_max, m->keys,
+                                                   m->row_of, m->lkeys, m->lrow, m->rw, m->err, validate ? 1 : 0,
+                                                   st));
   if (m->extra)
-    TIMED(m, ASGD_K_DENSE_FWD, launch_dense_fwd(m->bf16, m->A1, m->Wh(), m->bh(), B, rows_pad, m->A2, m->H1,
-                                                m->H1T, m->rows_pad_max, m->stream));
+    TIMED_ON(m, ASGD_K_DENSE_FWD, st, launch_dense_fwd(m->bf16, m->A1, m->Wh(), m->bh(), B, rows_pad, m->A2,
+                                                       m->H1, m->H1T, m->rows_pad_max, st));
   if (validate) {
     int32_t e = 0;
-    HIP_TRY(hipMemcpyAsync(&e, m->err, sizeof(e), hipMemcpyDeviceToHost, m->stream));
-    HIP_TRY(hipStreamSynchronize(m->stream));
+    HIP_TRY(hipMemcpyAsync(&e, m->err, sizeof(e), hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipStreamSynchronize(st));
     if (e) {
       char buf[160];
       snprintf(buf, sizeof buf,
@@ -358,8 +383,12 @@ asgd_status run_sort(asgd_model* m, hipStream_t st, int n_keys, const int32_t** 
   return ASGD_OK;
 }
 
+// The fused output-layer forward and the per-row lse / target terms on the
+// model's stream; with y, dA1 (dA2 with the second hidden layer) follows on
+// da_stream, after an event when that is another stream (the training step
+// runs it beside the backward).
 asgd_status run_forward(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int rows_pad,
-                        const LabelJob* labels) {
+                        const LabelJob* labels, hipStream_t da_stream) {
   const int B = x->n_rows;
   const int splits = fwd_splits(m, B);
   const int n_tiles = (m->L + OUT_TILE - 1) / OUT_TILE;
@@ -369,14 +398,22 @@ asgd_status run_forward(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int
   TIMED(m, ASGD_K_OUT_FWD, launch_out_fwd_train(m->bf16, m->W2(), m->b2(), m->L, m->H1, B, splits, m->m_part,
                                m->s_part, m->o_part, rows_pad, labels, &m->label_plan, m->stream));
   CsrDev yd = y ? dev(y) : CsrDev{};
-  TIMED(m, ASGD_K_OUT_COMBINE, launch_out_combine(m->bf16, B, s_eff, m->m_part, m->s_part, m->o_part, rows_pad, m->W2(),
-                             m->b2(), m->L, m->H1, m->extra ? m->A2 : m->A1, y ? &yd : nullptr, m->lse,
-                             m->loss_rows, m->extra ? m->dA2 : m->dA1, m->stream));
+  TIMED(m, ASGD_K_OUT_COMBINE, launch_out_lse_targets(m->bf16, B, s_eff, m->m_part, m->s_part, rows_pad, m->W2(),
+                                                      m->b2(), m->L, m->H1, y ? &yd : nullptr, m->lse,
+                                                      m->loss_rows, m->tw, m->stream));
+  if (!y) return ASGD_OK;
+  if (da_stream != m->stream) {
+    HIP_TRY(hipEventRecord(m->ev_dA1, m->stream));
+    HIP_TRY(hipStreamWaitEvent(da_stream, m->ev_dA1, 0));
+  }
+  TIMED_ON(m, ASGD_K_HIDDEN, da_stream, launch_out_dA1(B, s_eff, m->m_part, m->s_part, m->o_part, rows_pad, m->tw,
+                                                       m->extra ? m->A2 : m->A1, m->extra ? m->dA2 : m->dA1,
+                                                       da_stream));
   return ASGD_OK;
 }
 
-// The output layer with stored logits: the labels grouped for the backward (a
-// launch of its own here), Z written by the logits kernel, lse and the loss rows
+// The output layer with stored logits: Z written by the logits kernel (whose
+// launch also groups the labels for the backward), lse and the loss rows
 // from one pass over Z, then dA (dA2 with the second hidden layer) from P W2
 // with P read back from Z.
 asgd_status run_forward_unfused(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int rows_pad,
@@ -387,9 +424,8 @@ asgd_status run_forward_unfused(asgd_model* m, const asgd_csr* x, const asgd_csr
   const int tps = (n_tiles + splits - 1) / splits;
   const int s_eff = (n_tiles + tps - 1) / tps;
   if ((int64_t)s_eff * rows_pad > m->part_rows) return fail(ASGD_ERANGE, "partial buffer too small");
-  if (labels) TIMED(m, ASGD_K_LABELS, launch_label_blocks(*labels, m->L, m->stream));
   TIMED(m, ASGD_K_LOGITS, launch_out_logits(m->bf16, m->W2(), m->b2(), m->L, m->H1, B, m->Z, m->ldz, 0,
-                                            m->stream));
+                                            m->n_cu, labels, &m->label_plan_unf, m->stream));
   CsrDev yd = y ? dev(y) : CsrDev{};
   TIMED(m, ASGD_K_SOFTMAX, launch_softmax_ce(m->Z, m->ldz, B, m->sm_m, m->sm_s, rows_pad, y ? &yd : nullptr,
                                              m->lse, m->loss_rows, m->stream));
@@ -476,6 +512,10 @@ asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t s
   if (e == hipSuccess) {
     m->label_plan = label_job_plan(m->bf16, L);
     if (!m->label_plan.ok) e = hipErrorInvalidConfiguration;
+    if (m->unfused) {
+      m->label_plan_unf = logits_label_plan(m->bf16, L);
+      if (!m->label_plan_unf.ok) e = hipErrorInvalidConfiguration;
+    }
   }
   if (e == hipSuccess) e = hipMalloc((void**)&m->params, m->n_pad * sizeof(float));
   if (e != hipSuccess) {
@@ -529,6 +569,7 @@ asgd_status asgd_model_free(asgd_model* m) {
 asgd_status asgd_model_set_stream(asgd_model* m, void* hip_stream) {
   if (!m) return fail(ASGD_EINVAL, "model is NULL");
   hipStream_t ns = (hipStream_t)hip_stream;
+  m->pipe = false;
   if (ns != m->stream) {
     HIP_TRY(hipEventRecord(m->ev, m->stream));
     HIP_TRY(hipStreamWaitEvent(ns, m->ev, 0));
@@ -540,7 +581,9 @@ asgd_status asgd_model_set_stream(asgd_model* m, void* hip_stream) {
 asgd_status asgd_model_copy(asgd_model* dst, const asgd_model* src) {
   if (!dst || !src) return fail(ASGD_EINVAL, "model is NULL");
   if (dst == src) return ASGD_OK;
-  if (dst->F != src->F || dst->L != src->L) return fail(ASGD_EINVAL, "models differ in shape");
+  if (dst->F != src->F || dst->L != src->L || dst->n_pad != src->n_pad)
+    return fail(ASGD_EINVAL, "models differ in shape");
+  dst->pipe = false;
   asgd_status s = sync_events_into(dst->stream, const_cast<asgd_model*>(src));
   if (s) return s;
   HIP_TRY(hipMemcpyAsync(dst->params, src->params, dst->n_pad * sizeof(float),
@@ -593,6 +636,7 @@ asgd_status asgd_model_set_params(asgd_model* m, int32_t which, const void* host
   asgd_status s = param_span(m, which, &p, &want);
   if (s) return s;
   if (bytes != want) return fail(ASGD_EINVAL, "byte count does not match the tensor size");
+  m->pipe = false;
   HIP_TRY(hipMemcpyAsync(p, host, bytes, hipMemcpyHostToDevice, m->stream));
   HIP_TRY(hipStreamSynchronize(m->stream));
   return ASGD_OK;
@@ -607,28 +651,49 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   if (!(lr == lr)) return fail(ASGD_EINVAL, "lr is NaN");
   const int B = x->n_rows;
   int rows_pad = 0;
-  s = run_gather(m, x, y, &rows_pad);
-  if (s) return s;
-  // The feature sort depends only on what the gather wrote: it runs on the
-  // internal stream, overlapped with the output-layer forward, whose launch
-  // also groups the labels for the backward (one workgroup of its own).  The
-  // W1 update, the b1 update and the mean loss follow the sort on the internal
-  // stream once dA1 exists, overlapped with the output-layer backward (they
-  // touch disjoint data); the step ends when both streams have finished.
   const int32_t *sk = nullptr, *sv = nullptr;
-  HIP_TRY(hipEventRecord(m->ev_fork, m->stream));
-  HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_fork, 0));
-  s = run_sort(m, m->aux, x->nnz, &sk, &sv);
-  if (s) return s;
   const LabelJob labels{m->lkeys, y->nnz, m->lrow, m->lbeg, m->lpair, m->lcnt, 0};
-  s = m->unfused ? run_forward_unfused(m, x, y, rows_pad, &labels) : run_forward(m, x, y, rows_pad, &labels);
-  if (s) return s;
-  if (m->extra)  // dA1 from dA2 through the second hidden layer, whose update follows
-    TIMED(m, ASGD_K_DENSE_BWD, launch_dense_bwd(m->dA2, m->A1, m->Wh(), m->bh(), B, rows_pad, lr, m->dA1,
-                                                m->stream));
-  HIP_TRY(hipEventRecord(m->ev_dA1, m->stream));
-  HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_dA1, 0));
   CsrDev xd = dev(x);
+  m->pipe = m->pipe && !m->unfused;
+  if (!m->unfused) {
+    // Two streams.  Internal: gather (after the previous step's W1 update,
+    // so it overlaps that step's output-layer backward), feature sort, then,
+    // once the forward's partials and target terms exist, dA1, the second
+    // hidden layer's backward, the sparse W1 update, b1 and the mean loss.
+    // Model's stream: forward (whose launch also groups the labels), lse and
+    // target terms, backward with the W2 update; the step ends when both have
+    // finished.  Unless the previous call was a training step, the internal
+    // stream first waits for the model's stream.
+    if (!m->pipe) {
+      HIP_TRY(hipEventRecord(m->ev_fork, m->stream));
+      HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_fork, 0));
+    }
+    m->pipe = false;
+    s = run_gather(m, x, y, m->aux, &rows_pad);
+    if (s) return s;
+    HIP_TRY(hipEventRecord(m->ev_fork, m->aux));
+    HIP_TRY(hipStreamWaitEvent(m->stream, m->ev_fork, 0));
+    s = run_sort(m, m->aux, x->nnz, &sk, &sv);
+    if (s) return s;
+    s = run_forward(m, x, y, rows_pad, &labels, m->aux);
+    if (s) return s;
+  } else {
+    // Stored logits: the gather and the output layer on the model's stream,
+    // the feature sort on the internal stream beside them.
+    s = run_gather(m, x, y, m->stream, &rows_pad);
+    if (s) return s;
+    HIP_TRY(hipEventRecord(m->ev_fork, m->stream));
+    HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_fork, 0));
+    s = run_sort(m, m->aux, x->nnz, &sk, &sv);
+    if (s) return s;
+    s = run_forward_unfused(m, x, y, rows_pad, &labels);
+    if (s) return s;
+    HIP_TRY(hipEventRecord(m->ev_dA1, m->stream));
+    HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_dA1, 0));
+  }
+  if (m->extra)  // dA1 from dA2 through the second hidden layer, whose update follows
+    TIMED_ON(m, ASGD_K_DENSE_BWD, m->aux, launch_dense_bwd(m->dA2, m->A1, m->Wh(), m->bh(), B, rows_pad, lr,
+                                                           m->dA1, m->aux));
   TIMED_ON(m, ASGD_K_W1_UPDATE, m->aux,
            launch_sparse_update(m->W1(), m->F, sk, sv, x->nnz, m->row_of, xd, m->dA1, lr, B, m->b1(),
                                 m->loss_rows, m->loss, m->w1_part, m->aux));
@@ -636,6 +701,7 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   TIMED(m, ASGD_K_OUT_BWD, launch_out_bwd(m->bf16, m->W2(), m->b2(), m->L, m->H1, m->H1T, m->rows_pad_max, B,
                          m->lse, m->rw, m->lbeg, m->lpair, lr, m->n_cu, m->stream));
   HIP_TRY(hipStreamWaitEvent(m->stream, m->ev_join, 0));
+  m->pipe = !m->unfused;
   if (loss_out) return asgd_model_last_loss(m, loss_out);
   return ASGD_OK;
 }
@@ -658,7 +724,8 @@ asgd_status asgd_predict_topk(asgd_model* m, const asgd_csr* x, int32_t k, int32
   if (!ids_dev) return fail(ASGD_EINVAL, "ids_dev is NULL");
   const int B = x->n_rows;
   int rows_pad = 0;
-  s = run_gather(m, x, nullptr, &rows_pad);
+  m->pipe = false;
+  s = run_gather(m, x, nullptr, m->stream, &rows_pad);
   if (s) return s;
   const int n_tiles = (m->L + OUT_TILE - 1) / OUT_TILE;
   const int splits = topk_splits(B, n_tiles);
@@ -677,19 +744,25 @@ asgd_status asgd_merge(asgd_model* global, asgd_model* prev_global, asgd_model* 
   if (!global || !replicas || !weights) return fail(ASGD_EINVAL, "NULL argument");
   if (n < 1 || n > MERGE_MAX) return fail(ASGD_EINVAL, "n must be in [1, 16]");
   if (prev_global == global) return fail(ASGD_EINVAL, "prev_global must differ from global");
-  if (prev_global && (prev_global->F != global->F || prev_global->L != global->L))
+  if (prev_global && (prev_global->F != global->F || prev_global->L != global->L ||
+                      prev_global->n_pad != global->n_pad))
     return fail(ASGD_EINVAL, "prev_global differs in shape");
   for (int i = 0; i < n; ++i) {
     asgd_model* r = replicas[i];
     if (!r) return fail(ASGD_EINVAL, "replica is NULL");
     if (r == global || r == prev_global) return fail(ASGD_EINVAL, "a replica aliases the global model");
-    if (r->F != global->F || r->L != global->L) return fail(ASGD_EINVAL, "replica differs in shape");
+    if (r->F != global->F || r->L != global->L || r->n_pad != global->n_pad)
+      return fail(ASGD_EINVAL, "replica differs in shape");
     if (!(weights[i] == weights[i])) return fail(ASGD_EINVAL, "weight is NaN");
     for (int j = 0; j < i; ++j)
       if (replicas[j] == r && broadcast) return fail(ASGD_EINVAL, "duplicate replica with broadcast");
   }
   hipStream_t st = global->stream;
+  // every participant's next training step must wait for the merge on its own stream
+  global->pipe = false;
+  if (prev_global) prev_global->pipe = false;
   for (int i = 0; i < n; ++i) {
+    replicas[i]->pipe = false;
     asgd_status s = sync_events_into(st, replicas[i]);
     if (s) return s;
   }
@@ -816,16 +889,19 @@ asgd_status asgd_debug_forward(asgd_model* m, const asgd_csr* x, const asgd_csr*
   if (loss_rows_dev && !y) return fail(ASGD_EINVAL, "loss rows need y");
   const int B = x->n_rows;
   int rows_pad = 0;
-  s = run_gather(m, x, y, &rows_pad);
+  m->pipe = false;
+  s = run_gather(m, x, y, m->stream, &rows_pad);
   if (s) return s;
-  s = m->unfused ? run_forward_unfused(m, x, y, rows_pad, nullptr) : run_forward(m, x, y, rows_pad, nullptr);
+  s = m->unfused ? run_forward_unfused(m, x, y, rows_pad, nullptr)
+                 : run_forward(m, x, y, rows_pad, nullptr, m->stream);
   if (s) return s;
   if (z_dev) {
     if (m->unfused)  // the step's own stored logits, without their padding columns
       HIP_TRY(hipMemcpy2DAsync(z_dev, (size_t)m->L * 4, m->Z, (size_t)m->ldz * 4, (size_t)m->L * 4, B,
                                hipMemcpyDeviceToDevice, m->stream));
     else
-      HIP_TRY(launch_out_logits(m->bf16, m->W2(), m->b2(), m->L, m->H1, B, z_dev, m->L, 1, m->stream));
+      HIP_TRY(launch_out_logits(m->bf16, m->W2(), m->b2(), m->L, m->H1, B, z_dev, m->L, 1, m->n_cu, nullptr,
+                                nullptr, m->stream));
   }
   if (a1_dev)
     HIP_TRY(hipMemcpyAsync(a1_dev, m->A1, (size_t)B * HID * 4, hipMemcpyDeviceToDevice, m->stream));
@@ -842,7 +918,8 @@ asgd_status asgd_debug_touched_rows(asgd_model* m, const asgd_csr* x, int32_t* i
   asgd_status s = check_batch(m, x, nullptr);
   if (s) return s;
   int rows_pad = 0;
-  s = run_gather(m, x, nullptr, &rows_pad);
+  m->pipe = false;
+  s = run_gather(m, x, nullptr, m->stream, &rows_pad);
   if (s) return s;
   const int32_t *sk = nullptr, *sv = nullptr;
   s = run_sort(m, m->stream, x->nnz, &sk, &sv);

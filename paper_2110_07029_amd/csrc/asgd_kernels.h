@@ -62,6 +62,8 @@ struct LabelJobPlan {
   int ok, lds_bytes, in_lds;
 };
 LabelJobPlan label_job_plan(bool use_bf16, int L);
+// The same for the label-grouping workgroup of another launch of `nthreads` threads.
+LabelJobPlan label_job_plan_for(const void* fn, int nthreads, int L);
 
 // ---- output layer -----------------------------------------------------------
 constexpr int OUT_TILE = 32;  // labels per forward tile
@@ -73,12 +75,14 @@ int out_rows_per_block(bool use_bf16);
 hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2, int L, const void* H1,
                                 int B, int splits, float* m_part, float* s_part, float* o_part,
                                 int ld_part, const LabelJob* job, const LabelJobPlan* plan, hipStream_t st);
-// Per row: lse, loss_i, dA1 (see kernel); y may be NULL (lse only).
-hipError_t launch_out_combine(bool use_bf16, int B, int splits, const float* m_part,
-                              const float* s_part, const float* o_part, int ld_part,
-                              const float* W2, const float* b2, int L, const void* H1,
-                              const float* A1, const CsrDev* y, float* lse, float* loss_rows,
-                              float* dA1, hipStream_t st);
+// Per row, after the forward: lse, and with y the loss and tw = mean_{y in Y_i} W2[y]
+// [B x 128] (reads W2 before the backward updates it).
+hipError_t launch_out_lse_targets(bool use_bf16, int B, int splits, const float* m_part, const float* s_part,
+                                  int ld_part, const float* W2, const float* b2, int L, const void* H1,
+                                  const CsrDev* y, float* lse, float* loss_rows, float* tw, hipStream_t st);
+// Per row: dA1 = ((O/s - tw) / B) * [A1 > 0] from the forward's partials (reads no W2).
+hipError_t launch_out_dA1(int B, int splits, const float* m_part, const float* s_part, const float* o_part,
+                          int ld_part, const float* tw, const float* A1, float* dA1, hipStream_t st);
 // Recompute Z per label tile, dZ = (softmax - T)/B, dW2 = dZ^T H1, db2; update W2, b2 in place.
 hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, const void* H1,
                           const void* H1T, int ld_t, int B, const float* lse, const float* rw,
@@ -110,8 +114,12 @@ hipError_t launch_dense_bwd(const float* dA2, const float* A1, float* Wh, float*
 // ---- output layer with stored logits (k_unfused.hip) ----------------------------
 // Z = H W2^T + b2 into Z [B x ldz] fp32.  exact = 0: ldz >= ceil(L/32)*32 and the
 // columns past L hold -inf; exact = 1: ldz >= L and only labels < L are written.
+// With job != NULL, one more workgroup of the launch groups the labels (plan from
+// logits_label_plan).
+LabelJobPlan logits_label_plan(bool use_bf16, int L);
 hipError_t launch_out_logits(bool use_bf16, const float* W2, const float* b2, int L, const void* H1, int B,
-                             float* Z, int ldz, int exact, hipStream_t st);
+                             float* Z, int ldz, int exact, int n_cu, const LabelJob* job,
+                             const LabelJobPlan* plan, hipStream_t st);
 // lse and, with y, loss rows from the stored Z (one pass over it); m_part / s_part
 // hold softmax_splits(ldz) x ld_part floats each.
 int softmax_splits(int ldz);
@@ -123,8 +131,6 @@ int unfused_dh_splits(int n_cu, int aux_cus, int B, bool use_bf16, int n_tiles);
 hipError_t launch_unfused_dh(bool use_bf16, const float* W2, const float* b2, int L, const float* Z, int ldz,
                              const float* lse, int B, int splits, float* o_part, int ld_part, const CsrDev& y,
                              const float* rw, const float* A, float* dA, hipStream_t st);
-// The label grouping of LabelJob as a launch of its own.
-hipError_t launch_label_blocks(const LabelJob& job, int L, hipStream_t st);
 
 // ---- prediction ---------------------------------------------------------------
 int topk_splits(int B, int n_tiles);

@@ -15,13 +15,14 @@
 namespace asgd {
 
 constexpr int DN_THREADS = 256;
-constexpr int DN_ROWS = 8;  // rows per workgroup of the row-parallel kernels
+constexpr int DN_ROWS = 4;   // rows per workgroup of the row-parallel kernels
+constexpr int WS = HID + 1;  // LDS row stride of Wh: reads along either index are conflict-free
 
 // Row-parallel product with a resident 128 x 128 weight: thread t computes
-// output unit j = t % 128 of rows r0 + t / 128 + 2i (i < 4).  FWD: out[r][o] =
-// bh[o] + sum_k relu(in[r][k]) Wh[o][k]; otherwise out[r][k] = sum_o in[r][o]
-// Wh[o][k], masked by [A1 > 0].  The weight is staged so that thread j reads
-// consecutive words (conflict-free): FWD keeps Wh^T, the backward Wh itself.
+// unit j = t % 128 of rows r0 + t / 128 + 2i (i < DN_ROWS / 2).  FWD: out[r][o]
+// = bh[o] + sum_k relu(in[r][k]) Wh[o][k]; otherwise out[r][k] = sum_o in[r][o]
+// Wh[o][k], masked by [A1 > 0].  Wh sits in LDS as [o][k] with row stride 129,
+// so lanes that differ in o (FWD) or in k (backward) hit distinct banks.
 template <bool FWD, bool BF16>
 __global__ __launch_bounds__(DN_THREADS) void k_dense_rows(const float* __restrict__ in,
                                                           const float* __restrict__ Wh,
@@ -31,21 +32,15 @@ __global__ __launch_bounds__(DN_THREADS) void k_dense_rows(const float* __restri
                                                           typename Mma<BF16>::elem* __restrict__ HopT,
                                                           int ld_t, const float* __restrict__ A1) {
   using E = typename Mma<BF16>::elem;
-  __shared__ float w[HID * HID];        // 64 KB
+  __shared__ float w[HID * WS];         // 66 KB
   __shared__ float xs[DN_ROWS][HID];    // the workgroup's input rows
   const int tid = threadIdx.x;
   const int r0 = blockIdx.x * DN_ROWS;
   for (int e = tid; e < HID * HID / 4; e += DN_THREADS) {
     const float4 v = reinterpret_cast<const float4*>(Wh)[e];
-    if constexpr (FWD) {  // element (o, k) of Wh to w[k][o]
-      const int o = (4 * e) / HID, k = (4 * e) % HID;
-      w[(k + 0) * HID + o] = v.x;
-      w[(k + 1) * HID + o] = v.y;
-      w[(k + 2) * HID + o] = v.z;
-      w[(k + 3) * HID + o] = v.w;
-    } else {
-      reinterpret_cast<float4*>(w)[e] = v;
-    }
+    const int o = (4 * e) / HID, k = (4 * e) % HID;
+    float* d = w + o * WS + k;
+    d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
   }
   for (int e = tid; e < DN_ROWS * HID; e += DN_THREADS) {
     const int r = e / HID, k = e % HID;
@@ -53,17 +48,19 @@ __global__ __launch_bounds__(DN_THREADS) void k_dense_rows(const float* __restri
     xs[r][k] = FWD ? fmaxf(v, 0.0f) : v;
   }
   __syncthreads();
+  constexpr int RPT = DN_ROWS / 2;
   const int j = tid % HID, rr = tid / HID;
-  float acc[DN_ROWS / 2];
+  float acc[RPT];
 #pragma unroll
-  for (int i = 0; i < DN_ROWS / 2; ++i) acc[i] = FWD ? bh[j] : 0.0f;
+  for (int i = 0; i < RPT; ++i) acc[i] = FWD ? bh[j] : 0.0f;
+#pragma unroll 8
   for (int k = 0; k < HID; ++k) {
-    const float wk = w[k * HID + j];
+    const float wk = FWD ? w[j * WS + k] : w[k * WS + j];
 #pragma unroll
-    for (int i = 0; i < DN_ROWS / 2; ++i) acc[i] = fmaf(xs[rr + 2 * i][k], wk, acc[i]);
+    for (int i = 0; i < RPT; ++i) acc[i] = fmaf(xs[rr + 2 * i][k], wk, acc[i]);
   }
 #pragma unroll
-  for (int i = 0; i < DN_ROWS / 2; ++i) {
+  for (int i = 0; i < RPT; ++i) {
     const int r = r0 + rr + 2 * i;
     if (r >= rows_pad) continue;
     const bool live = r < B;
@@ -83,18 +80,35 @@ __global__ __launch_bounds__(DN_THREADS) void k_dense_rows(const float* __restri
 
 // dWh[o][k] = sum_r dA2[r][o] relu(A1[r][k]) and dbh[o] = sum_r dA2[r][o], in
 // row order; then the update in place.  Workgroup = 2 output units x 128
-// input units; the dA2 value of a row is the same for a whole half.
+// input units; the rows come through LDS in chunks of 64 (all of a chunk's
+// loads in flight together), the chunk's dA2 values of the two units beside.
+constexpr int WG_CHUNK = 64;
 __global__ __launch_bounds__(DN_THREADS) void k_dense_wgrad(const float* __restrict__ dA2,
                                                            const float* __restrict__ A1, int B,
                                                            float lr, float* __restrict__ Wh,
                                                            float* __restrict__ bh) {
-  const int k = threadIdx.x % HID;
-  const int o = blockIdx.x * 2 + threadIdx.x / HID;
+  __shared__ float hs[WG_CHUNK][HID];
+  __shared__ float ds[WG_CHUNK][2];
+  const int tid = threadIdx.x;
+  const int k = tid % HID, half = tid / HID;
+  const int o = blockIdx.x * 2 + half;
   float acc = 0.0f, db = 0.0f;
-  for (int r = 0; r < B; ++r) {
-    const float d = dA2[(size_t)r * HID + o];
-    acc = fmaf(d, fmaxf(A1[(size_t)r * HID + k], 0.0f), acc);
-    db += d;
+  for (int c0 = 0; c0 < B; c0 += WG_CHUNK) {
+    const int nr = min(WG_CHUNK, B - c0);
+    __syncthreads();  // the previous chunk is consumed
+    for (int e = tid; e < nr * HID / 4; e += DN_THREADS) {
+      const float4 v = reinterpret_cast<const float4*>(A1 + (size_t)c0 * HID)[e];
+      float* d = &hs[0][0] + 4 * e;
+      d[0] = fmaxf(v.x, 0.0f); d[1] = fmaxf(v.y, 0.0f); d[2] = fmaxf(v.z, 0.0f); d[3] = fmaxf(v.w, 0.0f);
+    }
+    for (int e = tid; e < nr * 2; e += DN_THREADS)
+      ds[e / 2][e % 2] = dA2[(size_t)(c0 + e / 2) * HID + blockIdx.x * 2 + e % 2];
+    __syncthreads();
+    for (int r = 0; r < nr; ++r) {
+      const float d = ds[r][half];
+      acc = fmaf(d, hs[r][k], acc);
+      db += d;
+    }
   }
   Wh[o * HID + k] = fmaf(-lr, acc, Wh[o * HID + k]);
   if (k == 0) bh[o] = fmaf(-lr, db, bh[o]);

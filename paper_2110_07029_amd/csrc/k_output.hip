@@ -250,22 +250,26 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
   }
 }
 
-LabelJobPlan label_job_plan(bool use_bf16, int L) {
-  const void* fn = use_bf16 ? (const void*)k_out_fwd_train<true> : (const void*)k_out_fwd_train<false>;
+LabelJobPlan label_job_plan_for(const void* fn, int nthreads, int L) {
   LabelJobPlan p{};
   hipFuncAttributes fa{};
   int dev = 0, lds_max = 0;
   if (hipFuncGetAttributes(&fa, fn) != hipSuccess || hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
     return p;
-  // what the forward's own arrays leave of a workgroup's LDS (160 KB on gfx950)
+  // what the kernel's own arrays leave of a workgroup's LDS (160 KB on gfx950)
   const int budget = lds_max - (int)fa.sharedSizeBytes;
   if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, budget) != hipSuccess) return p;
-  const int ints = (L + 31) / 32 + FWD_THREADS / 64;
+  const int ints = (L + 31) / 32 + nthreads / 64;
   p.in_lds = ints * 4 <= budget;
-  p.lds_bytes = 4 * (p.in_lds ? ints : FWD_THREADS / 64);
+  p.lds_bytes = 4 * (p.in_lds ? ints : nthreads / 64);
   p.ok = p.lds_bytes <= budget;
   return p;
+}
+
+LabelJobPlan label_job_plan(bool use_bf16, int L) {
+  return label_job_plan_for(use_bf16 ? (const void*)k_out_fwd_train<true> : (const void*)k_out_fwd_train<false>,
+                            FWD_THREADS, L);
 }
 
 hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2, int L, const void* H1,
@@ -296,57 +300,89 @@ hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2,
 }
 
 // ---------------------------------------------------------------------------
-// Per row: merge the splits, log-sum-exp, loss, dA1.  512 threads = 16 split
-// groups x 32 threads x 4 hidden units (16-byte loads) for the
-// softmax-weighted sums, 8 wavefronts x the row's labels for the target terms.
-// Each group merges its splits online against its own running maximum (so
-// its loads need not wait for the row's maximum), then the 16 groups are
-// rescaled to the row's maximum; every partial is combined in a fixed order,
-// so the result does not depend on scheduling.
+// Per row, in two kernels so that only the small one sits between the forward
+// and the backward:
+//   k_out_lse_targets  lse from the splits' (max, sum) pairs, and the row's
+//                      target terms: the mean of W2[y] over y in Y_i (the
+//                      pre-update W2, before the backward writes it), the
+//                      target logits and the loss;
+//   k_out_dA1          the splits' O merged against the same maxima,
+//                      dH1 = (O/s - mean_{y in Y_i} W2[y]) / B, dA1 = dH1 [A1 > 0]
+//                      (runs beside the backward: it reads no W2).
+// k_out_lse_targets: 512 threads, one (max, sum) pair per thread merged by
+// wavefront reductions, 8 wavefronts x the row's labels for the target terms.
+// k_out_dA1: 256 threads = 8 split groups x 32 threads x 4 hidden units; each
+// group merges its splits online against its own running maximum, then the
+// groups are rescaled to the row's maximum (4 KB of LDS, so that it fits on a
+// CU beside the backward).  Every partial is combined in a fixed order, so the
+// results do not depend on scheduling.
 // ---------------------------------------------------------------------------
 constexpr int CMB_THREADS = 512;
-constexpr int CMB_GROUPS = CMB_THREADS / 32;  // 16
 constexpr int CMB_WAVES = CMB_THREADS / 64;   // 8
+constexpr int DA_THREADS = 256;
+constexpr int CMB_GROUPS = DA_THREADS / 32;   // 8
 
-template <bool BF16>
-__global__ __launch_bounds__(CMB_THREADS) void k_out_combine(
-    int B, int splits, const float* __restrict__ m_part, const float* __restrict__ s_part,
-    const float* __restrict__ o_part, int ld_part, const float* __restrict__ W2,
-    const float* __restrict__ b2, int L, const typename Mma<BF16>::elem* __restrict__ H1,
-    const float* __restrict__ A1, CsrDev y, int has_y, float invB, float* __restrict__ lse_out,
-    float* __restrict__ loss_rows, float* __restrict__ dA1) {
-  __shared__ float red_o[CMB_GROUPS][HID];
-  __shared__ float red_s[CMB_GROUPS];
-  __shared__ float red_m[CMB_GROUPS];
-  __shared__ float red_t[CMB_WAVES][HID];
-  __shared__ float red_z[CMB_WAVES];
-  const int i = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int grp = t >> 5, h4 = (t & 31) * 4;
+// (m, s) <- the merge of two (maximum, sum of 2^(x - maximum)) pairs, base 2 or
+// natural alike through exp_fast (natural logarithms here)
+__device__ __forceinline__ void ms_merge_ln(float& m, float& s, float m2, float s2) {
+  const float mm = fmaxf(m, m2);
+  if (mm == -INFINITY) return;
+  s = (m == -INFINITY ? 0.0f : s * exp_fast(m - mm)) + (m2 == -INFINITY ? 0.0f : s2 * exp_fast(m2 - mm));
+  m = mm;
+}
 
-  float mg = -INFINITY, St = 0.0f;
-  float4 O = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+// Group grp's online merge of splits grp, grp + 16, ...: running maximum mg,
+// sum St and (WITH_O) the weighted O of hidden units h4 .. h4 + 3.
+template <bool WITH_O>
+__device__ __forceinline__ void merge_splits(int i, int splits, const float* __restrict__ m_part,
+                                             const float* __restrict__ s_part, const float* __restrict__ o_part,
+                                             int ld_part, int grp, int h4, float& mg, float& St, float4& O) {
+  mg = -INFINITY;
+  St = 0.0f;
+  O = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
 #pragma unroll 8
   for (int s = grp; s < splits; s += CMB_GROUPS) {
     const size_t r = (size_t)s * ld_part + i;
     const float ms = m_part[r];
     const float ss = s_part[r];
-    const float4 o = *reinterpret_cast<const float4*>(o_part + r * HID + h4);
+    float4 o = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if constexpr (WITH_O) o = *reinterpret_cast<const float4*>(o_part + r * HID + h4);
     // (no split has -inf: each holds at least one label of finite bias)
     const float mn = fmaxf(mg, ms);
     const float a = exp_fast(mg - mn), e = exp_fast(ms - mn);
     St = fmaf(e, ss, St * a);
-    O.x = fmaf(e, o.x, O.x * a);
-    O.y = fmaf(e, o.y, O.y * a);
-    O.z = fmaf(e, o.z, O.z * a);
-    O.w = fmaf(e, o.w, O.w * a);
+    if constexpr (WITH_O) {
+      O.x = fmaf(e, o.x, O.x * a);
+      O.y = fmaf(e, o.y, O.y * a);
+      O.z = fmaf(e, o.z, O.z * a);
+      O.w = fmaf(e, o.w, O.w * a);
+    }
     mg = mn;
   }
-  *reinterpret_cast<float4*>(&red_o[grp][h4]) = O;
-  if ((t & 31) == 0) {
-    red_s[grp] = St;
-    red_m[grp] = mg;
-  }
+}
 
+template <bool BF16>
+__global__ __launch_bounds__(CMB_THREADS) void k_out_lse_targets(
+    int splits, const float* __restrict__ m_part, const float* __restrict__ s_part, int ld_part,
+    const float* __restrict__ W2, const float* __restrict__ b2, int L,
+    const typename Mma<BF16>::elem* __restrict__ H1, CsrDev y, int has_y, float* __restrict__ lse_out,
+    float* __restrict__ loss_rows, float* __restrict__ tw_out) {
+  __shared__ float red_s[CMB_WAVES];
+  __shared__ float red_m[CMB_WAVES];
+  __shared__ float red_t[CMB_WAVES][HID];
+  __shared__ float red_z[CMB_WAVES];
+  const int i = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  {
+    float mg = -INFINITY, St = 0.0f;
+    for (int k = t; k < splits; k += CMB_THREADS)
+      ms_merge_ln(mg, St, m_part[(size_t)k * ld_part + i], s_part[(size_t)k * ld_part + i]);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) ms_merge_ln(mg, St, __shfl_xor(mg, o), __shfl_xor(St, o));
+    if (lane == 0) {
+      red_s[w] = St;
+      red_m[w] = mg;
+    }
+  }
   // target terms: wave w takes labels q = w, w + 8, ... of row i; lane owns hidden 2l, 2l+1
   float tw0 = 0.0f, tw1 = 0.0f, zw = 0.0f;
   int cnt = 0;
@@ -379,16 +415,9 @@ __global__ __launch_bounds__(CMB_THREADS) void k_out_combine(
   }
   __syncthreads();
   if (t < HID) {
-    float M = red_m[0];
+    float M = red_m[0], Stot = red_s[0];
 #pragma unroll
-    for (int k = 1; k < CMB_GROUPS; ++k) M = fmaxf(M, red_m[k]);
-    float Ot = 0.0f, Stot = 0.0f;
-#pragma unroll
-    for (int k = 0; k < CMB_GROUPS; ++k) {
-      const float e = red_m[k] == -INFINITY ? 0.0f : exp_fast(red_m[k] - M);  // groups without a split
-      Ot = fmaf(e, red_o[k][t], Ot);
-      Stot = fmaf(e, red_s[k], Stot);
-    }
+    for (int k = 1; k < CMB_WAVES; ++k) ms_merge_ln(M, Stot, red_m[k], red_s[k]);
     const float lse = M + logf(Stot);
     if (t == 0) lse_out[i] = lse;
     if (has_y) {
@@ -399,28 +428,64 @@ __global__ __launch_bounds__(CMB_THREADS) void k_out_combine(
         zs += red_z[k];
       }
       const float inv_cnt = cnt > 0 ? 1.0f / (float)cnt : 0.0f;
-      const float dh = (Ot / Stot - tw * inv_cnt) * invB;
-      dA1[(size_t)i * HID + t] = A1[(size_t)i * HID + t] > 0.0f ? dh : 0.0f;
+      tw_out[(size_t)i * HID + t] = tw * inv_cnt;
       if (t == 0) loss_rows[i] = lse - zs * inv_cnt;
     }
   }
 }
 
-hipError_t launch_out_combine(bool use_bf16, int B, int splits, const float* m_part,
-                              const float* s_part, const float* o_part, int ld_part,
-                              const float* W2, const float* b2, int L, const void* H1,
-                              const float* A1, const CsrDev* y, float* lse, float* loss_rows,
-                              float* dA1, hipStream_t st) {
+__global__ __launch_bounds__(DA_THREADS) void k_out_dA1(int splits, const float* __restrict__ m_part,
+                                                         const float* __restrict__ s_part,
+                                                         const float* __restrict__ o_part, int ld_part,
+                                                         const float* __restrict__ tw, const float* __restrict__ A1,
+                                                         float invB, float* __restrict__ dA1) {
+  __shared__ float red_o[CMB_GROUPS][HID];
+  __shared__ float red_s[CMB_GROUPS];
+  __shared__ float red_m[CMB_GROUPS];
+  const int i = blockIdx.x, t = threadIdx.x;
+  const int grp = t >> 5, h4 = (t & 31) * 4;
+  float mg, St;
+  float4 O;
+  merge_splits<true>(i, splits, m_part, s_part, o_part, ld_part, grp, h4, mg, St, O);
+  *reinterpret_cast<float4*>(&red_o[grp][h4]) = O;
+  if ((t & 31) == 0) {
+    red_s[grp] = St;
+    red_m[grp] = mg;
+  }
+  __syncthreads();
+  if (t < HID) {
+    float M = red_m[0];
+#pragma unroll
+    for (int k = 1; k < CMB_GROUPS; ++k) M = fmaxf(M, red_m[k]);
+    float Ot = 0.0f, Stot = 0.0f;
+#pragma unroll
+    for (int k = 0; k < CMB_GROUPS; ++k) {
+      const float e = red_m[k] == -INFINITY ? 0.0f : exp_fast(red_m[k] - M);
+      Ot = fmaf(e, red_o[k][t], Ot);
+      Stot = fmaf(e, red_s[k], Stot);
+    }
+    const float dh = (Ot / Stot - tw[(size_t)i * HID + t]) * invB;
+    dA1[(size_t)i * HID + t] = A1[(size_t)i * HID + t] > 0.0f ? dh : 0.0f;
+  }
+}
+
+hipError_t launch_out_lse_targets(bool use_bf16, int B, int splits, const float* m_part, const float* s_part,
+                                  int ld_part, const float* W2, const float* b2, int L, const void* H1,
+                                  const CsrDev* y, float* lse, float* loss_rows, float* tw, hipStream_t st) {
   CsrDev yy = y ? *y : CsrDev{0, 0, 0, nullptr, nullptr, nullptr};
-  const float invB = 1.0f / (float)B;
   if (use_bf16)
-    hipLaunchKernelGGL(k_out_combine<true>, dim3(B), dim3(CMB_THREADS), 0, st, B, splits, m_part,
-                       s_part, o_part, ld_part, W2, b2, L, (const bf16*)H1, A1, yy, y != nullptr,
-                       invB, lse, loss_rows, dA1);
+    hipLaunchKernelGGL(k_out_lse_targets<true>, dim3(B), dim3(CMB_THREADS), 0, st, splits, m_part, s_part,
+                       ld_part, W2, b2, L, (const bf16*)H1, yy, y != nullptr, lse, loss_rows, tw);
   else
-    hipLaunchKernelGGL(k_out_combine<false>, dim3(B), dim3(CMB_THREADS), 0, st, B, splits, m_part,
-                       s_part, o_part, ld_part, W2, b2, L, (const float*)H1, A1, yy, y != nullptr,
-                       invB, lse, loss_rows, dA1);
+    hipLaunchKernelGGL(k_out_lse_targets<false>, dim3(B), dim3(CMB_THREADS), 0, st, splits, m_part, s_part,
+                       ld_part, W2, b2, L, (const float*)H1, yy, y != nullptr, lse, loss_rows, tw);
+  return hipGetLastError();
+}
+
+hipError_t launch_out_dA1(int B, int splits, const float* m_part, const float* s_part, const float* o_part,
+                          int ld_part, const float* tw, const float* A1, float* dA1, hipStream_t st) {
+  hipLaunchKernelGGL(k_out_dA1, dim3(B), dim3(DA_THREADS), 0, st, splits, m_part, s_part, o_part, ld_part, tw,
+                     A1, 1.0f / (float)B, dA1);
   return hipGetLastError();
 }
 

@@ -12,8 +12,8 @@
 //                    split, row) on the matrix cores
 //   k_dh_combine     dH = (sum_splits O - mean_{y in Y_i} W2[y]) / B and
 //                    dA = dH * [A > 0]
-//   k_label_blocks   the (row, label) pairs grouped by label block for the
-//                    backward (in the fused path a workgroup of the forward)
+// The logits launch carries one more workgroup that groups the (row, label)
+// pairs by label block for the backward, as the fused forward's launch does.
 // The W2 / b2 update is the fused backward of k_out_bwd.hip, which takes lse
 // from k_softmax_final and recomputes the logits it needs from H and W2 (that
 // costs no memory traffic; reading Z back would cost B*L*4 bytes).
@@ -30,9 +30,11 @@ namespace asgd {
 // Logits.  Workgroup = (label split, 256 rows), 8 waves x 32 rows, H fragments
 // resident in registers; W2 tiles double-buffered in LDS, the next one loaded
 // into registers while the current one is used.  Lane (g, n) holds row n and
-// labels 8q + 4g + 0..3 of the tile (the accumulator's layout): four 16-byte
-// stores per tile.  With `exact` the stores go element by element and stop at
-// label L (a caller's [B x L] buffer); otherwise ldz covers whole tiles.
+// labels 8q + 4g + 0..3 of the tile (the accumulator's layout); the wave turns
+// its 32 x 32 block around in LDS so that each 16-byte store instruction
+// writes eight whole 128-byte row segments of Z.  With `exact` the stores go
+// element by element and stop at label L (a caller's [B x L] buffer);
+// otherwise ldz covers whole tiles.
 // ---------------------------------------------------------------------------
 template <bool BF16>
 __global__ __launch_bounds__(FWD_THREADS) void k_out_logits(const float* __restrict__ W2,
@@ -40,7 +42,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_logits(const float* __restr
                                                             const typename Mma<BF16>::elem* __restrict__ H1,
                                                             int B, int tiles_per_split, int n_tiles,
                                                             int s_eff, float* __restrict__ Z, int ldz,
-                                                            int exact) {
+                                                            int exact, int n_fwd, LabelJob lj) {
   using M = Mma<BF16>;
   using E = typename M::elem;
   using Fr = typename M::frag;
@@ -48,6 +50,17 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_logits(const float* __restr
   constexpr int NCH = 32 / M::KC;
   __shared__ __attribute__((aligned(16))) E wr[2][tile_elems<BF16>()];
   __shared__ __attribute__((aligned(16))) float bt[2][OUT_TILE];
+  constexpr int ZT = OUT_TILE + 4;  // row stride of a wave's transposition block (floats)
+  __shared__ __attribute__((aligned(16))) float zt[FwdShape<BF16>::WAVES][32 * ZT];
+  if ((int)blockIdx.x >= n_fwd) {  // the label grouping (dispatched last)
+    extern __shared__ int32_t job_lds[];
+    if (lj.in_lds)
+      wg_label_blocks<FWD_THREADS, true>(lj.lkeys, lj.m, L, lj.lrow, lj.lbeg, lj.lpair, job_lds,
+                                         job_lds + ((L + 31) >> 5));
+    else
+      wg_label_blocks<FWD_THREADS, false>(lj.lkeys, lj.m, L, lj.lrow, lj.lbeg, lj.lpair, lj.lcnt, job_lds);
+    return;
+  }
   const int lane = threadIdx.x & 63, g = lane >> 5, n = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int split = (int)blockIdx.x % s_eff;
@@ -87,13 +100,25 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_logits(const float* __restr
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
       for (int c = 0; c < NCH; ++c) z = M::mma(tile_frag_w<BF16>(wr[buf], rbase, n, kb, c, g), hf[kb][c], z);
-    if (row < B) {
-      float* zr = Z + (size_t)row * ldz + t * OUT_TILE + 4 * g;
-      if (!exact) {
+    if (!exact) {
+      // the accumulator layout into the wave's block (row n, labels 8q + 4g ..), then
+      // out as row segments: lane l stores row 8k + l / 8, labels 4 (l % 8) .. + 3
+      float* zb = zt[wave];
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          *reinterpret_cast<float4*>(zr + 8 * q) = make_float4(z[4 * q], z[4 * q + 1], z[4 * q + 2], z[4 * q + 3]);
-      } else {
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<float4*>(zb + n * ZT + 8 * q + 4 * g) =
+            make_float4(z[4 * q], z[4 * q + 1], z[4 * q + 2], z[4 * q + 3]);
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int rl = 8 * k + (lane >> 3), cl = 4 * (lane & 7);
+        const float4 v = *reinterpret_cast<const float4*>(zb + rl * ZT + cl);
+        if (row0 + rl < B) *reinterpret_cast<float4*>(Z + (size_t)(row0 + rl) * ldz + t * OUT_TILE + cl) = v;
+      }
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    } else if (row < B) {
+      float* zr = Z + (size_t)row * ldz + t * OUT_TILE + 4 * g;
+      {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int ll = 8 * (r >> 2) + (r & 3);
@@ -107,24 +132,47 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_logits(const float* __restr
   }
 }
 
-int logits_splits(int B, int n_tiles) { return topk_splits(B, n_tiles); }
+// The job's counters stay in global memory here: dynamic LDS is sized per launch,
+// and counters in LDS would take it from every logits workgroup (two of which
+// share a CU).
+LabelJobPlan logits_label_plan(bool /*use_bf16*/, int /*L*/) {
+  LabelJobPlan p{};
+  p.ok = 1;
+  p.in_lds = 0;
+  p.lds_bytes = 4 * (FWD_THREADS / 64);
+  return p;
+}
 
 hipError_t launch_out_logits(bool use_bf16, const float* W2, const float* b2, int L, const void* H1, int B,
-                             float* Z, int ldz, int exact, hipStream_t st) {
+                             float* Z, int ldz, int exact, int n_cu, const LabelJob* job,
+                             const LabelJobPlan* plan, hipStream_t st) {
   const int n_tiles = (L + OUT_TILE - 1) / OUT_TILE;
   if (!exact && ldz < n_tiles * OUT_TILE) return hipErrorInvalidValue;
   if (exact && ldz < L) return hipErrorInvalidValue;
-  const int splits = logits_splits(B, n_tiles);
+  const int RB = out_rows_per_block(use_bf16);
+  const int nrb = (B + RB - 1) / RB;
+  // two workgroups per CU: the kernel is bound by its stores of Z
+  const int want = (2 * n_cu + nrb - 1) / nrb;
+  const int splits = want < n_tiles ? want : n_tiles;
   const int tps = (n_tiles + splits - 1) / splits;
   const int s_eff = (n_tiles + tps - 1) / tps;
-  const int RB = out_rows_per_block(use_bf16);
-  const dim3 grid(s_eff * ((B + RB - 1) / RB)), block(FWD_THREADS);
+  const int n_fwd = s_eff * nrb;
+  LabelJob lj{};
+  int lds = 0, n_job = 0;
+  if (job) {
+    if (!plan || !plan->ok) return hipErrorInvalidValue;
+    lj = *job;
+    lj.in_lds = plan->in_lds;
+    lds = plan->lds_bytes;
+    n_job = 1;
+  }
+  const dim3 grid(n_fwd + n_job), block(FWD_THREADS);
   if (use_bf16)
-    hipLaunchKernelGGL(k_out_logits<true>, grid, block, 0, st, W2, b2, L, (const bf16*)H1, B, tps, n_tiles,
-                       s_eff, Z, ldz, exact);
+    hipLaunchKernelGGL(k_out_logits<true>, grid, block, lds, st, W2, b2, L, (const bf16*)H1, B, tps, n_tiles,
+                       s_eff, Z, ldz, exact, n_fwd, lj);
   else
-    hipLaunchKernelGGL(k_out_logits<false>, grid, block, 0, st, W2, b2, L, (const float*)H1, B, tps, n_tiles,
-                       s_eff, Z, ldz, exact);
+    hipLaunchKernelGGL(k_out_logits<false>, grid, block, lds, st, W2, b2, L, (const float*)H1, B, tps, n_tiles,
+                       s_eff, Z, ldz, exact, n_fwd, lj);
   return hipGetLastError();
 }
 
@@ -144,9 +192,16 @@ __device__ __forceinline__ void row_range(const CsrDev& a, int i, int* q0, int* 
 // wavefront and then the workgroup merge their (m, s) pairs with cross-lane
 // reductions.  Entries of -inf (labels past L) contribute nothing.
 // ---------------------------------------------------------------------------
+// Z is read once per pass: non-temporal loads keep it from displacing what the
+// caches hold (measured on the pass alone: 118 -> 103 us for 256 x 670,112).
+__device__ __forceinline__ float4 load_nt(const float4* p) {
+  const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+
 constexpr int SM_THREADS = 256;
 constexpr int SM_VEC = 8;                          // float4 loads in flight per thread
-constexpr int SM_CHUNK = SM_THREADS * SM_VEC * 4 * 2;  // columns per workgroup: two rounds of loads
+constexpr int SM_CHUNK = SM_THREADS * SM_VEC * 4 * 4;  // columns per workgroup: four rounds of loads
 
 __device__ __forceinline__ void ms_merge(float& m, float& s, float m2, float s2) {
   const float mm = fmaxf(m, m2);
@@ -169,7 +224,7 @@ __global__ __launch_bounds__(SM_THREADS) void k_softmax_part(const float* __rest
 #pragma unroll
     for (int j = 0; j < SM_VEC; ++j) {
       const int idx = base + j * SM_THREADS + (int)threadIdx.x;
-      v[j] = idx < v1 ? zr[idx] : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+      v[j] = idx < v1 ? load_nt(zr + idx) : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
     }
     float mx = -INFINITY;
 #pragma unroll
@@ -299,7 +354,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_unfused_dh(const float* __restr
   auto load_z = [&](int t, float4 (&zv)[4]) {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      zv[q] = live ? *reinterpret_cast<const float4*>(zrow + t * OUT_TILE + 8 * q)
+      zv[q] = live ? load_nt(reinterpret_cast<const float4*>(zrow + t * OUT_TILE + 8 * q))
                    : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
   };
   TileRegs tr;
@@ -347,15 +402,26 @@ __global__ __launch_bounds__(FWD_THREADS) void k_unfused_dh(const float* __restr
   }
 }
 
-// Per row, one thread per hidden unit: dH = (sum_k O_k - rw sum_{y in Y_i} W2[y]) / B, summed in
-// split order, then dA = dH where A > 0.
-__global__ __launch_bounds__(HID) void k_dh_combine(const float* __restrict__ o_part, int ld_part, int splits,
-                                                    const float* __restrict__ W2, int L, CsrDev y,
-                                                    const float* __restrict__ rw, const float* __restrict__ A,
-                                                    float invB, float* __restrict__ dA) {
-  const int row = blockIdx.x, j = threadIdx.x;
-  float o = 0.0f;
-  for (int k = 0; k < splits; ++k) o += o_part[((size_t)k * ld_part + row) * HID + j];
+// Per row, 4 groups of 128 threads (one per hidden unit): group c sums the
+// splits k = c (mod 4) in order, then the groups are added in order (a fixed
+// summation order); dH = (sum_k O_k - rw sum_{y in Y_i} W2[y]) / B and
+// dA = dH where A > 0.
+constexpr int DHC_GROUPS = 4;
+__global__ __launch_bounds__(HID * DHC_GROUPS) void k_dh_combine(const float* __restrict__ o_part, int ld_part,
+                                                                 int splits, const float* __restrict__ W2, int L,
+                                                                 CsrDev y, const float* __restrict__ rw,
+                                                                 const float* __restrict__ A, float invB,
+                                                                 float* __restrict__ dA) {
+  __shared__ float part[DHC_GROUPS][HID];
+  const int row = blockIdx.x, j = threadIdx.x % HID, grp = threadIdx.x / HID;
+  float og = 0.0f;
+  for (int k = grp; k < splits; k += DHC_GROUPS) og += o_part[((size_t)k * ld_part + row) * HID + j];
+  part[grp][j] = og;
+  __syncthreads();
+  if (grp) return;
+  float o = part[0][j];
+#pragma unroll
+  for (int c = 1; c < DHC_GROUPS; ++c) o += part[c][j];
   int q0, q1;
   row_range(y, row, &q0, &q1);
   float t = 0.0f;
@@ -391,32 +457,8 @@ hipError_t launch_unfused_dh(bool use_bf16, const float* W2, const float* b2, in
   else
     hipLaunchKernelGGL(k_unfused_dh<false>, grid, block, 0, st, W2, b2, L, Z, ldz, lse, B, tps, n_tiles, s_eff,
                        o_part, ld_part);
-  hipLaunchKernelGGL(k_dh_combine, dim3(B), dim3(HID), 0, st, o_part, ld_part, s_eff, W2, L, y, rw, A,
-                     1.0f / (float)B, dA);
-  return hipGetLastError();
-}
-
-// The label grouping as a launch of its own: one workgroup, counters in LDS
-// when ceil(L/32) of them fit, else in global memory (lcnt).
-constexpr int LB_THREADS = 512;
-template <bool LDS>
-__global__ __launch_bounds__(LB_THREADS) void k_label_blocks(LabelJob lj, int L) {
-  extern __shared__ int32_t lb_lds[];
-  if constexpr (LDS)
-    wg_label_blocks<LB_THREADS, true>(lj.lkeys, lj.m, L, lj.lrow, lj.lbeg, lj.lpair, lb_lds,
-                                      lb_lds + ((L + 31) >> 5));
-  else
-    wg_label_blocks<LB_THREADS, false>(lj.lkeys, lj.m, L, lj.lrow, lj.lbeg, lj.lpair, lj.lcnt, lb_lds);
-}
-
-hipError_t launch_label_blocks(const LabelJob& job, int L, hipStream_t st) {
-  const int ints = (L + 31) / 32 + LB_THREADS / 64;
-  constexpr int kLds = 64 * 1024;  // no attribute call needed below 64 KB
-  if (ints * 4 <= kLds)
-    hipLaunchKernelGGL(k_label_blocks<true>, dim3(1), dim3(LB_THREADS), (size_t)ints * 4, st, job, L);
-  else
-    hipLaunchKernelGGL(k_label_blocks<false>, dim3(1), dim3(LB_THREADS), (size_t)(LB_THREADS / 64) * 4, st, job,
-                       L);
+  hipLaunchKernelGGL(k_dh_combine, dim3(B), dim3(HID * DHC_GROUPS), 0, st, o_part, ld_part, s_eff, W2, L, y, rw,
+                     A, 1.0f / (float)B, dA);
   return hipGetLastError();
 }
 

@@ -332,3 +332,40 @@ def test_argument_errors_leave_model_unchanged():
             assert np.array_equal(p0[k].view(np.uint32), p1[k].view(np.uint32)), k
     finally:
         s.free()
+
+
+@pytest.mark.parametrize("bf16", [True, False])
+def test_consecutive_steps_match_the_oracle_sequence(bf16):
+    """Steps issued back to back (the next step's gather runs on the internal
+    stream beside the previous backward, on the other copy of H1), with
+    batches of different sizes, a prediction and a parameter write in between
+    (after which the next step's gather must wait for the model's stream
+    again): the model after every step follows the oracle's sequence."""
+    import torch
+    flush(f"consecutive steps bf16={bf16}")
+    w = SMALL_MID
+    s = Setup(w, 2000, 256, bf16=bf16)
+    try:
+        p = s.params()
+        bounds = [(0, 256), (256, 300), (300, 556), (556, 557), (557, 813), (813, 1000), (1000, 1256)]
+        ids = torch.empty((256, 1), dtype=torch.int32, device="cuda")
+        # free-running over seven steps, rounding differences carry from step to step: the
+        # elementwise floor is the RMS of the reference update (as for the elastic rounds)
+        rt = RTOL_BF16 if bf16 else 1e-3
+        for k, (r0, r1) in enumerate(bounds):
+            asgd.asgd_train_step(s.m, s.xb(r0, r1), s.yb(r0, r1), 0.05)
+            xh, yh = s.host_batch(r0, r1)
+            p, *_ = om.train_step(p, xh, yh, 0.05, "fp32")
+            if k == 2:   # a prediction between two steps
+                asgd.asgd_predict_topk(s.m, s.xb(0, 256), 1, ids)
+            if k == 4:   # a parameter write between two steps (the same values)
+                asgd.asgd_model_set_params(s.m, asgd.ASGD_PARAM_B1, s.params()["b1"])
+        torch.cuda.synchronize()
+        got = s.params()
+        init = om.init_params(w.n_features, w.n_labels, 128, s.seed)
+        for k in ("W1", "b1", "W2", "b2"):
+            d_ref = p[k].astype(np.float64) - init[k]
+            rms = float(np.sqrt(np.mean(d_ref ** 2)))
+            assert_update_close(k, init[k], got[k], p[k], rt, mag=np.full(d_ref.shape, rms))
+    finally:
+        s.free()
