@@ -141,6 +141,8 @@ struct asgd_model {
   // internal stream may then start the next step's gather without waiting for
   // the model's stream (the previous backward only reads the other copies)
   bool pipe = false;
+  // whether the gather runs on the internal stream (see asgd_train_step)
+  bool gather_aux = false;
   float* tw = nullptr;   // per row: mean of W2[y] over the row's labels (pre-update)
   float* dA1 = nullptr;
   float* lse = nullptr;
@@ -481,6 +483,14 @@ asgd_status asgd_model_init(asgd_model** out, const asgd_config* cfg, uint64_t s
   m->bf16 = cfg->gemm_bf16 == 1;
   m->extra = cfg->extra_hidden_layers == 1;
   m->unfused = (cfg->flags & ASGD_UNFUSED_OUTPUT) != 0;
+  // The gather moves to the internal stream, beside the previous step's
+  // backward, when the output layer dominates the step: with many labels per
+  // batch entry the internal stream (gather, sort, sparse update: work in
+  // proportion to the batch's entries) then stays shorter than the model's
+  // stream (work in proportion to L).  Measured: L / max_nnz of 33 (the
+  // wide-label workload) gains 5 us per step; 4.9 (wide-feature) and 0.4
+  // (tiny) lose 14 and 17 us, the internal stream becoming the longer one.
+  m->gather_aux = !m->unfused && (int64_t)cfg->n_labels >= 8 * std::max<int64_t>(cfg->max_nnz, 1);
   m->elem = m->bf16 ? 2 : 4;
   m->stream = (hipStream_t)hip_stream;
   m->rows_pad_max = (int)round_up(cfg->max_batch, out_rows_per_block(m->bf16));
@@ -654,8 +664,8 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   const int32_t *sk = nullptr, *sv = nullptr;
   const LabelJob labels{m->lkeys, y->nnz, m->lrow, m->lbeg, m->lpair, m->lcnt, 0};
   CsrDev xd = dev(x);
-  m->pipe = m->pipe && !m->unfused;
-  if (!m->unfused) {
+  m->pipe = m->pipe && m->gather_aux;
+  if (m->gather_aux) {
     // Two streams.  Internal: gather (after the previous step's W1 update,
     // so it overlaps that step's output-layer backward), feature sort, then,
     // once the forward's partials and target terms exist, dA1, the second
@@ -677,23 +687,28 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
     if (s) return s;
     s = run_forward(m, x, y, rows_pad, &labels, m->aux);
     if (s) return s;
+    if (m->extra)  // dA1 from dA2 through the second hidden layer, whose update follows
+      TIMED_ON(m, ASGD_K_DENSE_BWD, m->aux, launch_dense_bwd(m->dA2, m->A1, m->Wh(), m->bh(), B, rows_pad, lr,
+                                                             m->dA1, m->aux));
   } else {
-    // Stored logits: the gather and the output layer on the model's stream,
-    // the feature sort on the internal stream beside them.
+    // The gather and the output layer's forward, and with it dA1, on the
+    // model's stream; the feature sort on the internal stream beside them,
+    // and the sparse update beside the backward.
     s = run_gather(m, x, y, m->stream, &rows_pad);
     if (s) return s;
     HIP_TRY(hipEventRecord(m->ev_fork, m->stream));
     HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_fork, 0));
     s = run_sort(m, m->aux, x->nnz, &sk, &sv);
     if (s) return s;
-    s = run_forward_unfused(m, x, y, rows_pad, &labels);
+    s = m->unfused ? run_forward_unfused(m, x, y, rows_pad, &labels)
+                   : run_forward(m, x, y, rows_pad, &labels, m->stream);
     if (s) return s;
+    if (m->extra)
+      TIMED(m, ASGD_K_DENSE_BWD, launch_dense_bwd(m->dA2, m->A1, m->Wh(), m->bh(), B, rows_pad, lr, m->dA1,
+                                                  m->stream));
     HIP_TRY(hipEventRecord(m->ev_dA1, m->stream));
     HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_dA1, 0));
   }
-  if (m->extra)  // dA1 from dA2 through the second hidden layer, whose update follows
-    TIMED_ON(m, ASGD_K_DENSE_BWD, m->aux, launch_dense_bwd(m->dA2, m->A1, m->Wh(), m->bh(), B, rows_pad, lr,
-                                                           m->dA1, m->aux));
   TIMED_ON(m, ASGD_K_W1_UPDATE, m->aux,
            launch_sparse_update(m->W1(), m->F, sk, sv, x->nnz, m->row_of, xd, m->dA1, lr, B, m->b1(),
                                 m->loss_rows, m->loss, m->w1_part, m->aux));
@@ -701,7 +716,7 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   TIMED(m, ASGD_K_OUT_BWD, launch_out_bwd(m->bf16, m->W2(), m->b2(), m->L, m->H1, m->H1T, m->rows_pad_max, B,
                          m->lse, m->rw, m->lbeg, m->lpair, lr, m->n_cu, m->stream));
   HIP_TRY(hipStreamWaitEvent(m->stream, m->ev_join, 0));
-  m->pipe = !m->unfused;
+  m->pipe = m->gather_aux;
   if (loss_out) return asgd_model_last_loss(m, loss_out);
   return ASGD_OK;
 }

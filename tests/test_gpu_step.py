@@ -334,16 +334,23 @@ def test_argument_errors_leave_model_unchanged():
         s.free()
 
 
-@pytest.mark.parametrize("bf16", [True, False])
-def test_consecutive_steps_match_the_oracle_sequence(bf16):
-    """Steps issued back to back (the next step's gather runs on the internal
-    stream beside the previous backward, on the other copy of H1), with
-    batches of different sizes, a prediction and a parameter write in between
-    (after which the next step's gather must wait for the model's stream
-    again): the model after every step follows the oracle's sequence."""
+# many labels per batch entry (L / max_nnz ~ 35): the library runs the gather on its
+# internal stream, beside the previous step's backward
+WIDE_SMALL = synth.Workload("wide-small", 20_000, 200_003, 2_000, 256, 0.01, True, "lognormal", 3.0,
+                            0.7, 500, 1.05, "uniform", "poisson", 4.0, 1.2, 2)
+
+
+@pytest.mark.parametrize("w,bf16", [(WIDE_SMALL, True), (WIDE_SMALL, False), (SMALL_MID, True)])
+def test_consecutive_steps_match_the_oracle_sequence(w, bf16):
+    """Steps issued back to back, with batches of different sizes, a
+    prediction and a parameter write in between: the model after every step
+    follows the oracle's sequence.  With many labels (WIDE_SMALL) the next
+    step's gather runs on the internal stream beside the previous backward,
+    on the other copy of H1, and after a call other than a step it must wait
+    for the model's stream again; otherwise the gather stays on the model's
+    stream."""
     import torch
-    flush(f"consecutive steps bf16={bf16}")
-    w = SMALL_MID
+    flush(f"consecutive steps {w.name} bf16={bf16}")
     s = Setup(w, 2000, 256, bf16=bf16)
     try:
         p = s.params()
