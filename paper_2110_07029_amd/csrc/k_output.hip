@@ -71,13 +71,20 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
   }
   const int lane = threadIdx.x & 63, g = lane >> 5, n = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int split = (int)blockIdx.x % s_eff;
+  // Workgroup -> (split, row block).  Workgroups are dealt to the 8 XCDs in
+  // turn (workgroup b to XCD b mod 8), each with its own L2, so the row blocks
+  // of one split (which read the same W2 tiles) get consecutive numbers in
+  // XCD-major order v: they share an XCD, and its L2 serves the tiles once.
+  const int nrb = n_fwd / s_eff;
+  const int b = (int)blockIdx.x;
+  const int v = n_fwd % 8 == 0 ? (b % 8) * (n_fwd / 8) + b / 8 : b;
+  const int split = v / nrb;
   const int t_begin = split * tiles_per_split;
   const int t_end = min(n_tiles, t_begin + tiles_per_split);
   const int t_last = t_end - 1;
   // Rows past B (up to the 256-row padding, zero in H1) are computed like the
   // others and never written out, so the loop has no row-dependent branch.
-  const int row0 = ((int)blockIdx.x / s_eff) * RB + wave * 32;
+  const int row0 = (v % nrb) * RB + wave * 32;
   const W2Src src = w2_src(W2, b2, L);
   const int rbase[2] = {tw_row_base(n, g, 0), tw_row_base(n, g, 1)};
   const int cbase[2] = {tw_col_base(lane, 0), tw_col_base(lane, 1)};

@@ -192,7 +192,8 @@ __device__ __forceinline__ void row_range(const CsrDev& a, int i, int* q0, int* 
 // wavefront and then the workgroup merge their (m, s) pairs with cross-lane
 // reductions.  Entries of -inf (labels past L) contribute nothing.
 // ---------------------------------------------------------------------------
-// Z is read once per pass: non-temporal loads keep it from displacing what the
+// Z is read once by the softmax pass, in whole 16-byte pieces of contiguous
+// 1 KB runs per wave: non-temporal loads keep it from displacing what the
 // caches hold (measured on the pass alone: 118 -> 103 us for 256 x 670,112).
 __device__ __forceinline__ float4 load_nt(const float4* p) {
   const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
@@ -354,7 +355,10 @@ __global__ __launch_bounds__(FWD_THREADS) void k_unfused_dh(const float* __restr
   auto load_z = [&](int t, float4 (&zv)[4]) {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      zv[q] = live ? load_nt(reinterpret_cast<const float4*>(zrow + t * OUT_TILE + 8 * q))
+      // (plain loads: a lane reads 16 of a row's 128 bytes per instruction, and
+      // non-temporal loads let the line go before the other three quarters
+      // are read: 1.5x the bytes from HBM, measured)
+      zv[q] = live ? *reinterpret_cast<const float4*>(zrow + t * OUT_TILE + 8 * q)
                    : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
   };
   TileRegs tr;
