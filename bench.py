@@ -38,9 +38,17 @@ OVERLAPPED = ("gather", "sort", "labels", "hidden", "dense_fwd", "dense_bwd", "w
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 PMC_TRAFFIC = {
     ("wide-label", 256, "out_bwd"): dict(
-        sources=("csrc/k_out_bwd.hip", "csrc/asgd_dev.h", "csrc/asgd_kernels.h"),
-        sha256="e0185b912e91973c004705296c9ed5cac885c88d24764964903f35bbcc676c3d",
-        fetch_kib=169677.6, write_kib=337663.1),
+        sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
+        sha256="92e509b1d36eb57af587fabb9d00c9a1b8fcb93b17baea6a7311e4daf8e6bf3e",
+        fetch_kib=169676.8, write_kib=337663.1),
+    ("wide-label", 1024, "out_bwd"): dict(
+        sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
+        sha256="92e509b1d36eb57af587fabb9d00c9a1b8fcb93b17baea6a7311e4daf8e6bf3e",
+        fetch_kib=176716.9, write_kib=337973.2),
+    ("elastic", 4, "merge"): dict(
+        sources=('csrc/k_merge.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
+        sha256="a75a94295383593e6e13395fadee8cac897bef6c0b77484b8ce27ca18d48b422",
+        fetch_kib=1216909.2, write_kib=2028091.2),
 }
 
 
@@ -315,7 +323,7 @@ def run_elastic(args):
                    "global_batch": mega, "clock": "timed", "weights": "samples", "momentum": 0.9,
                    "parallelism": "4 replicas on 4 HIP streams", "step": "one round (dispatch + merge)"},
         "roofline": {"kernel": "merge", "bound": "hbm", "achieved": merge["GB/s"], "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": merge["hbm_frac"], "traffic": None},
+                     "unit": "GB/s", "frac": merge["hbm_frac"], "traffic": measured_traffic("elastic", n, "merge")},
         "cpu_baseline": cpu,
         "settle": {"ms": args.settle_ms, "rounds": n_settle},
         "kernels": {"merge": merge},

@@ -128,9 +128,9 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc_o[hb][r] = 0.0f;
 
-  // Software pipeline over a ring of three LDS tiles and two register tiles.
-  // In the iteration of tile t: the logits of tile t+1 go to the matrix cores
-  // while the softmax numerators of tile t are formed; then O^T += W2_t^T P_t^T
+  // Software pipeline over a ring of LDS tiles and two register tiles.  In the
+  // iteration of tile t: the logits of tile t+1 go to the matrix cores while
+  // the softmax numerators of tile t are formed; then O^T += W2_t^T P_t^T
   // while tile t+P+1 (loaded into registers two iterations earlier) is
   // converted into the ring and tile t+P+3 is loaded in its place; a barrier
   // closes every P-th iteration.  Tile u lives in ring slot (u - t_begin) mod
@@ -187,12 +187,28 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
         for (int c = 0; c < NCH; ++c) oa[hb][c] = tile_frag_wt<BF16>(wr[b0], wt[b0], cbase, hb, c, lane);
     }
 
+    // The next tile's logits go to the matrix cores first; this tile's maximum
+    // and numerators are formed on the vector units while they run.  The
+    // numerators are taken against the current reference before the maximum
+    // is known (the empty asm keeps them ahead of the branch), and formed again
+    // in the rare iteration that raises the reference, so every p that is used
+    // is computed against the reference the row ends with at that point.
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c)
+        zn = M::mma(BF16 ? za[kb][c % PRE] : tile_frag_w<BF16>(wr[b1], rbase, n, kb, c, g), hf[kb][c], zn);
     // running maximum of this tile (rows are lanes: one max per lane pair)
     float tmax = z[0];
 #pragma unroll
     for (int r = 1; r < 16; ++r) tmax = fmaxf(tmax, z[r]);
     tmax = half_swap_max(tmax);
     const float m2c = tmax * LOG2E;
+    float p[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, -m_run));
+#pragma unroll
+    for (int r = 0; r < 16; ++r) asm volatile("" : "+v"(p[r]));
     if (__any(m2c > m_run + LAZY)) {
       const float m2n = m2c > m_run + LAZY ? m2c : m_run;
       const float scale = __builtin_amdgcn_exp2f(m_run - m2n);
@@ -202,21 +218,12 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc_o[hb][r] *= scale;
       m_run = m2n;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, -m_run));
     }
-    // next tile's logits (matrix cores) ...
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-      for (int c = 0; c < NCH; ++c)
-        zn = M::mma(BF16 ? za[kb][c % PRE] : tile_frag_w<BF16>(wr[b1], rbase, n, kb, c, g), hf[kb][c], zn);
-    // ... while this tile's numerators are formed (vector units)
-    float p[16];
     float ps = 0.0f;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      p[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, -m_run));
-      ps += p[r];
-    }
+    for (int r = 0; r < 16; ++r) ps += p[r];
     s_run += ps;
     Fr pf[NCH];
 #pragma unroll
@@ -368,6 +375,12 @@ __device__ __forceinline__ void merge_splits(int i, int splits, const float* __r
   }
 }
 
+// Row of workgroup b in a launch of one workgroup per row over n rows.
+// Workgroups are dealt to the 8 XCDs in turn; giving each XCD a contiguous
+// range of rows lets one L2 serve the cache lines that neighbouring rows share
+// in the per-split (max, sum) arrays, instead of every XCD fetching them all.
+__device__ __forceinline__ int xcd_row(int b, int n) { return n % 8 == 0 ? (b % 8) * (n / 8) + b / 8 : b; }
+
 template <bool BF16>
 __global__ __launch_bounds__(CMB_THREADS) void k_out_lse_targets(
     int splits, const float* __restrict__ m_part, const float* __restrict__ s_part, int ld_part,
@@ -378,7 +391,7 @@ __global__ __launch_bounds__(CMB_THREADS) void k_out_lse_targets(
   __shared__ float red_m[CMB_WAVES];
   __shared__ float red_t[CMB_WAVES][HID];
   __shared__ float red_z[CMB_WAVES];
-  const int i = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int i = xcd_row((int)blockIdx.x, (int)gridDim.x), t = threadIdx.x, lane = t & 63, w = t >> 6;
   {
     float mg = -INFINITY, St = 0.0f;
     for (int k = t; k < splits; k += CMB_THREADS)
@@ -449,7 +462,7 @@ __global__ __launch_bounds__(DA_THREADS) void k_out_dA1(int splits, const float*
   __shared__ float red_o[CMB_GROUPS][HID];
   __shared__ float red_s[CMB_GROUPS];
   __shared__ float red_m[CMB_GROUPS];
-  const int i = blockIdx.x, t = threadIdx.x;
+  const int i = xcd_row((int)blockIdx.x, (int)gridDim.x), t = threadIdx.x;
   const int grp = t >> 5, h4 = (t & 31) * 4;
   float mg, St;
   float4 O;
