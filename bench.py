@@ -321,7 +321,8 @@ def run_elastic(args):
         "config": {"workload": "elastic-4x-wide-label", "n_features": w.n_features, "n_labels": w.n_labels,
                    "hidden": H, "replicas": n, "b_min": b_min, "b_max": b_max, "megabatch": mega,
                    "global_batch": mega, "clock": "timed", "weights": "samples", "momentum": 0.9,
-                   "parallelism": "4 replicas on 4 HIP streams", "step": "one round (dispatch + merge)"},
+                   "parallelism": "4 replicas on 4 HIP streams", "step": "one round (dispatch + merge)",
+                   "hw_queues": os.environ.get("GPU_MAX_HW_QUEUES")},
         "roofline": {"kernel": "merge", "bound": "hbm", "achieved": merge["GB/s"], "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": merge["hbm_frac"], "traffic": measured_traffic("elastic", n, "merge")},
         "cpu_baseline": cpu,
@@ -432,6 +433,14 @@ def main():
               f"configuration share a single MI355X, and the multi-GPU merge is a design, not a measured path.",
               file=sys.stderr)
         sys.exit(2)
+    if args.workload == "elastic" and "GPU_MAX_HW_QUEUES" not in os.environ:
+        # The elastic round runs every replica on a model stream and an internal
+        # stream of its own.  With the runtime's default of 4 hardware queues,
+        # several of those streams share a queue, and the order in which a shared
+        # queue serves them, not the replicas' speed, decides which replica is
+        # free first: Alg. 1 then drives two of the four batch sizes to b_min.
+        # One hardware queue per stream (read when the runtime starts) avoids it.
+        os.environ["GPU_MAX_HW_QUEUES"] = "16"
     import torch
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
