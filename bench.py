@@ -498,10 +498,16 @@ def main():
         torch.cuda.synchronize()
         t_start.record(stream)
         used = []
+        h0 = time.perf_counter()
+        n_host = min(K, 16)
         for i in range(K):
             j = (W + i) % n_full
             used.append(j)
             asgd.asgd_train_step(m, xs[j], ys[j], lr)
+            if i + 1 == n_host:
+                # the host's own time to issue a step, taken over the first steps only (later
+                # calls can wait for room in the device queue)
+                host_ms = (time.perf_counter() - h0) * 1e3 / n_host
         t_end.record(stream)
         torch.cuda.synchronize()
         ms = t_start.elapsed_time(t_end)
@@ -587,6 +593,8 @@ def main():
         "cpu_baseline": cpu,
         "settle": {"ms": args.settle_ms, "steps": n_settle,
                    "why": "untimed load before the warm-up steps: the GPU's clocks ramp for tens of ms after idle"},
+        # host time to issue one step's launches: when it reaches ms_per_step the GPU waits for the host
+        "host_ms_per_step": round(host_ms, 4),
         "kernels": kernels,
     }
     print(json.dumps(out), flush=True)

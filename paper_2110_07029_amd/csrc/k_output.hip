@@ -403,7 +403,11 @@ __global__ __launch_bounds__(CMB_THREADS) void k_out_lse_targets(
       red_m[w] = mg;
     }
   }
-  // target terms: wave w takes labels q = w, w + 8, ... of row i; lane owns hidden 2l, 2l+1
+  // target terms: wave w takes labels q = w, w + 8, ... of row i, in that
+  // order; lane owns hidden 2l, 2l+1.  The row's label ids are read
+  // lane-parallel (every wave counts the valid ones), and a wave's W2 rows load
+  // TGT_BATCH at a time ahead of their reductions.
+  constexpr int TGT_BATCH = 4;
   float tw0 = 0.0f, tw1 = 0.0f, zw = 0.0f;
   int cnt = 0;
   if (has_y) {
@@ -414,20 +418,42 @@ __global__ __launch_bounds__(CMB_THREADS) void k_out_lse_targets(
     if (ye < ys) ye = ys;
     const float h0 = (float)H1[(size_t)i * HID + 2 * lane];
     const float h1v = (float)H1[(size_t)i * HID + 2 * lane + 1];
-    for (int q = ys; q < ye; ++q) {
-      const int lab = y.indices[q];
-      if (lab < 0 || lab >= L) continue;
-      ++cnt;
-      if (((q - ys) & (CMB_WAVES - 1)) != w) continue;
-      const float2 wv = *reinterpret_cast<const float2*>(W2 + (size_t)lab * HID + 2 * lane);
-      tw0 += wv.x;
-      tw1 += wv.y;
-      float o0 = wv.x, o1 = wv.y;
-      if constexpr (BF16) {
-        o0 = (float)(bf16)wv.x;
-        o1 = (float)(bf16)wv.y;
+    for (int q0 = ys; q0 < ye; q0 += 64) {
+      const int q = q0 + lane;
+      const int lab = q < ye ? y.indices[q] : -1;
+      cnt += __popcll(__ballot(lab >= 0 && lab < L));
+    }
+    // this wave's labels: the k-th is q = ys + w + 8k, k < mine; 64 per pass
+    const int mine = (ye - ys - w + CMB_WAVES - 1) / CMB_WAVES;
+    for (int k0 = 0; k0 < mine; k0 += 64) {
+      const int qk = ys + w + CMB_WAVES * (k0 + lane);
+      const int labv = k0 + lane < mine ? y.indices[qk] : -1;
+      const int nk = min(64, mine - k0);
+      for (int u0 = 0; u0 < nk; u0 += TGT_BATCH) {
+        float2 wv[TGT_BATCH];
+        float bv[TGT_BATCH];
+        bool ok[TGT_BATCH];
+#pragma unroll
+        for (int u = 0; u < TGT_BATCH; ++u) {
+          const int lab = __builtin_amdgcn_readlane(labv, min(u0 + u, nk - 1));
+          ok[u] = u0 + u < nk && lab >= 0 && lab < L;
+          const int lb = ok[u] ? lab : 0;
+          wv[u] = *reinterpret_cast<const float2*>(W2 + (size_t)lb * HID + 2 * lane);
+          bv[u] = b2[lb];
+        }
+#pragma unroll
+        for (int u = 0; u < TGT_BATCH; ++u) {
+          if (!ok[u]) continue;
+          tw0 += wv[u].x;
+          tw1 += wv[u].y;
+          float o0 = wv[u].x, o1 = wv[u].y;
+          if constexpr (BF16) {
+            o0 = (float)(bf16)wv[u].x;
+            o1 = (float)(bf16)wv[u].y;
+          }
+          zw += wave_sum(fmaf(h0, o0, h1v * o1)) + bv[u];
+        }
       }
-      zw += wave_sum(fmaf(h0, o0, h1v * o1)) + b2[lab];
     }
     red_t[w][2 * lane] = tw0;
     red_t[w][2 * lane + 1] = tw1;
