@@ -49,22 +49,30 @@ __global__ __launch_bounds__(SORT_THREADS) void k_sort_hist(const int32_t* __res
 // totals gives every digit's base.
 constexpr int SCAN_THREADS = 1024;
 constexpr int SCAN_DPT = (1 << SORT_MAX_BITS) / SCAN_THREADS;  // digits per thread
+constexpr int SCAN_BATCH = 16;  // chunk counts loaded together
 
 __global__ __launch_bounds__(SCAN_THREADS) void k_sort_scan(const int32_t* __restrict__ hist,
                                                             int nblk, int ndig,
                                                             int32_t* __restrict__ offs) {
   __shared__ int wsum[SCAN_THREADS / 64];
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  // (the chunks' counts are read SCAN_BATCH at a time, all loads in flight
+  // before the first sum)
   int tot[SCAN_DPT];
 #pragma unroll
   for (int k = 0; k < SCAN_DPT; ++k) tot[k] = 0;
-#pragma unroll 8
-  for (int b = 0; b < nblk; ++b)
 #pragma unroll
-    for (int k = 0; k < SCAN_DPT; ++k) {
-      const int d = t + k * SCAN_THREADS;
-      if (d < ndig) tot[k] += hist[(size_t)b * ndig + d];
+  for (int k = 0; k < SCAN_DPT; ++k) {
+    const int d = t + k * SCAN_THREADS;
+    if (d >= ndig) continue;
+    for (int b0 = 0; b0 < nblk; b0 += SCAN_BATCH) {
+      int c[SCAN_BATCH];
+#pragma unroll
+      for (int j = 0; j < SCAN_BATCH; ++j) c[j] = b0 + j < nblk ? hist[(size_t)(b0 + j) * ndig + d] : 0;
+#pragma unroll
+      for (int j = 0; j < SCAN_BATCH; ++j) tot[k] += c[j];
     }
+  }
   // digits in order d = t + k * SCAN_THREADS: scan the block once per k
   int carry = 0;
 #pragma unroll
@@ -92,18 +100,22 @@ __global__ __launch_bounds__(SCAN_THREADS) void k_sort_scan(const int32_t* __res
     __syncthreads();
     tot[k] = base;  // becomes the running offset of digit t + k * SCAN_THREADS
   }
-#pragma unroll 8
-  for (int b = 0; b < nblk; ++b)
 #pragma unroll
-    for (int k = 0; k < SCAN_DPT; ++k) {
-      const int d = t + k * SCAN_THREADS;
-      if (d < ndig) {
-        const size_t i = (size_t)b * ndig + d;
-        const int c = hist[i];
-        offs[i] = tot[k];
-        tot[k] += c;
-      }
+  for (int k = 0; k < SCAN_DPT; ++k) {
+    const int d = t + k * SCAN_THREADS;
+    if (d >= ndig) continue;
+    for (int b0 = 0; b0 < nblk; b0 += SCAN_BATCH) {
+      int c[SCAN_BATCH];
+#pragma unroll
+      for (int j = 0; j < SCAN_BATCH; ++j) c[j] = b0 + j < nblk ? hist[(size_t)(b0 + j) * ndig + d] : 0;
+#pragma unroll
+      for (int j = 0; j < SCAN_BATCH; ++j)
+        if (b0 + j < nblk) {
+          offs[(size_t)(b0 + j) * ndig + d] = tot[k];
+          tot[k] += c[j];
+        }
     }
+  }
 }
 
 __global__ __launch_bounds__(SORT_THREADS) void k_sort_scatter(
