@@ -46,22 +46,25 @@ hipError_t launch_fill_int(int32_t* p, int32_t v, int64_t n, hipStream_t st) {
 
 // ---------------------------------------------------------------------------
 // A1[i] = b1 + sum_{(f, v) in row i} v * W1[f];  H1 = max(A1, 0).
-// One workgroup (8 wavefronts) per sample row.  Lane l owns hidden units 2l
-// and 2l+1, so every W1 row is one coalesced 512-byte access.  The row's
-// entries are split into 8 contiguous ranges, one per wavefront; a wavefront
+// One workgroup (8 wavefronts, or 16 for batches whose rows average 160
+// entries or more) per sample row.  Lane l owns hidden units 2l and 2l+1, so
+// every W1 row is one coalesced 512-byte access.  The row's entries are split
+// into one contiguous range per wavefront; a wavefront
 // loads up to 64 (id, value) pairs at once (one per lane, also writing their
 // sort keys), broadcasts them with readlane and issues 16 W1 row loads before
 // the first is used.  Lanes past the range carry id -1, so a partial group of
 // 16 costs one round trip like a full one (the step time follows the longest
-// row of the batch, and nnz per row is heavy-tailed).  The 8 partial sums are
+// row of the batch, and nnz per row is heavy-tailed).  The partial sums are
 // added in wavefront order, then b1.
 // ---------------------------------------------------------------------------
 constexpr int GATHER_WAVES = 8;
+constexpr int GATHER_WAVES_LONG = 16;
+constexpr int GATHER_LONG_ROW = 160;  // mean entries per row from which 16 wavefronts take a row
 constexpr int GATHER_UNROLL = 16;
 static_assert(64 % GATHER_UNROLL == 0, "readlane indices stay below 64");
 
-template <bool BF16>
-__global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
+template <bool BF16, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void k_gather_fwd(
     CsrDev x, CsrDev y, int has_y, const float* __restrict__ W1, const float* __restrict__ b1,
     int F, int L, float* __restrict__ A1, typename Mma<BF16>::elem* __restrict__ H1,
     typename Mma<BF16>::elem* __restrict__ H1T, int rows_pad, int ld_t, int32_t* __restrict__ keys,
@@ -69,7 +72,7 @@ __global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
     float* __restrict__ rw,
     int32_t* __restrict__ err, int validate) {
   using E = typename Mma<BF16>::elem;
-  __shared__ float2 part[GATHER_WAVES][64];
+  __shared__ float2 part[WAVES][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i = blockIdx.x;
   const int h0 = 2 * lane;
@@ -93,7 +96,7 @@ __global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
     e = min(e, base + x.nnz);
     if (e < s) e = s;
   }
-  const int per = (e - s + GATHER_WAVES - 1) / GATHER_WAVES;
+  const int per = (e - s + WAVES - 1) / WAVES;
   const int ws = min(e, s + wave * per), we = min(e, ws + per);
   float2 acc = make_float2(0.0f, 0.0f);
   for (int p0 = ws; p0 < we; p0 += 64) {
@@ -138,7 +141,7 @@ __global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
   }
   part[wave][lane] = acc;
 
-  if (has_y && wave == GATHER_WAVES - 1) {
+  if (has_y && wave == WAVES - 1) {
     const int ybase = y.indptr[0];
     int ys = y.indptr[i], ye = y.indptr[i + 1];
     if (ys < ybase || ye > ybase + y.nnz || ye < ys) {
@@ -167,7 +170,7 @@ __global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
   if (wave == 0) {
     float2 a = part[0][lane];
 #pragma unroll
-    for (int k = 1; k < GATHER_WAVES; ++k) {
+    for (int k = 1; k < WAVES; ++k) {
       a.x += part[k][lane].x;
       a.y += part[k][lane].y;
     }
@@ -190,16 +193,24 @@ hipError_t launch_gather_fwd(bool use_bf16, const CsrDev& x, const CsrDev* y, co
                              int rows_pad, int ld_t, int32_t* keys, int32_t* row_of,
                              int32_t* lkeys, int32_t* lrow, float* rw, int32_t* err, int validate,
                              hipStream_t st) {
-  const dim3 grid(rows_pad), block(64 * GATHER_WAVES);
   CsrDev yy = y ? *y : CsrDev{0, 0, 0, nullptr, nullptr, nullptr};
-  if (use_bf16)
-    hipLaunchKernelGGL(k_gather_fwd<true>, grid, block, 0, st, x, yy, y != nullptr, W1, b1, F, L,
-                       A1, (bf16*)H1, (bf16*)H1T, rows_pad, ld_t, keys, row_of, lkeys, lrow, rw, err,
-                       validate);
-  else
-    hipLaunchKernelGGL(k_gather_fwd<false>, grid, block, 0, st, x, yy, y != nullptr, W1, b1, F, L,
-                       A1, (float*)H1, (float*)H1T, rows_pad, ld_t, keys, row_of, lkeys, lrow, rw, err,
-                       validate);
+  const bool lng = (int64_t)x.nnz >= (int64_t)GATHER_LONG_ROW * x.n_rows;
+  const dim3 grid(rows_pad), block(64 * (lng ? GATHER_WAVES_LONG : GATHER_WAVES));
+  auto go = [&](auto kern, auto* h1, auto* h1t) {
+    hipLaunchKernelGGL(kern, grid, block, 0, st, x, yy, y != nullptr, W1, b1, F, L, A1, h1, h1t, rows_pad, ld_t,
+                       keys, row_of, lkeys, lrow, rw, err, validate);
+  };
+  if (use_bf16) {
+    if (lng)
+      go(k_gather_fwd<true, GATHER_WAVES_LONG>, (bf16*)H1, (bf16*)H1T);
+    else
+      go(k_gather_fwd<true, GATHER_WAVES>, (bf16*)H1, (bf16*)H1T);
+  } else {
+    if (lng)
+      go(k_gather_fwd<false, GATHER_WAVES_LONG>, (float*)H1, (float*)H1T);
+    else
+      go(k_gather_fwd<false, GATHER_WAVES>, (float*)H1, (float*)H1T);
+  }
   return hipGetLastError();
 }
 
