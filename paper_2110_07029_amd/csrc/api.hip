@@ -126,6 +126,7 @@ struct asgd_model {
   int rows_pad_max = 0;  // rows of the output-layer operands
   int elem = 2;          // bytes per operand element
   float* A1 = nullptr;
+  float* gpart = nullptr;  // partial first-layer sums of rows split over several workgroups
   float* A2 = nullptr;   // second hidden layer: pre-activation and its gradient
   float* dA2 = nullptr;
   void* H1 = nullptr;    // the output layer's input in its operand type (H1, or H2 with the extra layer)
@@ -226,6 +227,8 @@ int64_t layout_workspace(asgd_model* m, char* base) {
   m->H1 = m->H1b[0];
   m->H1T = m->H1Tb[0];
   m->rw = m->rwb[0];
+  // (only a batch with max_nnz >= GATHER_LONG_ROW entries can average that many per row)
+  m->gpart = c.max_nnz >= GATHER_LONG_ROW ? carve<float>(p, (int64_t)GATHER_SPLIT * rp * HID) : nullptr;
   m->tw = carve<float>(p, (int64_t)rp * HID);
   m->dA1 = carve<float>(p, (int64_t)rp * HID);
   m->lse = carve<float>(p, rp);
@@ -356,7 +359,7 @@ asgd_status run_gather(asgd_model* m, const asgd_csr* x, const asgd_csr* y, hipS
   TIMED_ON(m, ASGD_K_GATHER, st, launch_gather_fwd(m->bf16, xd, y ? &yd : nullptr, m->W1(), m->b1(), m->F, m->L,
                                                    m->A1, m->H1, m->H1T, rows_pad, m->rows_pad_max, m->keys,
                                                    m->row_of, m->lkeys, m->lrow, m->rw, m->err, validate ? 1 : 0,
-                                                   st));
+                                                   m->gpart, st));
   if (m->extra)
     TIMED_ON(m, ASGD_K_DENSE_FWD, st, launch_dense_fwd(m->bf16, m->A1, m->Wh(), m->bh(), B, rows_pad, m->A2,
                                                        m->H1, m->H1T, m->rows_pad_max, st));

@@ -28,11 +28,16 @@ hipError_t launch_fill_int(int32_t* p, int32_t v, int64_t n, hipStream_t st);
 // [128 x ld_t]; rows in [B, rows_pad) are zero.  Feature entry p (0 <= p < x.nnz): keys[p] = feature id (F if
 // invalid), row_of[p] = its row.  With y != NULL, label entry q: lkeys[q] =
 // label id (L if invalid), lrow[q] = its row, and rw[i] = 1/|Y_i|.
+// Batches whose rows average GATHER_LONG_ROW entries or more split every row
+// over GATHER_SPLIT workgroups; gpart: workspace of GATHER_SPLIT x ld_t x HID
+// floats for their partial sums (ld_t >= rows_pad).
+constexpr int GATHER_SPLIT = 4;
+constexpr int GATHER_LONG_ROW = 160;
 hipError_t launch_gather_fwd(bool use_bf16, const CsrDev& x, const CsrDev* y, const float* W1,
                              const float* b1, int F, int L, float* A1, void* H1, void* H1T,
                              int rows_pad, int ld_t, int32_t* keys, int32_t* row_of,
                              int32_t* lkeys, int32_t* lrow, float* rw, int32_t* err, int validate,
-                             hipStream_t st);
+                             float* gpart, hipStream_t st);
 
 // ---- stable LSD radix sort of (key, position) -----------------------------
 constexpr int SORT_CHUNK = 1024;   // keys per workgroup

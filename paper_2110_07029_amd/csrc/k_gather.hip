@@ -46,38 +46,39 @@ hipError_t launch_fill_int(int32_t* p, int32_t v, int64_t n, hipStream_t st) {
 
 // ---------------------------------------------------------------------------
 // A1[i] = b1 + sum_{(f, v) in row i} v * W1[f];  H1 = max(A1, 0).
-// One workgroup (8 wavefronts, or 16 for batches whose rows average 160
-// entries or more) per sample row.  Lane l owns hidden units 2l and 2l+1, so
-// every W1 row is one coalesced 512-byte access.  The row's entries are split
-// into one contiguous range per wavefront; a wavefront
+// One workgroup (8 wavefronts) per sample row; for batches whose rows average
+// GATHER_LONG_ROW entries or more, GATHER_SPLIT workgroups per row, each
+// writing its partial sum, and a second launch adds them (the step time
+// follows the longest row, which then spreads over several CUs).  Lane l owns
+// hidden units 2l and 2l+1, so every W1 row is one coalesced 512-byte access.
+// The row's entries are split into one contiguous range per wavefront; a wavefront
 // loads up to 64 (id, value) pairs at once (one per lane, also writing their
 // sort keys), broadcasts them with readlane and issues 16 W1 row loads before
 // the first is used.  Lanes past the range carry id -1, so a partial group of
 // 16 costs one round trip like a full one (the step time follows the longest
 // row of the batch, and nnz per row is heavy-tailed).  The partial sums are
-// added in wavefront order, then b1.
+// added in wavefront order (then in workgroup order), then b1.
 // ---------------------------------------------------------------------------
 constexpr int GATHER_WAVES = 8;
-constexpr int GATHER_WAVES_LONG = 16;
-constexpr int GATHER_LONG_ROW = 160;  // mean entries per row from which 16 wavefronts take a row
 constexpr int GATHER_UNROLL = 16;
 static_assert(64 % GATHER_UNROLL == 0, "readlane indices stay below 64");
 
-template <bool BF16, int WAVES>
-__global__ __launch_bounds__(64 * WAVES) void k_gather_fwd(
+template <bool BF16, int SPLIT>
+__global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
     CsrDev x, CsrDev y, int has_y, const float* __restrict__ W1, const float* __restrict__ b1,
     int F, int L, float* __restrict__ A1, typename Mma<BF16>::elem* __restrict__ H1,
     typename Mma<BF16>::elem* __restrict__ H1T, int rows_pad, int ld_t, int32_t* __restrict__ keys,
     int32_t* __restrict__ row_of, int32_t* __restrict__ lkeys, int32_t* __restrict__ lrow,
     float* __restrict__ rw,
-    int32_t* __restrict__ err, int validate) {
+    int32_t* __restrict__ err, int validate, float* __restrict__ gpart) {
   using E = typename Mma<BF16>::elem;
+  constexpr int WAVES = GATHER_WAVES;
   __shared__ float2 part[WAVES][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int i = blockIdx.x;
+  const int i = (int)blockIdx.x / SPLIT, piece = (int)blockIdx.x % SPLIT;
   const int h0 = 2 * lane;
   if (i >= x.n_rows) {  // padding rows of the output-layer operands are zero
-    if (wave == 0) {
+    if (wave == 0 && piece == 0) {
       H1[(size_t)i * HID + h0] = (E)0.0f;
       H1[(size_t)i * HID + h0 + 1] = (E)0.0f;
       if constexpr (!BF16) {  // the transposed copy is read only by the fp32 backward
@@ -96,8 +97,10 @@ __global__ __launch_bounds__(64 * WAVES) void k_gather_fwd(
     e = min(e, base + x.nnz);
     if (e < s) e = s;
   }
-  const int per = (e - s + WAVES - 1) / WAVES;
-  const int ws = min(e, s + wave * per), we = min(e, ws + per);
+  // wavefront gw of the row's SPLIT * WAVES takes the gw-th contiguous range
+  const int gw = piece * WAVES + wave;
+  const int per = (e - s + SPLIT * WAVES - 1) / (SPLIT * WAVES);
+  const int ws = min(e, s + gw * per), we = min(e, ws + per);
   float2 acc = make_float2(0.0f, 0.0f);
   for (int p0 = ws; p0 < we; p0 += 64) {
     const int p = p0 + lane;
@@ -141,7 +144,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_gather_fwd(
   }
   part[wave][lane] = acc;
 
-  if (has_y && wave == WAVES - 1) {
+  if (has_y && piece == 0 && wave == WAVES - 1) {
     const int ybase = y.indptr[0];
     int ys = y.indptr[i], ye = y.indptr[i + 1];
     if (ys < ybase || ye > ybase + y.nnz || ye < ys) {
@@ -174,6 +177,10 @@ __global__ __launch_bounds__(64 * WAVES) void k_gather_fwd(
       a.x += part[k][lane].x;
       a.y += part[k][lane].y;
     }
+    if constexpr (SPLIT > 1) {
+      *reinterpret_cast<float2*>(gpart + ((size_t)piece * ld_t + i) * HID + h0) = a;
+      return;
+    }
     const float2 bb = *reinterpret_cast<const float2*>(b1 + h0);
     a.x = bb.x + a.x;
     a.y = bb.y + a.y;
@@ -188,28 +195,64 @@ __global__ __launch_bounds__(64 * WAVES) void k_gather_fwd(
   }
 }
 
+// Rows split over GATHER_SPLIT workgroups: A1 = b1 + the pieces' sums in
+// piece order, then H1 (and H1^T for fp32 operands) as above.
+template <bool BF16>
+__global__ __launch_bounds__(64) void k_gather_finish(int n_rows, const float* __restrict__ gpart, int ld_t,
+                                                      const float* __restrict__ b1, float* __restrict__ A1,
+                                                      typename Mma<BF16>::elem* __restrict__ H1,
+                                                      typename Mma<BF16>::elem* __restrict__ H1T) {
+  using E = typename Mma<BF16>::elem;
+  const int i = blockIdx.x, h0 = 2 * threadIdx.x;
+  if (i >= n_rows) return;
+  float2 a = *reinterpret_cast<const float2*>(gpart + (size_t)i * HID + h0);
+#pragma unroll
+  for (int k = 1; k < GATHER_SPLIT; ++k) {
+    const float2 v = *reinterpret_cast<const float2*>(gpart + ((size_t)k * ld_t + i) * HID + h0);
+    a.x += v.x;
+    a.y += v.y;
+  }
+  const float2 bb = *reinterpret_cast<const float2*>(b1 + h0);
+  a.x = bb.x + a.x;
+  a.y = bb.y + a.y;
+  *reinterpret_cast<float2*>(A1 + (size_t)i * HID + h0) = a;
+  const float r0 = fmaxf(a.x, 0.0f), r1 = fmaxf(a.y, 0.0f);
+  H1[(size_t)i * HID + h0] = (E)r0;
+  H1[(size_t)i * HID + h0 + 1] = (E)r1;
+  if constexpr (!BF16) {
+    H1T[(size_t)h0 * ld_t + i] = (E)r0;
+    H1T[(size_t)(h0 + 1) * ld_t + i] = (E)r1;
+  }
+}
+
 hipError_t launch_gather_fwd(bool use_bf16, const CsrDev& x, const CsrDev* y, const float* W1,
                              const float* b1, int F, int L, float* A1, void* H1, void* H1T,
                              int rows_pad, int ld_t, int32_t* keys, int32_t* row_of,
                              int32_t* lkeys, int32_t* lrow, float* rw, int32_t* err, int validate,
-                             hipStream_t st) {
+                             float* gpart, hipStream_t st) {
   CsrDev yy = y ? *y : CsrDev{0, 0, 0, nullptr, nullptr, nullptr};
-  const bool lng = (int64_t)x.nnz >= (int64_t)GATHER_LONG_ROW * x.n_rows;
-  const dim3 grid(rows_pad), block(64 * (lng ? GATHER_WAVES_LONG : GATHER_WAVES));
-  auto go = [&](auto kern, auto* h1, auto* h1t) {
-    hipLaunchKernelGGL(kern, grid, block, 0, st, x, yy, y != nullptr, W1, b1, F, L, A1, h1, h1t, rows_pad, ld_t,
-                       keys, row_of, lkeys, lrow, rw, err, validate);
+  const bool split = gpart && x.n_rows > 0 && (int64_t)x.nnz >= (int64_t)GATHER_LONG_ROW * x.n_rows;
+  const dim3 block(64 * GATHER_WAVES);
+  auto go = [&](auto kern, int pieces, auto* h1, auto* h1t) {
+    hipLaunchKernelGGL(kern, dim3(rows_pad * pieces), block, 0, st, x, yy, y != nullptr, W1, b1, F, L, A1, h1,
+                       h1t, rows_pad, ld_t, keys, row_of, lkeys, lrow, rw, err, validate, gpart);
   };
   if (use_bf16) {
-    if (lng)
-      go(k_gather_fwd<true, GATHER_WAVES_LONG>, (bf16*)H1, (bf16*)H1T);
-    else
-      go(k_gather_fwd<true, GATHER_WAVES>, (bf16*)H1, (bf16*)H1T);
+    if (split) {
+      go(k_gather_fwd<true, GATHER_SPLIT>, GATHER_SPLIT, (bf16*)H1, (bf16*)H1T);
+      hipLaunchKernelGGL(k_gather_finish<true>, dim3(x.n_rows), dim3(64), 0, st, x.n_rows, gpart, ld_t, b1, A1,
+                         (bf16*)H1, (bf16*)H1T);
+    } else {
+      go(k_gather_fwd<true, 1>, 1, (bf16*)H1, (bf16*)H1T);
+    }
   } else {
-    if (lng)
-      go(k_gather_fwd<false, GATHER_WAVES_LONG>, (float*)H1, (float*)H1T);
-    else
-      go(k_gather_fwd<false, GATHER_WAVES>, (float*)H1, (float*)H1T);
+    if (split) {
+      go(k_gather_fwd<false, GATHER_SPLIT>, GATHER_SPLIT, (float*)H1, (float*)H1T);
+      hipLaunchKernelGGL(k_gather_finish<false>, dim3(x.n_rows), dim3(64), 0, st, x.n_rows, gpart, ld_t, b1,
+                         A1, (float*)H1, (float*)H1T);
+    } else {
+      go(k_gather_fwd<false, 1>, 1, (float*)H1, (float*)H1T);
+    }
   }
   return hipGetLastError();
 }

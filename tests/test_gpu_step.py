@@ -192,6 +192,36 @@ def test_step_parity_with_22_bit_feature_ids():
         s.free()
 
 
+# rows of about 400 entries (lognormal, some thousands long): batches averaging
+# 160 entries or more per row split every row over several gather workgroups
+LONG_ROWS = synth.Workload("long-rows", 20_000, 3_000, 1_000, 128, 0.01, True, "lognormal", 5.6,
+                           0.9, 5_000, 1.05, "uniform", "poisson", 4.0, 1.2, 2)
+
+
+@pytest.mark.parametrize("rows,bf16", [((0, 128), True), ((128, 161), True), ((0, 128), False)])
+def test_step_parity_with_rows_split_over_gather_workgroups(rows, bf16):
+    """The gather's split path: every row over four workgroups, their partial
+    sums added by a second launch; A1 within its summation bound, the step's
+    updates within the parity bar."""
+    import torch
+    r0, r1 = rows
+    flush(f"step: long rows {rows} bf16={bf16}")
+    s = Setup(LONG_ROWS, 512, 128, bf16=bf16)
+    try:
+        xh, _ = s.host_batch(r0, r1)
+        assert (int(xh.indptr[-1]) - int(xh.indptr[0])) >= 160 * (r1 - r0)   # the split path runs
+        a1 = torch.empty((r1 - r0, 128), dtype=torch.float32, device="cuda")
+        asgd.asgd_debug_forward(s.m, s.xb(r0, r1), s.yb(r0, r1), a1_dev=a1)
+        torch.cuda.synchronize()
+        p = s.params()
+        ref = om.forward(p, xh, None, "fp32")
+        err = np.abs(a1.cpu().numpy().astype(np.float64) - ref["A1"])
+        assert np.all(err <= a1_bound(p, xh) + 1e-7 * np.abs(ref["A1"]))
+        _step_parity(s, r0, r1, 0.05, RTOL_BF16 if bf16 else RTOL_FP32, "fp32")
+    finally:
+        s.free()
+
+
 # more 32-label blocks than the forward launch's LDS holds counters for: the
 # label grouping then counts in global memory
 MANY_LABELS = synth.Workload("labels-1m", 5_000, 1_000_003, 128, 64, 0.01, True, "lognormal", 4.0,
