@@ -413,7 +413,7 @@ asgd_status run_forward(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int
   }
   TIMED_ON(m, ASGD_K_HIDDEN, da_stream, launch_out_dA1(B, s_eff, m->m_part, m->s_part, m->o_part, rows_pad, m->tw,
                                                        m->extra ? m->A2 : m->A1, m->extra ? m->dA2 : m->dA1,
-                                                       da_stream));
+                                                       da_stream == m->stream, da_stream));
   return ASGD_OK;
 }
 

@@ -85,9 +85,10 @@ hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2,
 hipError_t launch_out_lse_targets(bool use_bf16, int B, int splits, const float* m_part, const float* s_part,
                                   int ld_part, const float* W2, const float* b2, int L, const void* H1,
                                   const CsrDev* y, float* lse, float* loss_rows, float* tw, hipStream_t st);
-// Per row: dA1 = ((O/s - tw) / B) * [A1 > 0] from the forward's partials (reads no W2).
+// Per row: dA1 = ((O/s - tw) / B) * [A1 > 0] from the forward's partials (reads no W2);
+// wide: twice the threads per row (for a launch that runs alone, not beside the backward).
 hipError_t launch_out_dA1(int B, int splits, const float* m_part, const float* s_part, const float* o_part,
-                          int ld_part, const float* tw, const float* A1, float* dA1, hipStream_t st);
+                          int ld_part, const float* tw, const float* A1, float* dA1, bool wide, hipStream_t st);
 // Recompute Z per label tile, dZ = (softmax - T)/B, dW2 = dZ^T H1, db2; update W2, b2 in place.
 hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, const void* H1,
                           const void* H1T, int ld_t, int B, const float* lse, const float* rw,

@@ -325,16 +325,17 @@ hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2,
 //                      (runs beside the backward: it reads no W2).
 // k_out_lse_targets: 512 threads, one (max, sum) pair per thread merged by
 // wavefront reductions, 8 wavefronts x the row's labels for the target terms.
-// k_out_dA1: 256 threads = 8 split groups x 32 threads x 4 hidden units; each
-// group merges its splits online against its own running maximum, then the
-// groups are rescaled to the row's maximum (4 KB of LDS, so that it fits on a
-// CU beside the backward).  Every partial is combined in a fixed order, so the
-// results do not depend on scheduling.
+// k_out_dA1: G split groups x 32 threads x 4 hidden units; each group merges
+// its splits online against its own running maximum, then the groups are
+// rescaled to the row's maximum.  G = 8 (256 threads, 4 KB of LDS, so that it
+// fits on a CU beside the backward) or, when nothing runs beside it, 16.
+// Every partial is combined in a fixed order, so the results do not depend on
+// scheduling.
 // ---------------------------------------------------------------------------
 constexpr int CMB_THREADS = 512;
 constexpr int CMB_WAVES = CMB_THREADS / 64;   // 8
-constexpr int DA_THREADS = 256;
-constexpr int CMB_GROUPS = DA_THREADS / 32;   // 8
+constexpr int DA_GROUPS = 8;        // beside the backward: 256 threads, 4 KB of LDS
+constexpr int DA_GROUPS_WIDE = 16;  // on the model's stream, where nothing runs beside it
 
 // (m, s) <- the merge of two (maximum, sum of 2^(x - maximum)) pairs, base 2 or
 // natural alike through exp_fast (natural logarithms here)
@@ -347,7 +348,7 @@ __device__ __forceinline__ void ms_merge_ln(float& m, float& s, float m2, float 
 
 // Group grp's online merge of splits grp, grp + 16, ...: running maximum mg,
 // sum St and (WITH_O) the weighted O of hidden units h4 .. h4 + 3.
-template <bool WITH_O>
+template <bool WITH_O, int GROUPS>
 __device__ __forceinline__ void merge_splits(int i, int splits, const float* __restrict__ m_part,
                                              const float* __restrict__ s_part, const float* __restrict__ o_part,
                                              int ld_part, int grp, int h4, float& mg, float& St, float4& O) {
@@ -355,7 +356,7 @@ __device__ __forceinline__ void merge_splits(int i, int splits, const float* __r
   St = 0.0f;
   O = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
 #pragma unroll 8
-  for (int s = grp; s < splits; s += CMB_GROUPS) {
+  for (int s = grp; s < splits; s += GROUPS) {
     const size_t r = (size_t)s * ld_part + i;
     const float ms = m_part[r];
     const float ss = s_part[r];
@@ -480,19 +481,20 @@ __global__ __launch_bounds__(CMB_THREADS) void k_out_lse_targets(
   }
 }
 
-__global__ __launch_bounds__(DA_THREADS) void k_out_dA1(int splits, const float* __restrict__ m_part,
+template <int GROUPS>
+__global__ __launch_bounds__(32 * GROUPS) void k_out_dA1(int splits, const float* __restrict__ m_part,
                                                          const float* __restrict__ s_part,
                                                          const float* __restrict__ o_part, int ld_part,
                                                          const float* __restrict__ tw, const float* __restrict__ A1,
                                                          float invB, float* __restrict__ dA1) {
-  __shared__ float red_o[CMB_GROUPS][HID];
-  __shared__ float red_s[CMB_GROUPS];
-  __shared__ float red_m[CMB_GROUPS];
+  __shared__ float red_o[GROUPS][HID];
+  __shared__ float red_s[GROUPS];
+  __shared__ float red_m[GROUPS];
   const int i = xcd_row((int)blockIdx.x, (int)gridDim.x), t = threadIdx.x;
   const int grp = t >> 5, h4 = (t & 31) * 4;
   float mg, St;
   float4 O;
-  merge_splits<true>(i, splits, m_part, s_part, o_part, ld_part, grp, h4, mg, St, O);
+  merge_splits<true, GROUPS>(i, splits, m_part, s_part, o_part, ld_part, grp, h4, mg, St, O);
   *reinterpret_cast<float4*>(&red_o[grp][h4]) = O;
   if ((t & 31) == 0) {
     red_s[grp] = St;
@@ -502,10 +504,10 @@ __global__ __launch_bounds__(DA_THREADS) void k_out_dA1(int splits, const float*
   if (t < HID) {
     float M = red_m[0];
 #pragma unroll
-    for (int k = 1; k < CMB_GROUPS; ++k) M = fmaxf(M, red_m[k]);
+    for (int k = 1; k < GROUPS; ++k) M = fmaxf(M, red_m[k]);
     float Ot = 0.0f, Stot = 0.0f;
 #pragma unroll
-    for (int k = 0; k < CMB_GROUPS; ++k) {
+    for (int k = 0; k < GROUPS; ++k) {
       const float e = red_m[k] == -INFINITY ? 0.0f : exp_fast(red_m[k] - M);
       Ot = fmaf(e, red_o[k][t], Ot);
       Stot = fmaf(e, red_s[k], Stot);
@@ -529,9 +531,13 @@ hipError_t launch_out_lse_targets(bool use_bf16, int B, int splits, const float*
 }
 
 hipError_t launch_out_dA1(int B, int splits, const float* m_part, const float* s_part, const float* o_part,
-                          int ld_part, const float* tw, const float* A1, float* dA1, hipStream_t st) {
-  hipLaunchKernelGGL(k_out_dA1, dim3(B), dim3(DA_THREADS), 0, st, splits, m_part, s_part, o_part, ld_part, tw,
-                     A1, 1.0f / (float)B, dA1);
+                          int ld_part, const float* tw, const float* A1, float* dA1, bool wide, hipStream_t st) {
+  if (wide)
+    hipLaunchKernelGGL(k_out_dA1<DA_GROUPS_WIDE>, dim3(B), dim3(32 * DA_GROUPS_WIDE), 0, st, splits, m_part, s_part,
+                       o_part, ld_part, tw, A1, 1.0f / (float)B, dA1);
+  else
+    hipLaunchKernelGGL(k_out_dA1<DA_GROUPS>, dim3(B), dim3(32 * DA_GROUPS), 0, st, splits, m_part, s_part, o_part,
+                       ld_part, tw, A1, 1.0f / (float)B, dA1);
   return hipGetLastError();
 }
 
