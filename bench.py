@@ -433,7 +433,7 @@ def main():
               f"configuration share a single MI355X, and the multi-GPU merge is a design, not a measured path.",
               file=sys.stderr)
         sys.exit(2)
-    if args.workload == "elastic" and "GPU_MAX_HW_QUEUES" not in os.environ:
+    if args.workload == "elastic" and int(os.environ.get("GPU_MAX_HW_QUEUES", "0") or 0) < 16:
         # The elastic round runs every replica on a model stream and an internal
         # stream of its own.  With the runtime's default of 4 hardware queues,
         # several of those streams share a queue, and the order in which a shared
