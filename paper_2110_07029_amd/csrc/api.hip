@@ -403,17 +403,21 @@ asgd_status run_forward(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int
   TIMED(m, ASGD_K_OUT_FWD, launch_out_fwd_train(m->bf16, m->W2(), m->b2(), m->L, m->H1, B, splits, m->m_part,
                                m->s_part, m->o_part, rows_pad, labels, &m->label_plan, m->stream));
   CsrDev yd = y ? dev(y) : CsrDev{};
+  float* const A = m->extra ? m->A2 : m->A1;
+  float* const dA = m->extra ? m->dA2 : m->dA1;
+  // dA1 on the model's stream: in the same launch as lse and the target terms
+  const bool fused = y && da_stream == m->stream;
   TIMED(m, ASGD_K_OUT_COMBINE, launch_out_lse_targets(m->bf16, B, s_eff, m->m_part, m->s_part, rows_pad, m->W2(),
                                                       m->b2(), m->L, m->H1, y ? &yd : nullptr, m->lse,
-                                                      m->loss_rows, m->tw, m->stream));
-  if (!y) return ASGD_OK;
+                                                      m->loss_rows, m->tw, m->o_part, A, fused ? dA : nullptr,
+                                                      m->stream));
+  if (!y || fused) return ASGD_OK;
   if (da_stream != m->stream) {
     HIP_TRY(hipEventRecord(m->ev_dA1, m->stream));
     HIP_TRY(hipStreamWaitEvent(da_stream, m->ev_dA1, 0));
   }
   TIMED_ON(m, ASGD_K_HIDDEN, da_stream, launch_out_dA1(B, s_eff, m->m_part, m->s_part, m->o_part, rows_pad, m->tw,
-                                                       m->extra ? m->A2 : m->A1, m->extra ? m->dA2 : m->dA1,
-                                                       da_stream == m->stream, da_stream));
+                                                       A, dA, da_stream == m->stream, da_stream));
   return ASGD_OK;
 }
 

@@ -82,9 +82,12 @@ hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2,
                                 int ld_part, const LabelJob* job, const LabelJobPlan* plan, hipStream_t st);
 // Per row, after the forward: lse, and with y the loss and tw = mean_{y in Y_i} W2[y]
 // [B x 128] (reads W2 before the backward updates it).
+// With y and dA1 (non-null), the same launch also forms dA1 = ((O/s - tw) / B) * [A1 > 0]
+// from the partials (o_part, A1 as for launch_out_dA1); dA1 null: lse and targets only.
 hipError_t launch_out_lse_targets(bool use_bf16, int B, int splits, const float* m_part, const float* s_part,
                                   int ld_part, const float* W2, const float* b2, int L, const void* H1,
-                                  const CsrDev* y, float* lse, float* loss_rows, float* tw, hipStream_t st);
+                                  const CsrDev* y, float* lse, float* loss_rows, float* tw, const float* o_part,
+                                  const float* A1, float* dA1, hipStream_t st);
 // Per row: dA1 = ((O/s - tw) / B) * [A1 > 0] from the forward's partials (reads no W2);
 // wide: twice the threads per row (for a launch that runs alone, not beside the backward).
 hipError_t launch_out_dA1(int B, int splits, const float* m_part, const float* s_part, const float* o_part,

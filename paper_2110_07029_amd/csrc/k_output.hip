@@ -323,6 +323,8 @@ hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2,
 //   k_out_dA1          the splits' O merged against the same maxima,
 //                      dH1 = (O/s - mean_{y in Y_i} W2[y]) / B, dA1 = dH1 [A1 > 0]
 //                      (runs beside the backward: it reads no W2).
+// A step that forms dA1 on the model's stream anyway runs both in one launch
+// (k_out_lse_targets<., true>).
 // k_out_lse_targets: 512 threads, one (max, sum) pair per thread merged by
 // wavefront reductions, 8 wavefronts x the row's labels for the target terms.
 // k_out_dA1: G split groups x 32 threads x 4 hidden units; each group merges
@@ -382,12 +384,53 @@ __device__ __forceinline__ void merge_splits(int i, int splits, const float* __r
 // in the per-split (max, sum) arrays, instead of every XCD fetching them all.
 __device__ __forceinline__ int xcd_row(int b, int n) { return n % 8 == 0 ? (b % 8) * (n / 8) + b / 8 : b; }
 
-template <bool BF16>
+// dA1 of row i from the forward's partials, by a workgroup of GROUPS x 32
+// threads (every thread calls it): each group merges its splits' O online
+// against its own running maximum, then the groups are rescaled to the row's
+// maximum; thread t < HID writes hidden unit t, with tw_t the row's mean target
+// weight of that unit.  red_o [GROUPS][HID], red_s and red_m [GROUPS]: LDS.
+template <int GROUPS>
+__device__ __forceinline__ void da1_row(int i, int splits, const float* __restrict__ m_part,
+                                        const float* __restrict__ s_part, const float* __restrict__ o_part,
+                                        int ld_part, float tw_t, const float* __restrict__ A1, float invB,
+                                        float* __restrict__ dA1, float (*red_o)[HID], float* red_s, float* red_m) {
+  const int t = threadIdx.x;
+  const int grp = t >> 5, h4 = (t & 31) * 4;
+  float mg, St;
+  float4 O;
+  merge_splits<true, GROUPS>(i, splits, m_part, s_part, o_part, ld_part, grp, h4, mg, St, O);
+  *reinterpret_cast<float4*>(&red_o[grp][h4]) = O;
+  if ((t & 31) == 0) {
+    red_s[grp] = St;
+    red_m[grp] = mg;
+  }
+  __syncthreads();
+  if (t < HID) {
+    float M = red_m[0];
+#pragma unroll
+    for (int k = 1; k < GROUPS; ++k) M = fmaxf(M, red_m[k]);
+    float Ot = 0.0f, Stot = 0.0f;
+#pragma unroll
+    for (int k = 0; k < GROUPS; ++k) {
+      const float e = red_m[k] == -INFINITY ? 0.0f : exp_fast(red_m[k] - M);
+      Ot = fmaf(e, red_o[k][t], Ot);
+      Stot = fmaf(e, red_s[k], Stot);
+    }
+    const float dh = (Ot / Stot - tw_t) * invB;
+    dA1[(size_t)i * HID + t] = A1[(size_t)i * HID + t] > 0.0f ? dh : 0.0f;
+  }
+}
+
+// DA: the row's dA1 as well, in the same workgroup (16 split groups), for a
+// step that runs it on the model's stream anyway: one launch instead of two.
+template <bool BF16, bool DA>
 __global__ __launch_bounds__(CMB_THREADS) void k_out_lse_targets(
     int splits, const float* __restrict__ m_part, const float* __restrict__ s_part, int ld_part,
     const float* __restrict__ W2, const float* __restrict__ b2, int L,
     const typename Mma<BF16>::elem* __restrict__ H1, CsrDev y, int has_y, float* __restrict__ lse_out,
-    float* __restrict__ loss_rows, float* __restrict__ tw_out) {
+    float* __restrict__ loss_rows, float* __restrict__ tw_out, const float* __restrict__ o_part,
+    const float* __restrict__ A1, float invB, float* __restrict__ dA1) {
+  static_assert(!DA || CMB_THREADS == 32 * DA_GROUPS_WIDE, "dA1 takes the workgroup as 16 split groups");
   __shared__ float red_s[CMB_WAVES];
   __shared__ float red_m[CMB_WAVES];
   __shared__ float red_t[CMB_WAVES][HID];
@@ -461,6 +504,7 @@ __global__ __launch_bounds__(CMB_THREADS) void k_out_lse_targets(
     if (lane == 0) red_z[w] = zw;
   }
   __syncthreads();
+  float my_tw = 0.0f;
   if (t < HID) {
     float M = red_m[0], Stot = red_s[0];
 #pragma unroll
@@ -476,57 +520,55 @@ __global__ __launch_bounds__(CMB_THREADS) void k_out_lse_targets(
       }
       const float inv_cnt = cnt > 0 ? 1.0f / (float)cnt : 0.0f;
       tw_out[(size_t)i * HID + t] = tw * inv_cnt;
+      my_tw = tw * inv_cnt;
       if (t == 0) loss_rows[i] = lse - zs * inv_cnt;
     }
+  }
+  if constexpr (DA) {
+    __shared__ float red_o[DA_GROUPS_WIDE][HID];
+    __shared__ float red_s2[DA_GROUPS_WIDE];
+    __shared__ float red_m2[DA_GROUPS_WIDE];
+    da1_row<DA_GROUPS_WIDE>(i, splits, m_part, s_part, o_part, ld_part, my_tw, A1, invB, dA1, red_o, red_s2,
+                            red_m2);
   }
 }
 
 template <int GROUPS>
 __global__ __launch_bounds__(32 * GROUPS) void k_out_dA1(int splits, const float* __restrict__ m_part,
-                                                         const float* __restrict__ s_part,
-                                                         const float* __restrict__ o_part, int ld_part,
-                                                         const float* __restrict__ tw, const float* __restrict__ A1,
-                                                         float invB, float* __restrict__ dA1) {
+                                                        const float* __restrict__ s_part,
+                                                        const float* __restrict__ o_part, int ld_part,
+                                                        const float* __restrict__ tw, const float* __restrict__ A1,
+                                                        float invB, float* __restrict__ dA1) {
   __shared__ float red_o[GROUPS][HID];
   __shared__ float red_s[GROUPS];
   __shared__ float red_m[GROUPS];
   const int i = xcd_row((int)blockIdx.x, (int)gridDim.x), t = threadIdx.x;
-  const int grp = t >> 5, h4 = (t & 31) * 4;
-  float mg, St;
-  float4 O;
-  merge_splits<true, GROUPS>(i, splits, m_part, s_part, o_part, ld_part, grp, h4, mg, St, O);
-  *reinterpret_cast<float4*>(&red_o[grp][h4]) = O;
-  if ((t & 31) == 0) {
-    red_s[grp] = St;
-    red_m[grp] = mg;
-  }
-  __syncthreads();
-  if (t < HID) {
-    float M = red_m[0];
-#pragma unroll
-    for (int k = 1; k < GROUPS; ++k) M = fmaxf(M, red_m[k]);
-    float Ot = 0.0f, Stot = 0.0f;
-#pragma unroll
-    for (int k = 0; k < GROUPS; ++k) {
-      const float e = red_m[k] == -INFINITY ? 0.0f : exp_fast(red_m[k] - M);
-      Ot = fmaf(e, red_o[k][t], Ot);
-      Stot = fmaf(e, red_s[k], Stot);
-    }
-    const float dh = (Ot / Stot - tw[(size_t)i * HID + t]) * invB;
-    dA1[(size_t)i * HID + t] = A1[(size_t)i * HID + t] > 0.0f ? dh : 0.0f;
-  }
+  const float tw_t = t < HID ? tw[(size_t)i * HID + t] : 0.0f;
+  da1_row<GROUPS>(i, splits, m_part, s_part, o_part, ld_part, tw_t, A1, invB, dA1, red_o, red_s, red_m);
 }
 
 hipError_t launch_out_lse_targets(bool use_bf16, int B, int splits, const float* m_part, const float* s_part,
                                   int ld_part, const float* W2, const float* b2, int L, const void* H1,
-                                  const CsrDev* y, float* lse, float* loss_rows, float* tw, hipStream_t st) {
+                                  const CsrDev* y, float* lse, float* loss_rows, float* tw, const float* o_part,
+                                  const float* A1, float* dA1, hipStream_t st) {
   CsrDev yy = y ? *y : CsrDev{0, 0, 0, nullptr, nullptr, nullptr};
-  if (use_bf16)
-    hipLaunchKernelGGL(k_out_lse_targets<true>, dim3(B), dim3(CMB_THREADS), 0, st, splits, m_part, s_part,
-                       ld_part, W2, b2, L, (const bf16*)H1, yy, y != nullptr, lse, loss_rows, tw);
-  else
-    hipLaunchKernelGGL(k_out_lse_targets<false>, dim3(B), dim3(CMB_THREADS), 0, st, splits, m_part, s_part,
-                       ld_part, W2, b2, L, (const float*)H1, yy, y != nullptr, lse, loss_rows, tw);
+  const bool da = y && dA1;
+  const float invB = 1.0f / (float)B;
+  auto go = [&](auto kern, auto* h1) {
+    hipLaunchKernelGGL(kern, dim3(B), dim3(CMB_THREADS), 0, st, splits, m_part, s_part, ld_part, W2, b2, L, h1, yy,
+                       y != nullptr, lse, loss_rows, tw, o_part, A1, invB, dA1);
+  };
+  if (use_bf16) {
+    if (da)
+      go(k_out_lse_targets<true, true>, (const bf16*)H1);
+    else
+      go(k_out_lse_targets<true, false>, (const bf16*)H1);
+  } else {
+    if (da)
+      go(k_out_lse_targets<false, true>, (const float*)H1);
+    else
+      go(k_out_lse_targets<false, false>, (const float*)H1);
+  }
   return hipGetLastError();
 }
 
