@@ -64,7 +64,10 @@ __device__ __forceinline__ void lds_copy16(const void* src, unsigned lds) {
                : "memory");
 }
 
-template <bool BF16, int MODE>
+// RS > 1 (global mode only): the RS wavefronts of a label block split its row
+// blocks (rb = rp, rp + RS, ...) and their dW2 / db2 partials meet in LDS, for
+// label spaces too small to give every wavefront a block of its own.
+template <bool BF16, int MODE, int RS>
 __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
     float* __restrict__ W2, float* __restrict__ b2, int L,
     const typename Mma<BF16>::elem* __restrict__ H1, const typename Mma<BF16>::elem* __restrict__ H1T,
@@ -78,6 +81,8 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
   constexpr bool LDS_H1 = MODE != BWD_GLOBAL;
   static_assert(!LDS_H1 || BF16, "LDS staging is for bf16 operands");
   static_assert(MODE != BWD_STAGED, "B <= 256 with bf16 operands runs k_out_bwd_prefetch");
+  static_assert(RS == 1 || (MODE == BWD_GLOBAL && BWD_WAVES % RS == 0), "row split: global mode");
+  constexpr int LPW = BWD_WAVES / RS;  // label blocks per workgroup at a time (row split)
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   const int nrb = (B + 31) >> 5;
   const int bpad = nrb * 32;
@@ -99,6 +104,9 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
   float* tw_s = reinterpret_cast<float*>(sp);
   sp += bpad * sizeof(float);
   uint32_t* mask = reinterpret_cast<uint32_t*>(sp) + wave * 32 * mstride;
+  sp += BWD_WAVES * 32 * mstride * sizeof(uint32_t);
+  // row split: the partial dW2 (64 values per lane) and db2 of wavefronts rp > 0
+  float* red = reinterpret_cast<float*>(sp);
 
   // Row constants of rows [r0, r0 + nrows) at LDS index (row - r0).
   auto stage_rows = [&](int r0, int nrows) {
@@ -160,16 +168,20 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
   const int n_blocks = (L + 31) >> 5;
   // global: each wave walks its own blocks; chunked: the workgroup walks
   // groups of 8 blocks together (a uniform trip count for the barriers)
-  const int n_iter_units = MODE == BWD_CHUNKED ? (n_blocks + BWD_WAVES - 1) / BWD_WAVES : n_blocks;
-  const int first = MODE == BWD_CHUNKED ? blockIdx.x : blockIdx.x * BWD_WAVES + wave;
-  const int step = MODE == BWD_CHUNKED ? gridDim.x : gridDim.x * BWD_WAVES;
+  // (row split: groups of LPW blocks, walked by the workgroup together)
+  const int n_iter_units = MODE == BWD_CHUNKED ? (n_blocks + BWD_WAVES - 1) / BWD_WAVES
+                           : RS > 1            ? (n_blocks + LPW - 1) / LPW
+                                               : n_blocks;
+  const int first = MODE == BWD_CHUNKED || RS > 1 ? blockIdx.x : blockIdx.x * BWD_WAVES + wave;
+  const int step = MODE == BWD_CHUNKED || RS > 1 ? gridDim.x : gridDim.x * BWD_WAVES;
+  const int rp = RS > 1 ? wave % RS : 0;  // this wavefront's share of the row blocks
   // chunked: chunks are consumed in the order (unit, chunk); kc counts them,
   // and chunk kc lives in buffer kc & 1.  The first one is requested here.
   const int nch = (bpad + BWD_CROWS - 1) / BWD_CROWS;
   int kc = 0;
   if (MODE == BWD_CHUNKED && first < n_iter_units) issue_chunk(0, h1b);
   for (int unit = first; unit < n_iter_units; unit += step) {
-    const int blk = MODE == BWD_CHUNKED ? unit * BWD_WAVES + wave : unit;
+    const int blk = MODE == BWD_CHUNKED ? unit * BWD_WAVES + wave : RS > 1 ? unit * LPW + wave / RS : unit;
     const bool bactive = blk < n_blocks;
     const int l0 = blk * 32;
     const int label = l0 + n;
@@ -313,11 +325,36 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
       }
     } else {
       if (has_targets) build_mask(lo, hi, pr0, 0, bpad);
-      for (int rb = 0; rb < nrb; ++rb) row_block(nullptr, rb, rb * 32);
+      if (bactive)
+        for (int rb = rp; rb < nrb; rb += RS) row_block(nullptr, rb, rb * 32);
+    }
+    if constexpr (RS > 1) {
+      // partials of wavefronts rp > 0 to LDS (value-major, lane-contiguous),
+      // added by wavefront rp = 0 in rp order
+      float* my = red + (size_t)((wave / RS) * (RS - 1) + rp - 1) * 65 * 64;
+      if (rp > 0) {
+#pragma unroll
+        for (int hb = 0; hb < 4; ++hb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) my[(16 * hb + r) * 64 + lane] = accw[hb][r];
+        my[64 * 64 + lane] = db2p;
+      }
+      __syncthreads();
+      if (rp == 0) {
+        for (int k = 1; k < RS; ++k) {
+          const float* o = red + (size_t)((wave / RS) * (RS - 1) + k - 1) * 65 * 64;
+#pragma unroll
+          for (int hb = 0; hb < 4; ++hb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) accw[hb][r] += o[(16 * hb + r) * 64 + lane];
+          db2p += o[64 * 64 + lane];
+        }
+      }
+      __syncthreads();  // the slots are free again for the next group
     }
 
     const float db2 = db2p + __shfl_xor(db2p, 32);
-    if (bactive && lvalid) {
+    if (bactive && lvalid && rp == 0) {
       float* wout = W2 + (size_t)label * HID;
 #pragma unroll
       for (int hb = 0; hb < 4; ++hb)
@@ -597,7 +634,7 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
   }
 }
 
-template <bool BF16, int MODE>
+template <bool BF16, int MODE, int RS>
 static hipError_t launch_bwd(int grid, size_t shm, hipStream_t st, float* W2, float* b2, int L,
                              const void* H1, const void* H1T, int ld_t, int B, const float* lse,
                              const float* rw, const int32_t* lbeg, const int32_t* lpair, float lr,
@@ -606,12 +643,12 @@ static hipError_t launch_bwd(int grid, size_t shm, hipStream_t st, float* W2, fl
   const float log2_invB = (float)log2((double)invB);
   static bool attr_done = false;
   if (!attr_done) {
-    hipError_t e = hipFuncSetAttribute((const void*)k_out_bwd<BF16, MODE>,
+    hipError_t e = hipFuncSetAttribute((const void*)k_out_bwd<BF16, MODE, RS>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (e != hipSuccess) return e;
     attr_done = true;
   }
-  hipLaunchKernelGGL((k_out_bwd<BF16, MODE>), dim3(grid), dim3(BWD_THREADS), shm, st, W2, b2, L,
+  hipLaunchKernelGGL((k_out_bwd<BF16, MODE, RS>), dim3(grid), dim3(BWD_THREADS), shm, st, W2, b2, L,
                      (const E*)H1, (const E*)H1T, ld_t, B, lse, rw, lbeg, lpair, lr, invB, log2_invB);
   return hipGetLastError();
 }
@@ -653,10 +690,19 @@ hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, const void
     return hipGetLastError();
   }
   if (mode == BWD_CHUNKED)
-    return launch_bwd<true, BWD_CHUNKED>(grid, shm, st, W2, b2, L, H1, H1T, ld_t, B, lse, rw, lbeg,
-                                         lpair, lr, invB);
-  return launch_bwd<false, BWD_GLOBAL>(grid, shm, st, W2, b2, L, H1, H1T, ld_t, B, lse, rw, lbeg,
-                                       lpair, lr, invB);
+    return launch_bwd<true, BWD_CHUNKED, 1>(grid, shm, st, W2, b2, L, H1, H1T, ld_t, B, lse, rw, lbeg,
+                                            lpair, lr, invB);
+  // fp32 operands with few label blocks: 4 wavefronts share a block's rows
+  // (every wave would otherwise own a block and most of the GPU would idle)
+  constexpr int RS = 4;
+  if (n_blocks < n_cu * BWD_WAVES / RS && B <= 512) {
+    const int units = (n_blocks + BWD_WAVES / RS - 1) / (BWD_WAVES / RS);
+    const size_t shr = shm + (size_t)(BWD_WAVES / RS) * (RS - 1) * 65 * 64 * sizeof(float);
+    return launch_bwd<false, BWD_GLOBAL, RS>(units < 2 * n_cu ? units : 2 * n_cu, shr, st, W2, b2, L, H1, H1T,
+                                             ld_t, B, lse, rw, lbeg, lpair, lr, invB);
+  }
+  return launch_bwd<false, BWD_GLOBAL, 1>(grid, shm, st, W2, b2, L, H1, H1T, ld_t, B, lse, rw, lbeg,
+                                          lpair, lr, invB);
 }
 
 }  // namespace asgd
