@@ -222,6 +222,45 @@ def test_step_parity_with_rows_split_over_gather_workgroups(rows, bf16):
         s.free()
 
 
+def test_split_gather_with_empty_and_very_long_rows():
+    """A long-row batch (so the gather splits rows) whose rows are empty, one
+    entry, 4,000 entries and lengths that do not divide evenly over the 32
+    wavefronts of a split row: A1 within its bound, the step within the bar."""
+    import torch
+    flush("step: split gather, empty and very long rows")
+    w = LONG_ROWS
+    rng = np.random.default_rng(11)
+    lens = [0, 1, 4000, 37, 0, 1001, 2, 333]
+    ip, ind, val = [0], [], []
+    for n in lens:
+        f = np.sort(rng.choice(w.n_features, n, replace=False)).astype(np.int32)
+        ind.append(f)
+        val.append(rng.uniform(0.1, 1.0, n).astype(np.float32))
+        ip.append(ip[-1] + n)
+    x = synth.CSR(np.array(ip), np.concatenate(ind), np.concatenate(val), w.n_features)
+    lab = [np.sort(rng.choice(w.n_labels, 1 + i % 3, replace=False)).astype(np.int32) for i in range(len(lens))]
+    lip = np.concatenate([[0], np.cumsum([len(a) for a in lab])])
+    y = synth.CSR(lip, np.concatenate(lab), None, w.n_labels)
+    assert ip[-1] >= 160 * len(lens)   # the split path runs
+    s = Setup(w, 0, 128, ds=synth.Dataset(w, x, y))
+    try:
+        n = len(lens)
+        a1 = torch.empty((n, 128), dtype=torch.float32, device="cuda")
+        asgd.asgd_debug_forward(s.m, s.xb(0, n), s.yb(0, n), a1_dev=a1)
+        torch.cuda.synchronize()
+        p = s.params()
+        xh, _ = s.host_batch(0, n)
+        ref = om.forward(p, xh, None, "fp32")
+        err = np.abs(a1.cpu().numpy().astype(np.float64) - ref["A1"])
+        assert np.all(err <= a1_bound(p, xh) + 1e-7 * np.abs(ref["A1"]))
+        # empty rows: A1 = b1 exactly
+        for r in (0, 4):
+            assert np.array_equal(a1.cpu().numpy()[r].view(np.uint32), p["b1"].view(np.uint32))
+        _step_parity(s, 0, n, 0.05, RTOL_BF16, "fp32")
+    finally:
+        s.free()
+
+
 # more 32-label blocks than the forward launch's LDS holds counters for: the
 # label grouping then counts in global memory
 MANY_LABELS = synth.Workload("labels-1m", 5_000, 1_000_003, 128, 64, 0.01, True, "lognormal", 4.0,
