@@ -39,16 +39,20 @@ FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 PMC_TRAFFIC = {
     ("wide-label", 256, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="92e509b1d36eb57af587fabb9d00c9a1b8fcb93b17baea6a7311e4daf8e6bf3e",
-        fetch_kib=169676.8, write_kib=337663.1),
+        sha256="a25c9f724507c38ecc11a6c44575b1e6ccd8fecb3f05a14a4b865b6477c3f1cd",
+        fetch_kib=169679.2, write_kib=337663.1),
     ("wide-label", 1024, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="92e509b1d36eb57af587fabb9d00c9a1b8fcb93b17baea6a7311e4daf8e6bf3e",
-        fetch_kib=176716.9, write_kib=337973.2),
+        sha256="a25c9f724507c38ecc11a6c44575b1e6ccd8fecb3f05a14a4b865b6477c3f1cd",
+        fetch_kib=176752.4, write_kib=337959.9),
+    ("wide-feature", 128, "out_bwd"): dict(
+        sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
+        sha256="a25c9f724507c38ecc11a6c44575b1e6ccd8fecb3f05a14a4b865b6477c3f1cd",
+        fetch_kib=52209.5, write_kib=103524.0),
     ("elastic", 4, "merge"): dict(
         sources=('csrc/k_merge.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="a75a94295383593e6e13395fadee8cac897bef6c0b77484b8ce27ca18d48b422",
-        fetch_kib=1216909.2, write_kib=2028091.2),
+        sha256="b2b750be029d7b80184de7036e50504ab4cf5704d5abd74ebe84938ee61d420a",
+        fetch_kib=1216908.9, write_kib=2028091.2),
 }
 
 
