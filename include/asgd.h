@@ -386,9 +386,11 @@ enum {
   ASGD_K_GATHER = 0,      /* first-layer gather + sort keys */
   ASGD_K_SORT = 1,        /* radix sort of the batch's feature ids (internal stream) */
   ASGD_K_OUT_FWD = 2,     /* output-layer forward over all labels */
-  ASGD_K_OUT_COMBINE = 3, /* per-row merge of the label splits: lse, loss, target terms */
-  ASGD_K_HIDDEN = 4,      /* per-row dA1 from the forward's partials (internal stream,
-                             beside the backward) */
+  ASGD_K_OUT_COMBINE = 3, /* per-row merge of the label splits: lse, loss, target terms (and
+                             dA1 too, in the same launch, when the step forms dA1 on the
+                             model's stream: the wide-label-dominated pipelined step does not) */
+  ASGD_K_HIDDEN = 4,      /* per-row dA1 from the forward's partials, when it runs on the
+                             internal stream beside the backward */
   ASGD_K_OUT_BWD = 5,     /* output-layer backward + W2/b2 update */
   ASGD_K_W1_UPDATE = 6,   /* sparse W1 gradient + update, b1 update, mean loss (internal stream) */
   ASGD_K_MERGE = 7,       /* normalized merge (timed on the global model) */

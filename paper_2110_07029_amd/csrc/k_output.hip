@@ -9,8 +9,10 @@
 // dense part of dH1 = (P - T) W2 / B, so the backward never needs a second
 // pass over W2 for dH1.  Rows are the N dimension of both products, so all
 // per-row state (running max, rescale factor) is per lane.
-// Combine (k_out_combine): merges the splits of a row (log-sum-exp, loss,
-// dH1 = (O/s - mean_{y in Y_i} W2[y]) / B, dA1 = dH1 * [A1 > 0]).
+// Per row, after the forward: k_out_lse_targets merges the splits' (max, sum)
+// pairs (log-sum-exp) and forms the target terms and the loss; k_out_dA1
+// merges the splits' O (dH1 = (O/s - mean_{y in Y_i} W2[y]) / B,
+// dA1 = dH1 * [A1 > 0]); one launch does both when they share a stream.
 // The backward with the W2 / b2 update is in k_out_bwd.hip.
 #include <float.h>
 #include <math.h>
