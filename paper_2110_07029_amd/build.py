@@ -36,9 +36,18 @@ def sources() -> list:
                   glob.glob(os.path.join(PKG, "csrc", "*.cpp")))
 
 
+# Per-source options.  k_out_bwd.hip: matrix instructions write their results to
+# ordinary vector registers, so that the exponentials read the recomputed logits and
+# the W2 update reads dW2 without first copying them out of accumulation registers
+# (a kernel with the whole register file would otherwise get the accumulation form;
+# the operands pinned to accumulation registers stay there).
+FILE_FLAGS = {"k_out_bwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _compile(src: str, extra: list, verbose: bool) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [hipcc()] + COMMON + DEVICE_FLAGS + extra + ["-c", src, "-o", obj]
+    cmd = ([hipcc()] + COMMON + DEVICE_FLAGS + FILE_FLAGS.get(os.path.basename(src), []) + extra +
+           ["-c", src, "-o", obj])
     r = subprocess.run(cmd, capture_output=True, text=True)
     noise = "is not a recognized feature for this target"
     err = "\n".join(l for l in r.stderr.splitlines() if noise not in l)

@@ -435,10 +435,10 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
   // load or store k covers rows 2k and 2k+1, 16 bytes per lane, so every
   // instruction reads or writes two full 512-byte rows.  The operand layout of
   // the products (lane (g, n): row n, hidden 32kb + 8q + 4g + 0..3) is read
-  // from and written to the tile.  W2 and b2 are raw buffers: the block's
-  // offset is a scalar, the lane's a fixed vector offset plus a constant per
-  // row pair; rows past L read zeros and their stores are dropped by the
-  // buffer's bounds check.  Also loaded: the block's bias (lane n: label
+  // from and written to the tile.  W2 and b2 are raw buffers addressed by the
+  // lane's offset alone (the block's offset plus the lane's fixed offset plus
+  // a constant per row pair), which the buffer's bounds check covers: rows
+  // past L read zeros and their stores are dropped.  Also loaded: the block's bias (lane n: label
   // 32 blk + n) and pair range.
   const int crow_l = lane >> 5, ccol = 4 * (lane & 31);  // this lane's row pair slot and column
   const __amdgpu_buffer_rsrc_t w2r = __builtin_amdgcn_make_buffer_rsrc(W2, (short)0, L * HID * 4, BUF_RSRC_WORD3);
@@ -446,30 +446,54 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
   const int voff = (crow_l * HID + ccol) * 4;
   float4 nv[16];
   float nbias;
-  int nlo, nhi;
-  auto load_blk = [&](int b) {
-    b = min(b, n_blocks - 1);
+  int npr;       // the block's pair lo + lane (-1: none)
+  int nlo, nhi;  // its pair range [nlo, nhi), read one block earlier
+  auto load_blk = [&](int b, int plo, int phi) {
+    const int vb = voff + b * 32 * HID * 4;
 #pragma unroll
     for (int k = 0; k < 16; ++k)
-      nv[k] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(w2r, voff + k * 2 * HID * 4,
-                                                                                 b * 32 * HID * 4, 0));
-    nbias = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(b2r, n * 4, b * 32 * 4, 0));
-    nlo = lbeg[b];
-    nhi = lbeg[b + 1];
+      nv[k] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(w2r, vb + k * 2 * HID * 4, 0, 0));
+    nbias = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(b2r, n * 4 + b * 32 * 4, 0, 0));
+    npr = plo + lane < phi ? lpair[plo + lane] : -1;
+    nlo = plo;
+    nhi = phi;
   };
   auto stage_frag = [&](int kb, int q) -> float4& {
     return *reinterpret_cast<float4*>(stage + n * BWP_SLD + 32 * kb + 8 * q + 4 * g);
   };
 
-  const int first = blockIdx.x * BWP_WAVES + wave;
-  load_blk(first);
-  for (int blk = first; blk < n_blocks; blk += step) {
+  // The loaded block enters the staging tile right after the previous block's
+  // stores, and the block after it is requested at once: every iteration then
+  // issues the same memory instructions in the same order (the next block's
+  // 17 loads, this block's 16 row stores and one b2 store), so the wait for a
+  // block's loads never includes the stores issued after them.
+  // (The bias and the first 64 pairs wait in the tile's pad columns HID and
+  // HID + 1 + g of row n: a register copy of a loaded value would make the
+  // compiler wait for the load right away.)  The pair range of a block is read
+  // one block before its loads are issued, so that the pair load need not wait.
+  int lo, hi;
+  auto stage_loaded = [&]() {
 #pragma unroll
     for (int k = 0; k < 16; ++k) *reinterpret_cast<float4*>(stage + (2 * k + crow_l) * BWP_SLD + ccol) = nv[k];
-    const float bias = nbias;
-    const int lo = nlo, hi = nhi;
+    if (g == 0) stage[n * BWP_SLD + HID] = nbias;
+    stage[n * BWP_SLD + HID + 1 + g] = __builtin_bit_cast(float, npr);
+    lo = nlo;
+    hi = nhi;
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    load_blk(blk + step);  // the next block's rows load during this one
+  };
+  const int first = blockIdx.x * BWP_WAVES + wave;
+  if (first >= n_blocks) return;
+  load_blk(first, lbeg[first], lbeg[first + 1]);
+  stage_loaded();
+  {
+    const int b = min(first + step, n_blocks - 1);
+    load_blk(b, lbeg[b], lbeg[b + 1]);
+  }
+  for (int blk = first; blk < n_blocks; blk += step) {
+    const int bn2 = min(blk + 2 * step, n_blocks - 1);  // the block loaded at the end of this one
+    const int plo = lbeg[bn2], phi = lbeg[bn2 + 1];
+    const float bias = stage[n * BWP_SLD + HID];
+    const int pr0 = __builtin_bit_cast(int, stage[n * BWP_SLD + HID + 1 + g]);
     const int label = blk * 32 + n;
     const bool lvalid = label < L;
     const float bb = lvalid ? bias * LOG2E : -INFINITY;
@@ -498,11 +522,12 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
     if (has_targets) {
       for (int k = lane; k < 32 * nrb; k += 64) mask[k] = 0u;
       __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-      for (int q = lo + lane; q < hi; q += 64) {
-        const int pr = lpair[q];
+      auto put = [&](int pr) {
         const int row = pr >> 5;
         atomicOr(&mask[(pr & 31) * nrb + (row >> 5)], 1u << (row & 31));
-      }
+      };
+      if (pr0 >= 0) put(pr0);
+      for (int q = lo + 64 + lane; q < hi; q += 64) put(lpair[q]);
       __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     }
     f32x16 accw[4];
@@ -541,13 +566,15 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
           for (int c = 0; c < 2; ++c) z = M::mma(hr[kb][c], wf[kb][c], z);
         return z;
       };
-      f32x16 z;
+      // the logits of two row blocks alternate between za and zb (no copies)
+      f32x16 za, zb;
       {
         bf16x8 hr[4][2];
-        read_rows(0, hr, z);
-        z = logits(hr, z);
+        read_rows(0, hr, za);
+        za = logits(hr, za);
       }
-      for (int rb = 0; rb < nrb; ++rb) {
+      // row block rb from z (its logits); the logits of rb + 1 into zn
+      auto step = [&](int rb, const f32x16& z, f32x16& zn) {
         // (A)
         bf16x8 at[4][2];
 #pragma unroll
@@ -563,7 +590,6 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
           }
         // next row block (the last iteration recomputes a block and drops it)
         bf16x8 hr[4][2];
-        f32x16 zn;
         read_rows(min(rb + 1, nrb - 1), hr, zn);
         uint32_t mw = 0;
         float tv[16];
@@ -599,7 +625,10 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
         for (int hb = 0; hb < 4; ++hb)
 #pragma unroll
           for (int c = 0; c < 2; ++c) accw[hb] = M::mma(at[hb][c], df[c], accw[hb]);
-        z = zn;
+      };
+      for (int rb = 0; rb < nrb; rb += 2) {
+        step(rb, za, zb);
+        if (rb + 1 < nrb) step(rb + 1, zb, za);
       }
     };
     if (has_targets)
@@ -626,11 +655,18 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
       const float4 o = *reinterpret_cast<const float4*>(stage + (2 * k + crow_l) * BWP_SLD + ccol);
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o), w2r, voff + k * 2 * HID * 4,
-                                             blk * 32 * HID * 4, 0);
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o), w2r,
+                                             voff + blk * 32 * HID * 4 + k * 2 * HID * 4, 0, 0);
     }
-    if (lvalid && g == 0) b2[label] = fmaf(-lr, db2, bias);
+    // b2 from every lane, unconditionally (the lanes of half g = 1 and labels
+    // past L fall outside the buffer and are dropped)
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fmaf(-lr, db2, bias)), b2r,
+                                          (g == 0 ? n * 4 : L * 4) + blk * 32 * 4, 0, 0);
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    if (blk + step < n_blocks) {
+      stage_loaded();
+      load_blk(bn2, plo, phi);
+    }
   }
 }
 

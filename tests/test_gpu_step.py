@@ -278,6 +278,34 @@ def test_step_parity_with_label_counters_in_global_memory():
         s.free()
 
 
+# 40 labels: two label blocks (the second holds 8), each with hundreds of a
+# batch's (row, label) pairs
+FEW_LABELS = synth.Workload("labels-40", 5_000, 40, 600, 256, 0.01, True, "lognormal", 4.0,
+                            0.8, 2_000, 1.05, "uniform", "poisson", 4.0, None, 2)
+
+
+@pytest.mark.parametrize("rows", [(0, 256), (256, 455)])
+def test_step_parity_with_dense_label_blocks(rows):
+    """Every label block holds far more than 64 of the batch's (row, label)
+    pairs, so the backward reads a block's pairs past the first 64 from memory
+    (the first 64 arrive with the block's weights)."""
+    flush(f"step: 40 labels, rows {rows}")
+    s = Setup(FEW_LABELS, 600, 256)
+    try:
+        xh, yh = s.host_batch(*rows)
+        lab = np.asarray(yh.indices[int(yh.indptr[0]):int(yh.indptr[-1])])
+        assert np.bincount(lab // 32, minlength=2).min() > 64
+        before, after, _ = _step_parity(s, rows[0], rows[1], 0.05, RTOL_BF16, "fp32")
+        ref_emu, _, g, fw = om.train_step(before, xh, yh, 0.05, "bf16")
+        mag = step_magnitudes(before, xh, yh, g, fw, 0.05)
+        assert_update_close("W2(bf16 operands)", before["W2"], after["W2"], ref_emu["W2"], RTOL_EMU_ELEM,
+                            mag["W2"], norm_rtol=RTOL_EMU_NORM)
+        assert_update_close("b2(bf16 operands)", before["b2"], after["b2"], ref_emu["b2"], RTOL_EMU_ELEM,
+                            mag["b2"], norm_rtol=RTOL_EMU_NORM)
+    finally:
+        s.free()
+
+
 def test_step_parity_when_the_running_maximum_rises():
     """Biases rising by 6 per 32-label tile: on every tile of a split the row
     maximum exceeds the forward's running reference by more than its lazy
