@@ -156,7 +156,7 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
   // is a per-row reference that is raised only when a tile's maximum exceeds it
   // by more than LAZY (so p <= 2^LAZY); the final normalisation uses the same
   // reference, so the result is exact up to rounding.
-  constexpr float LAZY = 8.0f;
+  constexpr float LAZY = 8.0f, LAZY_SUM = 256.0f;  // LAZY_SUM = 2^LAZY
   auto iteration = [&](int t, TileRegs& tr) {
     const int b0 = slot(t), b1 = slot(t + 1), bst = slot(t + P + 1);
     // Operands of this iteration's two products, read from LDS first so that
@@ -189,29 +189,33 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
         for (int c = 0; c < NCH; ++c) oa[hb][c] = tile_frag_wt<BF16>(wr[b0], wt[b0], cbase, hb, c, lane);
     }
 
-    // The next tile's logits go to the matrix cores first; this tile's maximum
-    // and numerators are formed on the vector units while they run.  The
-    // numerators are taken against the current reference before the maximum
-    // is known (the empty asm keeps them ahead of the branch), and formed again
-    // in the rare iteration that raises the reference, so every p that is used
-    // is computed against the reference the row ends with at that point.
+    // The next tile's logits go to the matrix cores first; this tile's
+    // numerators are formed on the vector units while they run, against the
+    // current reference, and formed again in the rare iteration that raises
+    // it, so every p that is used is computed against the reference the row
+    // ends with at that point.
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
       for (int c = 0; c < NCH; ++c)
         zn = M::mma(BF16 ? za[kb][c % PRE] : tile_frag_w<BF16>(wr[b1], rbase, n, kb, c, g), hf[kb][c], zn);
-    // running maximum of this tile (rows are lanes: one max per lane pair)
-    float tmax = z[0];
-#pragma unroll
-    for (int r = 1; r < 16; ++r) tmax = fmaxf(tmax, z[r]);
-    tmax = half_swap_max(tmax);
-    const float m2c = tmax * LOG2E;
+    // The tile's maximum is only formed when some lane's numerators sum past
+    // 2^LAZY (or are not finite, as on a row's first tile, whose reference is
+    // -inf): no numerator exceeds its lane's sum, so every other tile keeps
+    // p <= 2^LAZY against the current reference.
     float p[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, -m_run));
+    float ps = 0.0f;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) asm volatile("" : "+v"(p[r]));
-    if (__any(m2c > m_run + LAZY)) {
+    for (int r = 0; r < 16; ++r) ps += p[r];
+    if (__any(!(ps <= LAZY_SUM))) {
+      // running maximum of this tile (rows are lanes: one max per lane pair)
+      float tmax = z[0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) tmax = fmaxf(tmax, z[r]);
+      tmax = half_swap_max(tmax);
+      const float m2c = tmax * LOG2E;
       const float m2n = m2c > m_run + LAZY ? m2c : m_run;
       const float scale = __builtin_amdgcn_exp2f(m_run - m2n);
       s_run *= scale;
@@ -220,12 +224,13 @@ __global__ __launch_bounds__(FWD_THREADS) void k_out_fwd_train(
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc_o[hb][r] *= scale;
       m_run = m2n;
+      ps = 0.0f;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, -m_run));
+      for (int r = 0; r < 16; ++r) {
+        p[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, -m_run));
+        ps += p[r];
+      }
     }
-    float ps = 0.0f;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) ps += p[r];
     s_run += ps;
     Fr pf[NCH];
 #pragma unroll
