@@ -46,7 +46,7 @@ hipError_t launch_fill_int(int32_t* p, int32_t v, int64_t n, hipStream_t st) {
 
 // ---------------------------------------------------------------------------
 // A1[i] = b1 + sum_{(f, v) in row i} v * W1[f];  H1 = max(A1, 0).
-// One workgroup (8 wavefronts) per sample row; for batches whose rows average
+// One workgroup (4 wavefronts) per sample row; for batches whose rows average
 // GATHER_LONG_ROW entries or more, GATHER_SPLIT workgroups per row, each
 // writing its partial sum, and a second launch adds them (the step time
 // follows the longest row, which then spreads over several CUs).  Lane l owns
@@ -59,7 +59,10 @@ hipError_t launch_fill_int(int32_t* p, int32_t v, int64_t n, hipStream_t st) {
 // row of the batch, and nnz per row is heavy-tailed).  The partial sums are
 // added in wavefront order (then in workgroup order), then b1.
 // ---------------------------------------------------------------------------
-constexpr int GATHER_WAVES = 8;
+// Four wavefronts (one per SIMD): the workgroup can start on a CU where the
+// output-layer backward leaves room for only one more wavefront per SIMD,
+// which is where the next step's gather runs.
+constexpr int GATHER_WAVES = 4;
 constexpr int GATHER_UNROLL = 16;
 static_assert(64 % GATHER_UNROLL == 0, "readlane indices stay below 64");
 

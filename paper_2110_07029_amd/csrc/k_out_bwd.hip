@@ -539,11 +539,14 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
 
     // The row-block loop, specialised on whether the block has true labels in
     // this batch (most blocks of a wide label space have none), so that its
-    // body is straight-line code in three phases: (A) every LDS read of the
-    // iteration (H1^T fragments of row block rb, H1 rows and row constants of
-    // rb+1), (B) the logits of rb+1 on the matrix cores beside the
-    // exponentials of rb, (C) dZ of rb into dW2.  The scheduling barriers keep
-    // the reads ahead of the arithmetic that hides their latency.
+    // body is straight-line code.  Step rb has two phases: (A) every LDS read
+    // of the step (H1^T fragments of row block rb, H1 rows and row constants of
+    // rb+1), then (B) the matrix work of two row blocks, the logits of rb+1 and
+    // the dW2 products of rb-1, beside the vector work of rb (exponentials,
+    // target terms, db2, the bf16 dZ operands).  A row block's dW2 products thus
+    // wait one step for their operands and never stand alone at the end of a
+    // step.  The scheduling barriers keep the reads ahead of the arithmetic
+    // that hides their latency.
     auto rows = [&](auto targets) {
       constexpr bool TGT = decltype(targets)::value;
       auto read_rows = [&](int rb, bf16x8 (&hr)[4][2], f32x16& c) {
@@ -566,17 +569,27 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
           for (int c = 0; c < 2; ++c) z = M::mma(hr[kb][c], wf[kb][c], z);
         return z;
       };
-      // the logits of two row blocks alternate between za and zb (no copies)
+      auto dw2 = [&](const bf16x8 (&at)[4][2], const Fr (&df)[2]) {
+#pragma unroll
+        for (int hb = 0; hb < 4; ++hb)
+#pragma unroll
+          for (int c = 0; c < 2; ++c) accw[hb] = M::mma(at[hb][c], df[c], accw[hb]);
+      };
+      // Two sets of per-row-block state alternate (no copies): the logits, the
+      // H1^T fragments and the bf16 dZ of a row block.
       f32x16 za, zb;
+      bf16x8 ata[4][2], atb[4][2];
+      Fr dfa[2], dfb[2];
       {
         bf16x8 hr[4][2];
         read_rows(0, hr, za);
         za = logits(hr, za);
       }
-      // row block rb from z (its logits); the logits of rb + 1 into zn
-      auto step = [&](int rb, const f32x16& z, f32x16& zn) {
+      // row block rb from z (its logits) into (at, df); the logits of rb + 1
+      // into zn; the dW2 products of rb - 1 from (atp, dfp) when PREV
+      auto step = [&](auto prev, int rb, const f32x16& z, f32x16& zn, bf16x8 (&at)[4][2], Fr (&df)[2],
+                      const bf16x8 (&atp)[4][2], const Fr (&dfp)[2]) {
         // (A)
-        bf16x8 at[4][2];
 #pragma unroll
         for (int hb = 0; hb < 4; ++hb)
 #pragma unroll
@@ -588,7 +601,7 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
             af[4] = hi4[0]; af[5] = hi4[1]; af[6] = hi4[2]; af[7] = hi4[3];
             at[hb][c] = af;
           }
-        // next row block (the last iteration recomputes a block and drops it)
+        // next row block (the last step recomputes a block and drops it)
         bf16x8 hr[4][2];
         read_rows(min(rb + 1, nrb - 1), hr, zn);
         uint32_t mw = 0;
@@ -602,33 +615,43 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
           }
         }
         __builtin_amdgcn_sched_barrier(0);
-        // (B)
-        zn = logits(hr, zn);
+        // (B), in eight groups fenced by scheduling barriers: group i issues
+        // logits product i of rb+1 and dW2 product i of rb-1 (independent
+        // accumulators, so they alternate on the matrix core without a stall),
+        // then numerators 2i and 2i+1 of rb, and every fourth group packs 8 of
+        // them into the bf16 operand of rb's own dW2 products.
         float dz[16];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) dz[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, bb));
-        __builtin_amdgcn_sched_barrier(0);
-        // (C)
-        if constexpr (TGT) {
+        for (int i = 0; i < 8; ++i) {
+          zn = M::mma(hr[i >> 1][i & 1], wf[i >> 1][i & 1], zn);
+          if constexpr (decltype(prev)::value)
+            accw[i >> 1] = M::mma(atp[i >> 1][i & 1], dfp[i & 1], accw[i >> 1]);
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int rl = 8 * (r >> 2) + 4 * g + (r & 3);
-            dz[r] -= ((mw >> rl) & 1u) ? tv[r] : 0.0f;
+          for (int j = 0; j < 2; ++j) {
+            const int r = 2 * i + j;
+            dz[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, bb));
+            if constexpr (TGT) {
+              const int rl = 8 * (r >> 2) + 4 * g + (r & 3);
+              dz[r] -= ((mw >> rl) & 1u) ? tv[r] : 0.0f;
+            }
+            db2p += dz[r];
           }
+          if ((i & 3) == 3) df[i >> 2] = frag_acc<true>(dz, i >> 2);
+          __builtin_amdgcn_sched_barrier(0);
         }
-#pragma unroll
-        for (int r = 0; r < 16; ++r) db2p += dz[r];
-        Fr df[2];
-#pragma unroll
-        for (int c = 0; c < 2; ++c) df[c] = frag_acc<true>(dz, c);
-#pragma unroll
-        for (int hb = 0; hb < 4; ++hb)
-#pragma unroll
-          for (int c = 0; c < 2; ++c) accw[hb] = M::mma(at[hb][c], df[c], accw[hb]);
       };
-      for (int rb = 0; rb < nrb; rb += 2) {
-        step(rb, za, zb);
-        if (rb + 1 < nrb) step(rb + 1, zb, za);
+      // row blocks: 0 alone, then pairs (odd rb in set b, even in set a), then
+      // the last one alone when nrb is even; its products follow
+      step(std::false_type{}, 0, za, zb, ata, dfa, atb, dfb);
+      for (int rb = 1; rb + 1 < nrb; rb += 2) {
+        step(std::true_type{}, rb, zb, za, atb, dfb, ata, dfa);
+        step(std::true_type{}, rb + 1, za, zb, ata, dfa, atb, dfb);
+      }
+      if (nrb & 1) {
+        dw2(ata, dfa);
+      } else {
+        step(std::true_type{}, nrb - 1, zb, za, atb, dfb, ata, dfa);
+        dw2(atb, dfb);
       }
     };
     if (has_targets)
