@@ -39,16 +39,16 @@ FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 PMC_TRAFFIC = {
     ("wide-label", 256, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="a25c9f724507c38ecc11a6c44575b1e6ccd8fecb3f05a14a4b865b6477c3f1cd",
-        fetch_kib=169679.2, write_kib=337663.1),
+        sha256="4ffa95bf50598de028fdfe1882ee1439715219228b288e5366f1fe1944ff353e",
+        fetch_kib=169816.3, write_kib=337663.1),
     ("wide-label", 1024, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="a25c9f724507c38ecc11a6c44575b1e6ccd8fecb3f05a14a4b865b6477c3f1cd",
-        fetch_kib=176752.4, write_kib=337959.9),
+        sha256="4ffa95bf50598de028fdfe1882ee1439715219228b288e5366f1fe1944ff353e",
+        fetch_kib=176680.8, write_kib=337960.3),
     ("wide-feature", 128, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="a25c9f724507c38ecc11a6c44575b1e6ccd8fecb3f05a14a4b865b6477c3f1cd",
-        fetch_kib=52209.5, write_kib=103524.0),
+        sha256="4ffa95bf50598de028fdfe1882ee1439715219228b288e5366f1fe1944ff353e",
+        fetch_kib=52254.0, write_kib=103524.0),
     ("elastic", 4, "merge"): dict(
         sources=('csrc/k_merge.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
         sha256="b2b750be029d7b80184de7036e50504ab4cf5704d5abd74ebe84938ee61d420a",

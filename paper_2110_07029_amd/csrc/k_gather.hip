@@ -46,7 +46,7 @@ hipError_t launch_fill_int(int32_t* p, int32_t v, int64_t n, hipStream_t st) {
 
 // ---------------------------------------------------------------------------
 // A1[i] = b1 + sum_{(f, v) in row i} v * W1[f];  H1 = max(A1, 0).
-// One workgroup (4 wavefronts) per sample row; for batches whose rows average
+// One workgroup per sample row; for batches whose rows average
 // GATHER_LONG_ROW entries or more, GATHER_SPLIT workgroups per row, each
 // writing its partial sum, and a second launch adds them (the step time
 // follows the longest row, which then spreads over several CUs).  Lane l owns
@@ -59,15 +59,17 @@ hipError_t launch_fill_int(int32_t* p, int32_t v, int64_t n, hipStream_t st) {
 // row of the batch, and nnz per row is heavy-tailed).  The partial sums are
 // added in wavefront order (then in workgroup order), then b1.
 // ---------------------------------------------------------------------------
-// Four wavefronts (one per SIMD): the workgroup can start on a CU where the
-// output-layer backward leaves room for only one more wavefront per SIMD,
-// which is where the next step's gather runs.
-constexpr int GATHER_WAVES = 4;
+// Short rows: four wavefronts (one per SIMD), so that the workgroup can start
+// on a CU where the output-layer backward leaves room for only one more
+// wavefront per SIMD, which is where the next step's gather runs when the
+// step is pipelined.  Long rows (split over workgroups; the gather then runs
+// alone on the model's stream): eight.
+constexpr int gather_waves(int split) { return split > 1 ? 8 : 4; }
 constexpr int GATHER_UNROLL = 16;
 static_assert(64 % GATHER_UNROLL == 0, "readlane indices stay below 64");
 
 template <bool BF16, int SPLIT>
-__global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
+__global__ __launch_bounds__(64 * gather_waves(SPLIT)) void k_gather_fwd(
     CsrDev x, CsrDev y, int has_y, const float* __restrict__ W1, const float* __restrict__ b1,
     int F, int L, float* __restrict__ A1, typename Mma<BF16>::elem* __restrict__ H1,
     typename Mma<BF16>::elem* __restrict__ H1T, int rows_pad, int ld_t, int32_t* __restrict__ keys,
@@ -75,7 +77,7 @@ __global__ __launch_bounds__(64 * GATHER_WAVES) void k_gather_fwd(
     float* __restrict__ rw,
     int32_t* __restrict__ err, int validate, float* __restrict__ gpart) {
   using E = typename Mma<BF16>::elem;
-  constexpr int WAVES = GATHER_WAVES;
+  constexpr int WAVES = gather_waves(SPLIT);
   __shared__ float2 part[WAVES][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i = (int)blockIdx.x / SPLIT, piece = (int)blockIdx.x % SPLIT;
@@ -235,8 +237,8 @@ hipError_t launch_gather_fwd(bool use_bf16, const CsrDev& x, const CsrDev* y, co
                              float* gpart, hipStream_t st) {
   CsrDev yy = y ? *y : CsrDev{0, 0, 0, nullptr, nullptr, nullptr};
   const bool split = gpart && x.n_rows > 0 && (int64_t)x.nnz >= (int64_t)GATHER_LONG_ROW * x.n_rows;
-  const dim3 block(64 * GATHER_WAVES);
   auto go = [&](auto kern, int pieces, auto* h1, auto* h1t) {
+    const dim3 block(64 * gather_waves(pieces));
     hipLaunchKernelGGL(kern, dim3(rows_pad * pieces), block, 0, st, x, yy, y != nullptr, W1, b1, F, L, A1, h1,
                        h1t, rows_pad, ld_t, keys, row_of, lkeys, lrow, rw, err, validate, gpart);
   };

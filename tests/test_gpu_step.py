@@ -224,7 +224,7 @@ def test_step_parity_with_rows_split_over_gather_workgroups(rows, bf16):
 
 def test_split_gather_with_empty_and_very_long_rows():
     """A long-row batch (so the gather splits rows) whose rows are empty, one
-    entry, 4,000 entries and lengths that do not divide evenly over the 16
+    entry, 4,000 entries and lengths that do not divide evenly over the 32
     wavefronts of a split row: A1 within its bound, the step within the bar."""
     import torch
     flush("step: split gather, empty and very long rows")
