@@ -146,7 +146,7 @@ def test_step_parity_fp32(rows):
 
 
 @pytest.mark.parametrize("rows,B", [((0, 256), 256), ((256, 389), 256), ((0, 600), 600),
-                                    ((3, 4), 256)])
+                                    ((3, 4), 256), ((0, 128), 256), ((100, 197), 256)])
 def test_step_parity_bf16(rows, B):
     flush(f"step bf16 mid-small rows {rows} max_batch {B}")
     s = Setup(SMALL_MID, 1024, B)
@@ -284,11 +284,12 @@ FEW_LABELS = synth.Workload("labels-40", 5_000, 40, 600, 256, 0.01, True, "logno
                             0.8, 2_000, 1.05, "uniform", "poisson", 4.0, None, 2)
 
 
-@pytest.mark.parametrize("rows", [(0, 256), (256, 455)])
+@pytest.mark.parametrize("rows", [(0, 256), (256, 455), (455, 555)])
 def test_step_parity_with_dense_label_blocks(rows):
     """Every label block holds far more than 64 of the batch's (row, label)
     pairs, so the backward reads a block's pairs past the first 64 from memory
-    (the first 64 arrive with the block's weights)."""
+    (the first 64 arrive with the block's weights); 40 labels are two tiles,
+    so each of the forward's two splits holds one."""
     flush(f"step: 40 labels, rows {rows}")
     s = Setup(FEW_LABELS, 600, 256)
     try:
