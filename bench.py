@@ -571,14 +571,24 @@ def main():
         kernels["gather_saturating"] = measure_gather_saturating(w, stream)
     d = kernels[dom]
     traffic = measured_traffic(w.name, B, dom)
-    roofline = {"kernel": dom, "bound": "hbm", "achieved": d["GB/s"], "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": d["hbm_frac"],
-                "traffic": None if traffic is None else round(traffic / 1e9, 4)}
+    # the dominant kernel against the resource it uses the larger share of: HBM
+    # (algorithmic bytes) or the matrix cores (algorithmic flops, at the dtype's peak)
+    mfma_bound = d["mfma_frac"] > d["hbm_frac"]
+    if mfma_bound:
+        roofline = {"kernel": dom, "bound": "mfma", "achieved": d["TFLOP/s"], "peak": MFMA_PEAK_TFLOPS[dtype],
+                    "unit": "TFLOP/s", "frac": d["mfma_frac"]}
+    else:
+        roofline = {"kernel": dom, "bound": "hbm", "achieved": d["GB/s"], "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": d["hbm_frac"]}
+    roofline["traffic"] = None if traffic is None else round(traffic / 1e9, 4)
     if traffic is not None:
         roofline["traffic_unit"] = "GB per launch"
     meas = measured_peaks(w.n_labels * H, stream)
     roofline["measured_peaks"] = meas
-    roofline["frac_of_measured"] = round(d["GB/s"] / meas["hbm_inplace_update_GBs"], 4)
+    # (the measured matrix-core rate is a bf16 GEMM's: no figure for fp32 operands)
+    roofline["frac_of_measured"] = (None if mfma_bound and dtype != "bf16" else
+                                    round(d["TFLOP/s"] / meas["bf16_gemm_TFLOPs"] if mfma_bound
+                                          else d["GB/s"] / meas["hbm_inplace_update_GBs"], 4))
     cpu = None
     if args.cpu_seconds > 0:
         log(f"oracle CPU baseline, ~{args.cpu_seconds:.0f} s budget")
