@@ -39,16 +39,16 @@ FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 PMC_TRAFFIC = {
     ("wide-label", 256, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="4ffa95bf50598de028fdfe1882ee1439715219228b288e5366f1fe1944ff353e",
-        fetch_kib=169816.3, write_kib=337663.1),
+        sha256="e5613706b808523bc873203ff6f811a45dce329b9c7ab8f522214b256d0cbe8c",
+        fetch_kib=169815.7, write_kib=337663.1),
     ("wide-label", 1024, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="4ffa95bf50598de028fdfe1882ee1439715219228b288e5366f1fe1944ff353e",
-        fetch_kib=176680.8, write_kib=337960.3),
+        sha256="e5613706b808523bc873203ff6f811a45dce329b9c7ab8f522214b256d0cbe8c",
+        fetch_kib=176752.0, write_kib=337964.9),
     ("wide-feature", 128, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="4ffa95bf50598de028fdfe1882ee1439715219228b288e5366f1fe1944ff353e",
-        fetch_kib=52254.0, write_kib=103524.0),
+        sha256="e5613706b808523bc873203ff6f811a45dce329b9c7ab8f522214b256d0cbe8c",
+        fetch_kib=52256.8, write_kib=103524.0),
     ("elastic", 4, "merge"): dict(
         sources=('csrc/k_merge.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
         sha256="b2b750be029d7b80184de7036e50504ab4cf5704d5abd74ebe84938ee61d420a",

@@ -379,10 +379,11 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
 // 4 wavefronts, one per SIMD, each with the full register file.  While a wave
 // works on one block of 32 labels, the next block's fp32 rows load into
 // registers as whole 512-byte rows (the access pattern of a plain streaming
-// update); at the block's start they go through the wave's LDS staging tile,
-// from which the products' operand layout is read, and the updated rows leave
-// the same way.  Inside a block the logits of row block rb+1 go to the matrix
-// cores while the exponentials of row block rb are formed.
+// update); once this block's updated rows have left through the wave's LDS
+// staging tile, they enter it, and the products' operand layout is read from
+// there.  Inside a block, each step issues the logits of row block rb+1 and
+// the dW2 products of rb-1 to the matrix cores while the exponentials of rb
+// are formed.
 // ---------------------------------------------------------------------------
 constexpr int BWP_WAVES = 4;
 constexpr int BWP_SLD = 132;  // staging tile row stride (floats): conflict-free both ways
