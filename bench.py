@@ -39,20 +39,20 @@ FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 PMC_TRAFFIC = {
     ("wide-label", 256, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="e5613706b808523bc873203ff6f811a45dce329b9c7ab8f522214b256d0cbe8c",
-        fetch_kib=169815.7, write_kib=337663.1),
+        sha256="746408ca1d9a519893b3a6a20d3893dd2088ef9f2c29093fe946c5cff8b9065c",
+        fetch_kib=169817.6, write_kib=337663.1),
     ("wide-label", 1024, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="e5613706b808523bc873203ff6f811a45dce329b9c7ab8f522214b256d0cbe8c",
-        fetch_kib=176752.0, write_kib=337964.9),
+        sha256="746408ca1d9a519893b3a6a20d3893dd2088ef9f2c29093fe946c5cff8b9065c",
+        fetch_kib=176687.1, write_kib=337953.0),
     ("wide-feature", 128, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="e5613706b808523bc873203ff6f811a45dce329b9c7ab8f522214b256d0cbe8c",
-        fetch_kib=52256.8, write_kib=103524.0),
+        sha256="746408ca1d9a519893b3a6a20d3893dd2088ef9f2c29093fe946c5cff8b9065c",
+        fetch_kib=52257.2, write_kib=103524.0),
     ("elastic", 4, "merge"): dict(
         sources=('csrc/k_merge.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="b2b750be029d7b80184de7036e50504ab4cf5704d5abd74ebe84938ee61d420a",
-        fetch_kib=1216908.9, write_kib=2028091.2),
+        sha256="cac912f9fbd11c0a0526c5a58b20552a4362a31425c7d79736900402ea9d3f63",
+        fetch_kib=1216912.2, write_kib=2028091.2),
 }
 
 

@@ -410,12 +410,12 @@ asgd_status run_forward(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int
   TIMED(m, ASGD_K_OUT_COMBINE, launch_out_lse_targets(m->bf16, B, s_eff, m->m_part, m->s_part, rows_pad, m->W2(),
                                                       m->b2(), m->L, m->H1, y ? &yd : nullptr, m->lse,
                                                       m->loss_rows, m->tw, m->o_part, A, fused ? dA : nullptr,
-                                                      m->stream));
+                                                      m->stream, y && !fused && da_stream != m->stream ? m->ev_dA1 : nullptr));
   if (!y || fused) return ASGD_OK;
-  if (da_stream != m->stream) {
-    HIP_TRY(hipEventRecord(m->ev_dA1, m->stream));
-    HIP_TRY(hipStreamWaitEvent(da_stream, m->ev_dA1, 0));
-  }
+  // the event was completed by the lse/targets launch itself: a separate record
+  // would put a marker between lse/targets and the backward on the model's
+  // stream, and a gap of several microseconds with it
+  if (da_stream != m->stream) HIP_TRY(hipStreamWaitEvent(da_stream, m->ev_dA1, 0));
   TIMED_ON(m, ASGD_K_HIDDEN, da_stream, launch_out_dA1(B, s_eff, m->m_part, m->s_part, m->o_part, rows_pad, m->tw,
                                                        A, dA, da_stream == m->stream, da_stream));
   return ASGD_OK;

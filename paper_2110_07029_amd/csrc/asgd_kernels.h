@@ -87,7 +87,9 @@ hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2,
 hipError_t launch_out_lse_targets(bool use_bf16, int B, int splits, const float* m_part, const float* s_part,
                                   int ld_part, const float* W2, const float* b2, int L, const void* H1,
                                   const CsrDev* y, float* lse, float* loss_rows, float* tw, const float* o_part,
-                                  const float* A1, float* dA1, hipStream_t st);
+                                  const float* A1, float* dA1, hipStream_t st, hipEvent_t done = nullptr);
+// (done: an event that the launch itself completes when the kernel has
+// finished, with no marker of its own on the stream)
 // Per row: dA1 = ((O/s - tw) / B) * [A1 > 0] from the forward's partials (reads no W2);
 // wide: twice the threads per row (for a launch that runs alone, not beside the backward).
 hipError_t launch_out_dA1(int B, int splits, const float* m_part, const float* s_part, const float* o_part,

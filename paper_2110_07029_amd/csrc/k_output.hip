@@ -17,6 +17,8 @@
 #include <float.h>
 #include <math.h>
 
+#include <hip/hip_ext.h>
+
 #include "asgd_dev.h"
 #include "asgd_kernels.h"
 #include "aux_dev.h"
@@ -557,13 +559,17 @@ __global__ __launch_bounds__(32 * GROUPS) void k_out_dA1(int splits, const float
 hipError_t launch_out_lse_targets(bool use_bf16, int B, int splits, const float* m_part, const float* s_part,
                                   int ld_part, const float* W2, const float* b2, int L, const void* H1,
                                   const CsrDev* y, float* lse, float* loss_rows, float* tw, const float* o_part,
-                                  const float* A1, float* dA1, hipStream_t st) {
+                                  const float* A1, float* dA1, hipStream_t st, hipEvent_t done) {
   CsrDev yy = y ? *y : CsrDev{0, 0, 0, nullptr, nullptr, nullptr};
   const bool da = y && dA1;
   const float invB = 1.0f / (float)B;
   auto go = [&](auto kern, auto* h1) {
-    hipLaunchKernelGGL(kern, dim3(B), dim3(CMB_THREADS), 0, st, splits, m_part, s_part, ld_part, W2, b2, L, h1, yy,
-                       y != nullptr, lse, loss_rows, tw, o_part, A1, invB, dA1);
+    if (done)
+      hipExtLaunchKernelGGL(kern, dim3(B), dim3(CMB_THREADS), 0, st, nullptr, done, 0, splits, m_part, s_part, ld_part,
+                            W2, b2, L, h1, yy, (int)(y != nullptr), lse, loss_rows, tw, o_part, A1, invB, dA1);
+    else
+      hipLaunchKernelGGL(kern, dim3(B), dim3(CMB_THREADS), 0, st, splits, m_part, s_part, ld_part, W2, b2, L, h1, yy,
+                         y != nullptr, lse, loss_rows, tw, o_part, A1, invB, dA1);
   };
   if (use_bf16) {
     if (da)
