@@ -344,7 +344,9 @@ hipEvent_t timer_start(asgd_model* m, int k, hipStream_t st, hipEvent_t* stop) {
 
 // Gather forward (+ keys) on stream st into the next copy of H1 / H1T / rw,
 // optional validation check.  Leaves H1 / A1 ready.
-asgd_status run_gather(asgd_model* m, const asgd_csr* x, const asgd_csr* y, hipStream_t st, int* rows_pad_out) {
+// done (optional): an event completed once the gather's work has finished on st
+asgd_status run_gather(asgd_model* m, const asgd_csr* x, const asgd_csr* y, hipStream_t st, int* rows_pad_out,
+                       hipEvent_t done = nullptr) {
   const int B = x->n_rows;
   const int RB = out_rows_per_block(m->bf16);
   const int rows_pad = (int)round_up(B, RB);
@@ -359,10 +361,12 @@ asgd_status run_gather(asgd_model* m, const asgd_csr* x, const asgd_csr* y, hipS
   TIMED_ON(m, ASGD_K_GATHER, st, launch_gather_fwd(m->bf16, xd, y ? &yd : nullptr, m->W1(), m->b1(), m->F, m->L,
                                                    m->A1, m->H1, m->H1T, rows_pad, m->rows_pad_max, m->keys,
                                                    m->row_of, m->lkeys, m->lrow, m->rw, m->err, validate ? 1 : 0,
-                                                   m->gpart, st));
-  if (m->extra)
+                                                   m->gpart, st, m->extra ? nullptr : done));
+  if (m->extra) {
     TIMED_ON(m, ASGD_K_DENSE_FWD, st, launch_dense_fwd(m->bf16, m->A1, m->Wh(), m->bh(), B, rows_pad, m->A2,
                                                        m->H1, m->H1T, m->rows_pad_max, st));
+    if (done) HIP_TRY(hipEventRecord(done, st));
+  }
   if (validate) {
     int32_t e = 0;
     HIP_TRY(hipMemcpyAsync(&e, m->err, sizeof(e), hipMemcpyDeviceToHost, st));
@@ -393,7 +397,7 @@ asgd_status run_sort(asgd_model* m, hipStream_t st, int n_keys, const int32_t** 
 // da_stream, after an event when that is another stream (the training step
 // runs it beside the backward).
 asgd_status run_forward(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int rows_pad,
-                        const LabelJob* labels, hipStream_t da_stream) {
+                        const LabelJob* labels, hipStream_t da_stream, hipEvent_t fused_done = nullptr) {
   const int B = x->n_rows;
   const int splits = fwd_splits(m, B);
   const int n_tiles = (m->L + OUT_TILE - 1) / OUT_TILE;
@@ -410,7 +414,9 @@ asgd_status run_forward(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int
   TIMED(m, ASGD_K_OUT_COMBINE, launch_out_lse_targets(m->bf16, B, s_eff, m->m_part, m->s_part, rows_pad, m->W2(),
                                                       m->b2(), m->L, m->H1, y ? &yd : nullptr, m->lse,
                                                       m->loss_rows, m->tw, m->o_part, A, fused ? dA : nullptr,
-                                                      m->stream, y && !fused && da_stream != m->stream ? m->ev_dA1 : nullptr));
+                                                      m->stream,
+                                                      fused ? fused_done
+                                                            : y && da_stream != m->stream ? m->ev_dA1 : nullptr));
   if (!y || fused) return ASGD_OK;
   // the event was completed by the lse/targets launch itself: a separate record
   // would put a marker between lse/targets and the backward on the model's
@@ -686,9 +692,8 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
       HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_fork, 0));
     }
     m->pipe = false;
-    s = run_gather(m, x, y, m->aux, &rows_pad);
+    s = run_gather(m, x, y, m->aux, &rows_pad, m->ev_fork);
     if (s) return s;
-    HIP_TRY(hipEventRecord(m->ev_fork, m->aux));
     HIP_TRY(hipStreamWaitEvent(m->stream, m->ev_fork, 0));
     s = run_sort(m, m->aux, x->nnz, &sk, &sv);
     if (s) return s;
@@ -701,25 +706,28 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
     // The gather and the output layer's forward, and with it dA1, on the
     // model's stream; the feature sort on the internal stream beside them,
     // and the sparse update beside the backward.
-    s = run_gather(m, x, y, m->stream, &rows_pad);
+    // (the events are completed by the launches themselves: a separate record
+    // would put a marker, and a gap, into the model's stream)
+    s = run_gather(m, x, y, m->stream, &rows_pad, m->ev_fork);
     if (s) return s;
-    HIP_TRY(hipEventRecord(m->ev_fork, m->stream));
     HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_fork, 0));
     s = run_sort(m, m->aux, x->nnz, &sk, &sv);
     if (s) return s;
+    // dA1's event: completed by the fused lse/targets + dA1 launch, or recorded
+    // after the stored-logits path or the second layer's backward
+    const bool dA1_by_launch = !m->unfused && !m->extra;
     s = m->unfused ? run_forward_unfused(m, x, y, rows_pad, &labels)
-                   : run_forward(m, x, y, rows_pad, &labels, m->stream);
+                   : run_forward(m, x, y, rows_pad, &labels, m->stream, dA1_by_launch ? m->ev_dA1 : nullptr);
     if (s) return s;
     if (m->extra)
       TIMED(m, ASGD_K_DENSE_BWD, launch_dense_bwd(m->dA2, m->A1, m->Wh(), m->bh(), B, rows_pad, lr, m->dA1,
                                                   m->stream));
-    HIP_TRY(hipEventRecord(m->ev_dA1, m->stream));
+    if (!dA1_by_launch) HIP_TRY(hipEventRecord(m->ev_dA1, m->stream));
     HIP_TRY(hipStreamWaitEvent(m->aux, m->ev_dA1, 0));
   }
   TIMED_ON(m, ASGD_K_W1_UPDATE, m->aux,
            launch_sparse_update(m->W1(), m->F, sk, sv, x->nnz, m->row_of, xd, m->dA1, lr, B, m->b1(),
-                                m->loss_rows, m->loss, m->w1_part, m->aux));
-  HIP_TRY(hipEventRecord(m->ev_join, m->aux));
+                                m->loss_rows, m->loss, m->w1_part, m->aux, m->ev_join));
   TIMED(m, ASGD_K_OUT_BWD, launch_out_bwd(m->bf16, m->W2(), m->b2(), m->L, m->H1, m->H1T, m->rows_pad_max, B,
                          m->lse, m->rw, m->lbeg, m->lpair, lr, m->n_cu, m->stream));
   HIP_TRY(hipStreamWaitEvent(m->stream, m->ev_join, 0));

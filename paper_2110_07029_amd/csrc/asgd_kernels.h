@@ -37,7 +37,9 @@ hipError_t launch_gather_fwd(bool use_bf16, const CsrDev& x, const CsrDev* y, co
                              const float* b1, int F, int L, float* A1, void* H1, void* H1T,
                              int rows_pad, int ld_t, int32_t* keys, int32_t* row_of,
                              int32_t* lkeys, int32_t* lrow, float* rw, int32_t* err, int validate,
-                             float* gpart, hipStream_t st);
+                             float* gpart, hipStream_t st, hipEvent_t done = nullptr);
+// (done: completed by the launcher's last kernel when it has finished, with no
+// marker of its own on the stream)
 
 // ---- stable LSD radix sort of (key, position) -----------------------------
 constexpr int SORT_CHUNK = 1024;   // keys per workgroup
@@ -106,7 +108,8 @@ hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, const void
 int sparse_windows(int n_keys);
 hipError_t launch_sparse_update(float* W1, int F, const int32_t* skeys, const int32_t* svals, int n_keys,
                                 const int32_t* row_of, const CsrDev& x, const float* dA1, float lr, int B,
-                                float* b1, const float* loss_rows, float* loss, float* part, hipStream_t st);
+                                float* b1, const float* loss_rows, float* loss, float* part, hipStream_t st,
+                                hipEvent_t done = nullptr);  // done: as for launch_gather_fwd
 // Distinct sorted feature ids (compaction of segment heads); count to *count_dev.
 hipError_t launch_touched(const int32_t* skeys, int n_keys, int F, int32_t* ids, int32_t* count_dev,
                           hipStream_t st);

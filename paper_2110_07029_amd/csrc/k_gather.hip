@@ -1,6 +1,8 @@
 // First layer: CSR batch times W1 as coalesced row gathers (sparse input layer
 // of the paper's MLP, Sec. 5.1), plus the per-entry sort keys used by the
 // backward pass and the model initialisation.
+#include <hip/hip_ext.h>
+
 #include "asgd_dev.h"
 #include "asgd_kernels.h"
 
@@ -234,29 +236,41 @@ hipError_t launch_gather_fwd(bool use_bf16, const CsrDev& x, const CsrDev* y, co
                              const float* b1, int F, int L, float* A1, void* H1, void* H1T,
                              int rows_pad, int ld_t, int32_t* keys, int32_t* row_of,
                              int32_t* lkeys, int32_t* lrow, float* rw, int32_t* err, int validate,
-                             float* gpart, hipStream_t st) {
+                             float* gpart, hipStream_t st, hipEvent_t done) {
   CsrDev yy = y ? *y : CsrDev{0, 0, 0, nullptr, nullptr, nullptr};
   const bool split = gpart && x.n_rows > 0 && (int64_t)x.nnz >= (int64_t)GATHER_LONG_ROW * x.n_rows;
-  auto go = [&](auto kern, int pieces, auto* h1, auto* h1t) {
-    const dim3 block(64 * gather_waves(pieces));
-    hipLaunchKernelGGL(kern, dim3(rows_pad * pieces), block, 0, st, x, yy, y != nullptr, W1, b1, F, L, A1, h1,
-                       h1t, rows_pad, ld_t, keys, row_of, lkeys, lrow, rw, err, validate, gpart);
+  // the last launch completes `done`
+  auto go = [&](auto kern, int pieces, auto* h1, auto* h1t, hipEvent_t ev) {
+    const dim3 grid(rows_pad * pieces), block(64 * gather_waves(pieces));
+    const int has_y = y != nullptr;
+    if (ev)
+      hipExtLaunchKernelGGL(kern, grid, block, 0, st, nullptr, ev, 0, x, yy, has_y, W1, b1, F, L, A1, h1, h1t,
+                            rows_pad, ld_t, keys, row_of, lkeys, lrow, rw, err, validate, gpart);
+    else
+      hipLaunchKernelGGL(kern, grid, block, 0, st, x, yy, has_y, W1, b1, F, L, A1, h1, h1t, rows_pad, ld_t, keys,
+                         row_of, lkeys, lrow, rw, err, validate, gpart);
+  };
+  auto finish = [&](auto kern, auto* h1, auto* h1t) {
+    if (done)
+      hipExtLaunchKernelGGL(kern, dim3(x.n_rows), dim3(64), 0, st, nullptr, done, 0, x.n_rows,
+                            (const float*)gpart, ld_t, b1, A1, h1, h1t);
+    else
+      hipLaunchKernelGGL(kern, dim3(x.n_rows), dim3(64), 0, st, x.n_rows, (const float*)gpart, ld_t, b1, A1, h1,
+                         h1t);
   };
   if (use_bf16) {
     if (split) {
-      go(k_gather_fwd<true, GATHER_SPLIT>, GATHER_SPLIT, (bf16*)H1, (bf16*)H1T);
-      hipLaunchKernelGGL(k_gather_finish<true>, dim3(x.n_rows), dim3(64), 0, st, x.n_rows, gpart, ld_t, b1, A1,
-                         (bf16*)H1, (bf16*)H1T);
+      go(k_gather_fwd<true, GATHER_SPLIT>, GATHER_SPLIT, (bf16*)H1, (bf16*)H1T, nullptr);
+      finish(k_gather_finish<true>, (bf16*)H1, (bf16*)H1T);
     } else {
-      go(k_gather_fwd<true, 1>, 1, (bf16*)H1, (bf16*)H1T);
+      go(k_gather_fwd<true, 1>, 1, (bf16*)H1, (bf16*)H1T, done);
     }
   } else {
     if (split) {
-      go(k_gather_fwd<false, GATHER_SPLIT>, GATHER_SPLIT, (float*)H1, (float*)H1T);
-      hipLaunchKernelGGL(k_gather_finish<false>, dim3(x.n_rows), dim3(64), 0, st, x.n_rows, gpart, ld_t, b1,
-                         A1, (float*)H1, (float*)H1T);
+      go(k_gather_fwd<false, GATHER_SPLIT>, GATHER_SPLIT, (float*)H1, (float*)H1T, nullptr);
+      finish(k_gather_finish<false>, (float*)H1, (float*)H1T);
     } else {
-      go(k_gather_fwd<false, 1>, 1, (float*)H1, (float*)H1T);
+      go(k_gather_fwd<false, 1>, 1, (float*)H1, (float*)H1T, done);
     }
   }
   return hipGetLastError();

@@ -7,6 +7,8 @@
 // no atomics.
 #include <limits.h>
 
+#include <hip/hip_ext.h>
+
 #include "asgd_dev.h"
 #include "asgd_kernels.h"
 
@@ -200,13 +202,26 @@ __global__ __launch_bounds__(SPU_THREADS) void k_sparse_join(float* __restrict__
 
 hipError_t launch_sparse_update(float* W1, int F, const int32_t* skeys, const int32_t* svals, int n_keys,
                                 const int32_t* row_of, const CsrDev& x, const float* dA1, float lr, int B,
-                                float* b1, const float* loss_rows, float* loss, float* part, hipStream_t st) {
+                                float* b1, const float* loss_rows, float* loss, float* part, hipStream_t st,
+                                hipEvent_t done) {
   const int nwin = n_keys > 0 ? sparse_windows(n_keys) : 0;
   const int nwb = (nwin + SPU_WAVES - 1) / SPU_WAVES;
-  hipLaunchKernelGGL(k_sparse_pieces, dim3(nwb + 1), dim3(SPU_THREADS), 0, st, W1, F, skeys, svals, n_keys,
-                     row_of, x, dA1, lr, B, b1, loss_rows, loss, part, nwb);
-  if (nwin > 1)
-    hipLaunchKernelGGL(k_sparse_join, dim3(nwb), dim3(SPU_THREADS), 0, st, W1, F, skeys, n_keys, lr, part);
+  // the last launch completes `done`
+  const bool join = nwin > 1;
+  const dim3 gp(nwb + 1), gj(nwb), blk(SPU_THREADS);
+  if (done && !join)
+    hipExtLaunchKernelGGL(k_sparse_pieces, gp, blk, 0, st, nullptr, done, 0, W1, F, skeys, svals, n_keys, row_of, x,
+                          dA1, lr, B, b1, loss_rows, loss, part, nwb);
+  else
+    hipLaunchKernelGGL(k_sparse_pieces, gp, blk, 0, st, W1, F, skeys, svals, n_keys, row_of, x, dA1, lr, B, b1,
+                       loss_rows, loss, part, nwb);
+  if (join) {
+    if (done)
+      hipExtLaunchKernelGGL(k_sparse_join, gj, blk, 0, st, nullptr, done, 0, W1, F, skeys, n_keys, lr,
+                            (const float*)part);
+    else
+      hipLaunchKernelGGL(k_sparse_join, gj, blk, 0, st, W1, F, skeys, n_keys, lr, (const float*)part);
+  }
   return hipGetLastError();
 }
 
