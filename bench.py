@@ -39,20 +39,20 @@ FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 PMC_TRAFFIC = {
     ("wide-label", 256, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="746408ca1d9a519893b3a6a20d3893dd2088ef9f2c29093fe946c5cff8b9065c",
-        fetch_kib=169817.6, write_kib=337663.1),
+        sha256="950488db17412a5398fee1d439ce7bab0ac0eef878111ef628e0d1f0a85acf3c",
+        fetch_kib=169828.2, write_kib=337663.1),
     ("wide-label", 1024, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="746408ca1d9a519893b3a6a20d3893dd2088ef9f2c29093fe946c5cff8b9065c",
-        fetch_kib=176687.1, write_kib=337953.0),
+        sha256="950488db17412a5398fee1d439ce7bab0ac0eef878111ef628e0d1f0a85acf3c",
+        fetch_kib=176673.9, write_kib=337960.1),
     ("wide-feature", 128, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="746408ca1d9a519893b3a6a20d3893dd2088ef9f2c29093fe946c5cff8b9065c",
-        fetch_kib=52257.2, write_kib=103524.0),
+        sha256="950488db17412a5398fee1d439ce7bab0ac0eef878111ef628e0d1f0a85acf3c",
+        fetch_kib=52260.1, write_kib=103524.0),
     ("elastic", 4, "merge"): dict(
         sources=('csrc/k_merge.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="cac912f9fbd11c0a0526c5a58b20552a4362a31425c7d79736900402ea9d3f63",
-        fetch_kib=1216912.2, write_kib=2028091.2),
+        sha256="c61e603706853e2741d94bd49b141d2580e6839ce3e10a5cfb043ac119ae774d",
+        fetch_kib=1216912.0, write_kib=2028091.2),
 }
 
 
