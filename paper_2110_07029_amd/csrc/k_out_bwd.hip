@@ -97,8 +97,9 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
     h1b = reinterpret_cast<E*>(sp);
     sp += 2 * BWD_CROWS * TW_LD * sizeof(E);
   }
-  // per row of the batch: crow = log2(1/B) - lse*log2(e) (-inf for rows past B)
-  // so that dZ = 2^(z*log2(e) + bias*log2(e) + crow) = softmax/B; tw = (1/|Y_i|)/B
+  // per row of the batch: the logits' accumulator starts at
+  // crow = (log2(1/B) - lse*log2(e)) / log2(e) (-inf for rows past B), so that
+  // dZ = 2^(z*log2(e) + bias*log2(e)) = softmax/B with one fma; tw = (1/|Y_i|)/B
   float* crow_s = reinterpret_cast<float*>(sp);
   sp += bpad * sizeof(float);
   float* tw_s = reinterpret_cast<float*>(sp);
@@ -112,7 +113,7 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
   auto stage_rows = [&](int r0, int nrows) {
     for (int i = tid; i < nrows; i += BWD_THREADS) {
       const int r = r0 + i;
-      crow_s[i] = r < B ? log2_invB - lse[r] * LOG2E : -INFINITY;
+      crow_s[i] = r < B ? (log2_invB - lse[r] * LOG2E) * LN2 : -INFINITY;
       tw_s[i] = r < B ? rw[r] * invB : 0.0f;
     }
   };
@@ -245,9 +246,13 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
     // one 32-row block of the batch (rows grow0 ..): rb indexes its rows in
     // the H1 chunk buffer hbuf and in the target mask
     auto row_block = [&](const E* hbuf, int rb, int grow0) {
+      // the accumulator starts at the row constants of rows 8*q + 4*g + (0..3)
       f32x16 z;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) z[r] = 0.0f;
+      for (int q = 0; q < 4; ++q) {
+        const float4 c4 = *reinterpret_cast<const float4*>(crow_s + grow0 + 8 * q + 4 * g);
+        z[4 * q + 0] = c4.x; z[4 * q + 1] = c4.y; z[4 * q + 2] = c4.z; z[4 * q + 3] = c4.w;
+      }
       if constexpr (LDS_H1) {
         const E* t = hbuf + rb * 32 * TW_LD;
 #pragma unroll
@@ -262,16 +267,9 @@ __global__ __launch_bounds__(BWD_THREADS) void k_out_bwd(
 #pragma unroll
           for (int c = 0; c < NCH; ++c) z = M::mma(frag_row<BF16>(hrow + 32 * kb, c, g), wf[kb][c], z);
       }
-      // rows 8*q + 4*g + (0..3) of this block: one float4 of row constants each
-      float cr[16];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float4 c4 = *reinterpret_cast<const float4*>(crow_s + grow0 + 8 * q + 4 * g);
-        cr[4 * q + 0] = c4.x; cr[4 * q + 1] = c4.y; cr[4 * q + 2] = c4.z; cr[4 * q + 3] = c4.w;
-      }
       float dz[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) dz[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, bb) + cr[r]);
+      for (int r = 0; r < 16; ++r) dz[r] = __builtin_amdgcn_exp2f(fmaf(z[r], LOG2E, bb));
       if (has_targets) {
         const uint32_t mw = mask[n * mstride + rb];
         if (__any(mw != 0u)) {
