@@ -39,16 +39,16 @@ FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 PMC_TRAFFIC = {
     ("wide-label", 256, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="950488db17412a5398fee1d439ce7bab0ac0eef878111ef628e0d1f0a85acf3c",
-        fetch_kib=169828.2, write_kib=337663.1),
+        sha256="092e28230a07e648a4a027f768d516929c228f403b495e5ba1661d34da57b7f0",
+        fetch_kib=169830.2, write_kib=337663.1),
     ("wide-label", 1024, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="950488db17412a5398fee1d439ce7bab0ac0eef878111ef628e0d1f0a85acf3c",
-        fetch_kib=176673.9, write_kib=337960.1),
+        sha256="092e28230a07e648a4a027f768d516929c228f403b495e5ba1661d34da57b7f0",
+        fetch_kib=177476.8, write_kib=337914.5),
     ("wide-feature", 128, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="950488db17412a5398fee1d439ce7bab0ac0eef878111ef628e0d1f0a85acf3c",
-        fetch_kib=52260.1, write_kib=103524.0),
+        sha256="092e28230a07e648a4a027f768d516929c228f403b495e5ba1661d34da57b7f0",
+        fetch_kib=52260.3, write_kib=103524.0),
     ("elastic", 4, "merge"): dict(
         sources=('csrc/k_merge.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
         sha256="c61e603706853e2741d94bd49b141d2580e6839ce3e10a5cfb043ac119ae774d",
