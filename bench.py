@@ -39,19 +39,19 @@ FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 PMC_TRAFFIC = {
     ("wide-label", 256, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="092e28230a07e648a4a027f768d516929c228f403b495e5ba1661d34da57b7f0",
-        fetch_kib=169830.2, write_kib=337663.1),
+        sha256="bd515fcc493667e9f5aed09b57095f2055fc1c03542cdaac00d2cd86aa7de0a9",
+        fetch_kib=169819.5, write_kib=337663.1),
     ("wide-label", 1024, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="092e28230a07e648a4a027f768d516929c228f403b495e5ba1661d34da57b7f0",
-        fetch_kib=177476.8, write_kib=337914.5),
+        sha256="bd515fcc493667e9f5aed09b57095f2055fc1c03542cdaac00d2cd86aa7de0a9",
+        fetch_kib=177337.2, write_kib=337920.8),
     ("wide-feature", 128, "out_bwd"): dict(
         sources=('csrc/k_out_bwd.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="092e28230a07e648a4a027f768d516929c228f403b495e5ba1661d34da57b7f0",
-        fetch_kib=52260.3, write_kib=103524.0),
+        sha256="bd515fcc493667e9f5aed09b57095f2055fc1c03542cdaac00d2cd86aa7de0a9",
+        fetch_kib=52256.6, write_kib=103524.0),
     ("elastic", 4, "merge"): dict(
         sources=('csrc/k_merge.hip', 'csrc/asgd_dev.h', 'csrc/asgd_kernels.h'),
-        sha256="c61e603706853e2741d94bd49b141d2580e6839ce3e10a5cfb043ac119ae774d",
+        sha256="76e8aa214af20f11e78470a2185c4c56fa9aadc98d47c7ddc7b4e6ab63479ba6",
         fetch_kib=1216912.0, write_kib=2028091.2),
 }
 

@@ -342,6 +342,36 @@ hipEvent_t timer_start(asgd_model* m, int k, hipStream_t st, hipEvent_t* stop) {
   } while (0)
 #define TIMED(m, k, expr) TIMED_ON(m, k, (m)->stream, expr)
 
+// Start and stop events of the next timed launch of group k for a launcher
+// that attaches them to its kernel's launch (completed at the kernel's own
+// start and end, with no markers around it); nullptr when not timing.
+void timer_pair(asgd_model* m, int k, hipEvent_t* t0, hipEvent_t* t1) {
+  *t0 = *t1 = nullptr;
+  if (!m->timing || m->tused[k] >= asgd_model::kTimerPool) return;
+  std::vector<hipEvent_t>& v = m->tev[k];
+  const int i = m->tused[k];
+  if ((int)v.size() < 2 * (i + 1)) {
+    hipEvent_t a = nullptr, b = nullptr;
+    if (hipEventCreate(&a) != hipSuccess) return;
+    if (hipEventCreate(&b) != hipSuccess) {
+      (void)hipEventDestroy(a);
+      return;
+    }
+    v.push_back(a);
+    v.push_back(b);
+  }
+  ++m->tused[k];
+  *t0 = v[2 * i];
+  *t1 = v[2 * i + 1];
+}
+// expr names the events t0_ and t1_
+#define TIMED_LAUNCH(m, k, expr)               \
+  do {                                         \
+    hipEvent_t t0_ = nullptr, t1_ = nullptr;   \
+    timer_pair((m), (k), &t0_, &t1_);          \
+    HIP_TRY(expr);                             \
+  } while (0)
+
 // Gather forward (+ keys) on stream st into the next copy of H1 / H1T / rw,
 // optional validation check.  Leaves H1 / A1 ready.
 // done (optional): an event completed once the gather's work has finished on st
@@ -404,8 +434,9 @@ asgd_status run_forward(asgd_model* m, const asgd_csr* x, const asgd_csr* y, int
   const int tps = (n_tiles + splits - 1) / splits;
   const int s_eff = (n_tiles + tps - 1) / tps;
   if ((int64_t)s_eff * rows_pad > m->part_rows) return fail(ASGD_ERANGE, "partial buffer too small");
-  TIMED(m, ASGD_K_OUT_FWD, launch_out_fwd_train(m->bf16, m->W2(), m->b2(), m->L, m->H1, B, splits, m->m_part,
-                               m->s_part, m->o_part, rows_pad, labels, &m->label_plan, m->stream));
+  TIMED_LAUNCH(m, ASGD_K_OUT_FWD,
+               launch_out_fwd_train(m->bf16, m->W2(), m->b2(), m->L, m->H1, B, splits, m->m_part, m->s_part,
+                                    m->o_part, rows_pad, labels, &m->label_plan, m->stream, t0_, t1_));
   CsrDev yd = y ? dev(y) : CsrDev{};
   float* const A = m->extra ? m->A2 : m->A1;
   float* const dA = m->extra ? m->dA2 : m->dA1;
@@ -728,8 +759,9 @@ asgd_status asgd_train_step(asgd_model* m, const asgd_csr* x, const asgd_csr* y,
   TIMED_ON(m, ASGD_K_W1_UPDATE, m->aux,
            launch_sparse_update(m->W1(), m->F, sk, sv, x->nnz, m->row_of, xd, m->dA1, lr, B, m->b1(),
                                 m->loss_rows, m->loss, m->w1_part, m->aux, m->ev_join));
-  TIMED(m, ASGD_K_OUT_BWD, launch_out_bwd(m->bf16, m->W2(), m->b2(), m->L, m->H1, m->H1T, m->rows_pad_max, B,
-                         m->lse, m->rw, m->lbeg, m->lpair, lr, m->n_cu, m->stream));
+  TIMED_LAUNCH(m, ASGD_K_OUT_BWD,
+               launch_out_bwd(m->bf16, m->W2(), m->b2(), m->L, m->H1, m->H1T, m->rows_pad_max, B, m->lse, m->rw,
+                              m->lbeg, m->lpair, lr, m->n_cu, m->stream, t0_, t1_));
   HIP_TRY(hipStreamWaitEvent(m->stream, m->ev_join, 0));
   m->pipe = m->gather_aux;
   if (loss_out) return asgd_model_last_loss(m, loss_out);

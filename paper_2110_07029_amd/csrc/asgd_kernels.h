@@ -81,7 +81,10 @@ int out_rows_per_block(bool use_bf16);
 // label_job_plan).
 hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2, int L, const void* H1,
                                 int B, int splits, float* m_part, float* s_part, float* o_part,
-                                int ld_part, const LabelJob* job, const LabelJobPlan* plan, hipStream_t st);
+                                int ld_part, const LabelJob* job, const LabelJobPlan* plan, hipStream_t st,
+                                hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
+// (t0, t1: optional events that the launch itself completes at the kernel's
+// start and end, for timing the kernel alone)
 // Per row, after the forward: lse, and with y the loss and tw = mean_{y in Y_i} W2[y]
 // [B x 128] (reads W2 before the backward updates it).
 // With y and dA1 (non-null), the same launch also forms dA1 = ((O/s - tw) / B) * [A1 > 0]
@@ -100,7 +103,8 @@ hipError_t launch_out_dA1(int B, int splits, const float* m_part, const float* s
 hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, const void* H1,
                           const void* H1T, int ld_t, int B, const float* lse, const float* rw,
                           const int32_t* lbeg, const int32_t* lpair, float lr, int n_cu,
-                          hipStream_t st);
+                          hipStream_t st, hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
+// (t0, t1 as for launch_out_fwd_train)
 // W1[f] -= lr * sum_{entries of f} x * dA1[row], one segment per distinct f
 // (keys sorted by feature, invalid ids >= F last); and, in the same launch,
 // db1 = sum_i dA1[i]; b1 -= lr db1; loss = mean_i loss_rows[i].

@@ -26,6 +26,7 @@
 //           buffer (global_load_lds, no registers in between);
 //   k_out_bwd, global (fp32 operands): H1 and H1^T read from their
 //           L2-resident global copies.
+#include <hip/hip_ext.h>
 #include <math.h>
 
 #include <type_traits>
@@ -693,8 +694,8 @@ __global__ __launch_bounds__(BWP_THREADS) void k_out_bwd_prefetch(
 }
 
 template <bool BF16, int MODE, int RS>
-static hipError_t launch_bwd(int grid, size_t shm, hipStream_t st, float* W2, float* b2, int L,
-                             const void* H1, const void* H1T, int ld_t, int B, const float* lse,
+static hipError_t launch_bwd(int grid, size_t shm, hipStream_t st, hipEvent_t t0, hipEvent_t t1, float* W2,
+                             float* b2, int L, const void* H1, const void* H1T, int ld_t, int B, const float* lse,
                              const float* rw, const int32_t* lbeg, const int32_t* lpair, float lr,
                              float invB) {
   using E = typename Mma<BF16>::elem;
@@ -706,15 +707,15 @@ static hipError_t launch_bwd(int grid, size_t shm, hipStream_t st, float* W2, fl
     if (e != hipSuccess) return e;
     attr_done = true;
   }
-  hipLaunchKernelGGL((k_out_bwd<BF16, MODE, RS>), dim3(grid), dim3(BWD_THREADS), shm, st, W2, b2, L,
-                     (const E*)H1, (const E*)H1T, ld_t, B, lse, rw, lbeg, lpair, lr, invB, log2_invB);
+  hipExtLaunchKernelGGL((k_out_bwd<BF16, MODE, RS>), dim3(grid), dim3(BWD_THREADS), shm, st, t0, t1, 0, W2, b2,
+                        L, (const E*)H1, (const E*)H1T, ld_t, B, lse, rw, lbeg, lpair, lr, invB, log2_invB);
   return hipGetLastError();
 }
 
 hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, const void* H1,
                           const void* H1T, int ld_t, int B, const float* lse, const float* rw,
                           const int32_t* lbeg, const int32_t* lpair, float lr, int n_cu,
-                          hipStream_t st) {
+                          hipStream_t st, hipEvent_t t0, hipEvent_t t1) {
   const int nrb = (B + 31) / 32;
   const int mode = !use_bf16 ? BWD_GLOBAL : (B <= BWD_CHUNK ? BWD_STAGED : BWD_CHUNKED);
   const int bpad = nrb * 32;
@@ -743,12 +744,12 @@ hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, const void
                        (size_t)BWP_WAVES * 32 * BWP_SLD * sizeof(float);
     int gp = (n_blocks + BWP_WAVES - 1) / BWP_WAVES;
     if (gp > n_cu) gp = n_cu;
-    hipLaunchKernelGGL(k_out_bwd_prefetch, dim3(gp), dim3(BWP_THREADS), shp, st, W2, b2, L,
-                       (const bf16*)H1, B, lse, rw, lbeg, lpair, lr, invB, (float)log2((double)invB));
+    hipExtLaunchKernelGGL(k_out_bwd_prefetch, dim3(gp), dim3(BWP_THREADS), shp, st, t0, t1, 0, W2, b2, L,
+                          (const bf16*)H1, B, lse, rw, lbeg, lpair, lr, invB, (float)log2((double)invB));
     return hipGetLastError();
   }
   if (mode == BWD_CHUNKED)
-    return launch_bwd<true, BWD_CHUNKED, 1>(grid, shm, st, W2, b2, L, H1, H1T, ld_t, B, lse, rw, lbeg,
+    return launch_bwd<true, BWD_CHUNKED, 1>(grid, shm, st, t0, t1, W2, b2, L, H1, H1T, ld_t, B, lse, rw, lbeg,
                                             lpair, lr, invB);
   // fp32 operands with few label blocks: 4 wavefronts share a block's rows
   // (every wave would otherwise own a block and most of the GPU would idle)
@@ -756,10 +757,10 @@ hipError_t launch_out_bwd(bool use_bf16, float* W2, float* b2, int L, const void
   if (n_blocks < n_cu * BWD_WAVES / RS && B <= 512) {
     const int units = (n_blocks + BWD_WAVES / RS - 1) / (BWD_WAVES / RS);
     const size_t shr = shm + (size_t)(BWD_WAVES / RS) * (RS - 1) * 65 * 64 * sizeof(float);
-    return launch_bwd<false, BWD_GLOBAL, RS>(units < 2 * n_cu ? units : 2 * n_cu, shr, st, W2, b2, L, H1, H1T,
-                                             ld_t, B, lse, rw, lbeg, lpair, lr, invB);
+    return launch_bwd<false, BWD_GLOBAL, RS>(units < 2 * n_cu ? units : 2 * n_cu, shr, st, t0, t1, W2, b2, L,
+                                             H1, H1T, ld_t, B, lse, rw, lbeg, lpair, lr, invB);
   }
-  return launch_bwd<false, BWD_GLOBAL, 1>(grid, shm, st, W2, b2, L, H1, H1T, ld_t, B, lse, rw, lbeg,
+  return launch_bwd<false, BWD_GLOBAL, 1>(grid, shm, st, t0, t1, W2, b2, L, H1, H1T, ld_t, B, lse, rw, lbeg,
                                           lpair, lr, invB);
 }
 

@@ -297,7 +297,8 @@ LabelJobPlan label_job_plan(bool use_bf16, int L) {
 
 hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2, int L, const void* H1,
                                 int B, int splits, float* m_part, float* s_part, float* o_part,
-                                int ld_part, const LabelJob* job, const LabelJobPlan* plan, hipStream_t st) {
+                                int ld_part, const LabelJob* job, const LabelJobPlan* plan, hipStream_t st,
+                                hipEvent_t t0, hipEvent_t t1) {
   const int n_tiles = (L + OUT_TILE - 1) / OUT_TILE;
   const int tps = (n_tiles + splits - 1) / splits;
   const int s_eff = (n_tiles + tps - 1) / tps;
@@ -314,11 +315,11 @@ hipError_t launch_out_fwd_train(bool use_bf16, const float* W2, const float* b2,
   }
   const dim3 grid(n_fwd + n_job), block(FWD_THREADS);
   if (use_bf16)
-    hipLaunchKernelGGL(k_out_fwd_train<true>, grid, block, lds, st, W2, b2, L, (const bf16*)H1, B, tps,
-                       n_tiles, m_part, s_part, o_part, ld_part, s_eff, n_fwd, lj);
+    hipExtLaunchKernelGGL(k_out_fwd_train<true>, grid, block, lds, st, t0, t1, 0, W2, b2, L, (const bf16*)H1, B,
+                          tps, n_tiles, m_part, s_part, o_part, ld_part, s_eff, n_fwd, lj);
   else
-    hipLaunchKernelGGL(k_out_fwd_train<false>, grid, block, lds, st, W2, b2, L, (const float*)H1, B, tps,
-                       n_tiles, m_part, s_part, o_part, ld_part, s_eff, n_fwd, lj);
+    hipExtLaunchKernelGGL(k_out_fwd_train<false>, grid, block, lds, st, t0, t1, 0, W2, b2, L, (const float*)H1,
+                          B, tps, n_tiles, m_part, s_part, o_part, ld_part, s_eff, n_fwd, lj);
   return hipGetLastError();
 }
 
