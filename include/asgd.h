@@ -404,10 +404,14 @@ enum {
   ASGD_K_COUNT = 14
 };
 
-/* enable != 0: from now on, bracket each kernel group launched for this model
+/* enable != 0: from now on, time each kernel group launched for this model
  * with a pair of HIP events (up to 1024 launches per group are recorded
- * between two reads; later launches of that group run untimed).  enable == 0
- * stops recording.  Timing adds two event records per group launch. */
+ * between two reads; later launches of that group run untimed).  The output
+ * layer's forward and backward (ASGD_K_OUT_FWD, ASGD_K_OUT_BWD) pass the pair
+ * to their launch, which completes them at the kernel's own start and end;
+ * the other groups record them on their stream before and after their
+ * launches, so their durations also count the dispatch.  enable == 0 stops
+ * recording. */
 asgd_status asgd_model_set_timing(asgd_model* m, int32_t enable);
 
 /* Sum of the event-measured durations (ms) and the number of timed launches
